@@ -1,0 +1,177 @@
+"""Pins of the oracle's permute / GEMM / SwiGLU / unpermute steps (CPU only).
+
+Independent references: pure-Python loops on tiny inputs (routing, GEMM
+elements via math.fsum, unpermute), torch autograd and torch's SiLU for the
+SwiGLU forward and backward, algebraic identities (transposing a 128x128-block
+scaled weight is exact, so dgrad equals fprop against the transposed weight;
+wgrad of all experts together is one product over the concatenated rows).
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.codec import e4m3_decode
+from oracle.quant import quant_rowwise, quant_block128, dequant_rowwise, TILE
+from oracle import moe
+
+
+def _routing(T, k, E, seed, drop=0.0):
+    rng = np.random.default_rng(seed)
+    idx = np.stack([rng.permutation(E)[:k] for _ in range(T)])
+    if drop:
+        idx[rng.random((T, k)) < drop] = -1
+    return idx
+
+
+def test_route_brute_force():
+    for (T, k, E, seed, drop) in [(37, 2, 5, 0, 0.0), (300, 4, 6, 1, 0.1), (5, 1, 9, 2, 0.0)]:
+        idx = _routing(T, k, E, seed, drop)
+        counts, offsets, row_map, src_row = moe.route(idx, E)
+        # pure-Python reference: walk experts in order, tokens ascending
+        row = 0
+        ref_map = {}
+        ref_off = [0]
+        for e in range(E):
+            start = row
+            for t in range(T):
+                for j in range(k):
+                    if idx[t, j] == e:
+                        ref_map[(t, j)] = row
+                        row += 1
+            n = row - start
+            row = start + ((n + 127) // 128) * 128
+            ref_off.append(row)
+        assert offsets.tolist() == ref_off
+        for t in range(T):
+            for j in range(k):
+                assert row_map[t, j] == ref_map.get((t, j), -1)
+        real = src_row >= 0
+        assert real.sum() == sum(1 for v in idx.ravel() if v >= 0)
+        assert np.array_equal(np.sort(src_row[real]), np.sort(np.nonzero(idx.ravel() >= 0)[0]))
+        assert all(o % 128 == 0 for o in ref_off)
+        assert offsets[-1] <= moe.rows_bound(T, k, E)
+        assert np.array_equal(counts, np.bincount(idx[idx >= 0].ravel(), minlength=E))
+
+
+def test_route_zero_token_experts():
+    idx = np.array([[0, 3], [3, 0], [0, 3]])
+    counts, offsets, row_map, src_row = moe.route(idx, 5)
+    assert counts.tolist() == [3, 0, 0, 3, 0]
+    assert offsets.tolist() == [0, 128, 128, 128, 256, 256]
+    assert row_map.tolist() == [[0, 128], [129, 1], [2, 130]]
+
+
+def test_permute_quant_rows_loop():
+    T, k, E, H = 40, 3, 4, 256
+    idx = _routing(T, k, E, 3, drop=0.05)
+    rng = np.random.default_rng(0)
+    x = torch.from_numpy(rng.standard_normal((T, H))).to(torch.bfloat16).float().numpy()
+    w = rng.random((T, k)).astype(np.float32)
+    _, offsets, row_map, src_row = moe.route(idx, E)
+    for row_w in (None, w):
+        q, s = moe.permute_quant_rows(x, src_row, k, row_w)
+        assert q.shape == (offsets[-1], H)
+        for r in range(offsets[-1]):
+            if src_row[r] < 0:
+                assert np.all(q[r] == 0) and np.all(s[r] == np.float32(2.0 ** -126))
+                continue
+            t, j = divmod(int(src_row[r]), k)
+            v = x[t] if row_w is None else np.float32(w[t, j]) * x[t]
+            qr, sr = quant_rowwise(v[None, :].astype(np.float32))
+            assert np.array_equal(q[r], qr[0]) and np.array_equal(s[r], sr[0])
+            assert row_map[t, j] == r
+
+
+def _quant_expert_weights(E, N, K, seed):
+    rng = np.random.default_rng(seed)
+    w = rng.standard_normal((E, N, K)) * 0.02
+    qs = [quant_block128(w[e]) for e in range(E)]
+    return np.stack([q for q, _ in qs]), np.stack([s for _, s in qs])
+
+
+def _dec_block(q, s):
+    return e4m3_decode(q) * np.repeat(np.repeat(s.astype(np.float64), TILE, 0), TILE, 1)
+
+
+def test_gemms_brute_force_elements():
+    E, N, K = 3, 256, 384
+    offsets = np.array([0, 128, 128, 384])   # expert 1 has no rows
+    rng = np.random.default_rng(1)
+    a = rng.standard_normal((offsets[-1], K))
+    aq, as_ = quant_rowwise(a)
+    wq, ws = _quant_expert_weights(E, N, K, 2)
+    out = moe.grouped_gemm_fprop(aq, as_, wq, ws, offsets)
+    A = e4m3_decode(aq) * np.repeat(as_.astype(np.float64), TILE, 1)
+    for (m, n) in [(0, 0), (127, 255), (128, 17), (383, 100), (200, 128)]:
+        e = 0 if m < 128 else 2
+        W = _dec_block(wq[e], ws[e])
+        assert out[m, n] == pytest.approx(math.fsum(A[m, kk] * W[n, kk] for kk in range(K)), rel=1e-13, abs=1e-300)
+    # dgrad: out[m, k] = sum_n G[m, n] W_e[n, k]
+    g = rng.standard_normal((offsets[-1], N))
+    gq, gs = quant_rowwise(g)
+    dg = moe.grouped_gemm_dgrad(gq, gs, wq, ws, offsets)
+    G = e4m3_decode(gq) * np.repeat(gs.astype(np.float64), TILE, 1)
+    for (m, kk) in [(0, 0), (127, 383), (300, 5)]:
+        e = 0 if m < 128 else 2
+        W = _dec_block(wq[e], ws[e])
+        assert dg[m, kk] == pytest.approx(math.fsum(G[m, n] * W[n, kk] for n in range(N)), rel=1e-13, abs=1e-300)
+    # dgrad == fprop against the transposed weight (transpose of a 128x128-block scaled tensor is exact)
+    wqT = np.ascontiguousarray(np.transpose(wq, (0, 2, 1)))
+    wsT = np.ascontiguousarray(np.transpose(ws, (0, 2, 1)))
+    assert np.allclose(dg, moe.grouped_gemm_fprop(gq, gs, wqT, wsT, offsets), rtol=1e-12, atol=1e-14)
+
+
+def test_wgrad_brute_force_and_zero_expert():
+    N, K = 256, 128
+    offsets = np.array([0, 256, 256, 384])
+    rng = np.random.default_rng(5)
+    gT = rng.standard_normal((N, 384))
+    xT = rng.standard_normal((K, 384))
+    gq, gs = quant_rowwise(gT)
+    xq, xs = quant_rowwise(xT)
+    dw = moe.grouped_gemm_wgrad(gq, gs, xq, xs, offsets)
+    assert dw.shape == (3, N, K)
+    assert np.all(dw[1] == 0)
+    GT = dequant_rowwise(gq, gs)
+    XT = dequant_rowwise(xq, xs)
+    for (e, n, kk) in [(0, 0, 0), (0, 255, 127), (2, 3, 64)]:
+        r0, r1 = offsets[e], offsets[e + 1]
+        assert dw[e, n, kk] == pytest.approx(math.fsum(GT[n, m] * XT[kk, m] for m in range(r0, r1)), rel=1e-13)
+    # all experts together: sum_e dW[e] = GT @ XT^T
+    assert np.allclose(dw.sum(axis=0), GT @ XT.T, rtol=1e-12, atol=1e-12)
+
+
+def test_swiglu_vs_torch_autograd():
+    rng = np.random.default_rng(6)
+    a = rng.standard_normal((16, 256)) * 3.0
+    dh = rng.standard_normal((16, 128))
+    at = torch.from_numpy(a).requires_grad_(True)
+    h = torch.nn.functional.silu(at[:, :128]) * at[:, 128:]
+    h.backward(torch.from_numpy(dh))
+    assert np.allclose(moe.swiglu(a), h.detach().numpy(), rtol=1e-14, atol=1e-14)
+    assert np.allclose(moe.swiglu_bwd(a, dh), at.grad.numpy(), rtol=1e-12, atol=1e-13)
+    hq, hs = moe.swiglu_quant(a)
+    q2, s2 = quant_rowwise(h.detach().numpy())
+    assert np.array_equal(hq, q2) and np.array_equal(hs, s2)
+
+
+def test_unpermute_loop_and_gather():
+    T, k, E, H = 30, 3, 5, 128
+    idx = _routing(T, k, E, 8, drop=0.1)
+    _, offsets, row_map, _ = moe.route(idx, E)
+    rng = np.random.default_rng(2)
+    yp = torch.from_numpy(rng.standard_normal((offsets[-1], H))).to(torch.bfloat16).double().numpy()
+    w = rng.random((T, k)).astype(np.float32)
+    y = moe.unpermute(yp, row_map, w)
+    for t in range(T):
+        for hh in (0, 77, 127):
+            acc = math.fsum(float(w[t, j]) * yp[row_map[t, j], hh] for j in range(k) if row_map[t, j] >= 0)
+            assert abs(y[t, hh] - acc) <= abs(acc) * 2.0 ** -8
+    # k = 1 with unit weight is a pure gather (exact)
+    idx1 = _routing(T, 1, E, 9)
+    _, off1, rm1, _ = moe.route(idx1, E)
+    yp1 = torch.from_numpy(rng.standard_normal((off1[-1], H))).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(moe.unpermute(yp1, rm1, None), yp1[rm1[:, 0]])
