@@ -1,0 +1,304 @@
+"""Benchmark of the FP8-Flow-MoE expert layer on one MI355X.
+
+One step = one pass of the whole hot path: 128x128 weight quantization (F0), the
+forward (F1 permute+quant, F2 fc1 fprop, F3 SwiGLU+quant, F4 fc2 fprop, F5 unpermute)
+and the backward (B1 dY permute+quant, B2 fc2 dgrad, B3 SwiGLU backward+quant, B4 fc1
+dgrad, B5 unpermute, B6 four scaling-aware transposes, B7/B8 wgrad), on the
+DeepSeek-V3 expert layer of one expert-parallel rank: 16384 tokens, hidden 7168,
+32 local experts, top-8 softmax routing, SwiGLU intermediate 2048.  Inputs are
+synthetic (seeded), resident in HBM before timing starts.
+
+Prints ONE JSON line.  `value` is the step's algorithmic GEMM FLOPs (18 M H I on the
+routed rows, padding excluded) divided by the step time.  `roofline` is the dominant
+kernel measured with HIP events on its launch stream inside the timed region;
+`cast_ops` is the standalone 1x128 quantization and scaling-aware transpose of a
+32768 x 7168 bf16 activation; `cpu_baseline` is the float64 CPU oracle timed on a
+bounded sample of the same layer.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP8_PEAK_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
+HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", choices=["dsv3", "skew", "tiny"], default="dsv3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cast-ops", action="store_true")
+    return ap.parse_args()
+
+
+def stage_costs(shape, M):
+    """Algorithmic FLOPs (GEMMs) and bytes (memory-bound steps) per stage, on the M routed rows."""
+    T, H, E, k, I = shape.T, shape.H, shape.E, shape.k, shape.I
+    sc = lambda n: 4 * n // 128  # one fp32 scale per 128 elements
+    wq = 2 * I * H + H * I       # weight elements per expert (W1 + W2)
+    c = {
+        "F0_weight_quant": ("hbm", E * wq * 3 + sc(E * wq)),
+        "F1_permute_quant": ("hbm", T * H * 2 + M * H + sc(M * H) + T * k * 4 * 3),
+        "F2_fc1_fprop": ("mfma", 2 * M * H * 2 * I),
+        "F3_swiglu_quant": ("hbm", M * 2 * I * 2 + M * I + sc(M * I)),
+        "F4_fc2_fprop": ("mfma", 2 * M * I * H),
+        "F5_unpermute": ("hbm", M * H * 2 + T * k * 8 + T * H * 2),
+        "B1_permute_quant_dy": ("hbm", T * H * 2 + T * k * 8 + M * H + sc(M * H)),
+        "B2_fc2_dgrad": ("mfma", 2 * M * H * I),
+        "B3_swiglu_bwd_quant": ("hbm", M * 2 * I * 2 + M * I * 2 + M * 2 * I + sc(M * 2 * I)),
+        "B4_fc1_dgrad": ("mfma", 2 * M * 2 * I * H),
+        "B5_unpermute": ("hbm", M * H * 2 + T * k * 4 + T * H * 2),
+        "B6_sat_x4": ("hbm", 2 * (M * (H + I + H + 2 * I) + sc(M * (H + I + H + 2 * I)))),
+        "B7_fc2_wgrad": ("mfma", 2 * M * H * I),
+        "B8_fc1_wgrad": ("mfma", 2 * M * 2 * I * H),
+    }
+    return c
+
+
+class StageTimer:
+    """HIP events recorded on the launch stream between stages."""
+
+    def __init__(self, torch, names, steps):
+        self.torch = torch
+        self.names = names
+        self.ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in names]
+                   for _ in range(steps)]
+
+    def ms(self):
+        out = {n: [] for n in self.names}
+        for row in self.ev:
+            for n, (a, b) in zip(self.names, row):
+                out[n].append(a.elapsed_time(b))
+        return {n: sum(v) / len(v) for n, v in out.items()}
+
+
+def run_step(L, d, ev=None):
+    """One full step; `ev` is a list of (start, end) event pairs, one per stage."""
+    from paper_2511_02302_amd import ff8
+
+    b, dm = L.buf, L.d
+    off = b["offsets"]
+    stages = [
+        lambda: L.quantize_weights(d["w1"], d["w2"]),
+        lambda: ff8.ff8_permute_quant(d["x"], None, dm.k, dm.E, d["topk_idx"], False, b["row_map"], off,
+                                      b["src_row"], b["xq"], b["xs"], b["ws"]),
+        lambda: ff8.ff8_grouped_gemm_fprop(b["xq"], b["xs"], b["w1q"], b["w1s"], off, b["a"]),
+        lambda: ff8.ff8_swiglu_quant(b["a"], b["hq"], b["hs"], off, dm.E),
+        lambda: ff8.ff8_grouped_gemm_fprop(b["hq"], b["hs"], b["w2q"], b["w2s"], off, b["y_perm"]),
+        lambda: ff8.ff8_unpermute(b["y_perm"], b["row_map"], d["probs"], b["y"]),
+        lambda: ff8.ff8_permute_quant(d["dy"], d["probs"], dm.k, dm.E, None, True, b["row_map"], off,
+                                      b["src_row"], b["dyq"], b["dys"]),
+        lambda: ff8.ff8_grouped_gemm_dgrad(b["dyq"], b["dys"], b["w2q"], b["w2s"], off, b["dh"]),
+        lambda: ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, dm.E),
+        lambda: ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"]),
+        lambda: ff8.ff8_unpermute(b["dx_perm"], b["row_map"], None, b["dx"]),
+        lambda: [ff8.ff8_scaling_aware_transpose(b[n + "q"], b[n + "s"], b[n + "Tq"], b[n + "Ts"], off, dm.E)
+                 for n in ("x", "h", "dy", "da")],
+        lambda: ff8.ff8_grouped_gemm_wgrad(b["dyTq"], b["dyTs"], b["hTq"], b["hTs"], off, b["dw2"]),
+        lambda: ff8.ff8_grouped_gemm_wgrad(b["daTq"], b["daTs"], b["xTq"], b["xTs"], off, b["dw1"]),
+    ]
+    for i, fn in enumerate(stages):
+        if ev is not None:
+            ev[i][0].record()
+        fn()
+        if ev is not None:
+            ev[i][1].record()
+
+
+def cast_ops(torch, reps=20):
+    """1x128 quantization and scaling-aware transpose of a 32768 x 7168 bf16 activation (0.1% x100 outliers),
+    plus the naive dequantize -> bf16 transpose -> requantize chain and the 2048 x 7168 weight block quant."""
+    import workloads
+    from paper_2511_02302_amd import ff8
+
+    R, C = workloads.CAST_X
+    x = workloads.outlier_activation(R, C, seed=0, device="cuda")
+    q = torch.empty((R, C), dtype=torch.uint8, device="cuda")
+    s = torch.empty((R, C // 128), dtype=torch.float32, device="cuda")
+    qT = torch.empty((C, R), dtype=torch.uint8, device="cuda")
+    sT = torch.empty((C, R // 128), dtype=torch.float32, device="cuda")
+    d = torch.empty((R, C), dtype=torch.bfloat16, device="cuda")
+    dT = torch.empty((C, R), dtype=torch.bfloat16, device="cuda")
+    qn = torch.empty((C, R), dtype=torch.uint8, device="cuda")
+    sn = torch.empty((C, R // 128), dtype=torch.float32, device="cuda")
+    wr, wc = workloads.CAST_W
+    w = workloads.randn_bf16((wr, wc), 0.02, seed=1, device="cuda")
+    wq = torch.empty((wr, wc), dtype=torch.uint8, device="cuda")
+    ws = torch.empty((wr // 128, wc // 128), dtype=torch.float32, device="cuda")
+    cp_src = torch.empty(R * C * 2 // 16 * 16, dtype=torch.uint8, device="cuda")
+    cp_dst = torch.empty_like(cp_src)
+
+    def timeit(fn):
+        for _ in range(3):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in evs)
+        return t[len(t) // 2]
+
+    out = {}
+    n = R * C
+    quant_bytes = n * 2 + n + n // 128 * 4
+    sat_bytes = 2 * (n + n // 128 * 4)
+    t_q = timeit(lambda: ff8.ff8_quant_rowwise(x, q, s))
+    t_sat = timeit(lambda: ff8.ff8_scaling_aware_transpose(q, s, qT, sT))
+
+    def naive():
+        ff8.ff8_baseline_dequant_rowwise(q, s, d)
+        ff8.ff8_baseline_transpose_bf16(d, dT)
+        ff8.ff8_quant_rowwise(dT, qn, sn)
+
+    t_naive = timeit(naive)
+    t_w = timeit(lambda: ff8.ff8_quant_block128(w, wq, ws))
+    t_cp = timeit(lambda: ff8.ff8_baseline_copy(cp_src, cp_dst))
+    cp_bytes = 2 * cp_src.numel()
+    for name, t, by in (("quant_rowwise_1x128", t_q, quant_bytes), ("scaling_aware_transpose", t_sat, sat_bytes),
+                        ("naive_dequant_transpose_requant", t_naive, sat_bytes),
+                        ("weight_quant_128x128_cache_resident", t_w, wr * wc * 3 + wr * wc // 16384 * 4),
+                        ("copy_reference", t_cp, cp_bytes)):
+        gbs = by / (t * 1e-3) / 1e9
+        out[name] = {"ms": round(t, 4), "GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 3),
+                     "bytes": by}
+    out["sat_speedup_vs_naive"] = round(t_naive / t_sat, 2)
+    out["workload"] = f"bf16 activation {R}x{C} N(0,1) with 0.1% x100 outliers; weight {wr}x{wc} N(0,0.02)"
+    return out
+
+
+def cpu_baseline(shape, rows=128, seed=0):
+    """The float64 oracle, as it stands, on a bounded sample of the workload.
+
+    Sample: expert 0 of the layer -- its 128x128 weight quantization (F0 for one
+    expert) and one 128-row group of its routed tokens through F1..B8.  The full step
+    runs F0 once per expert and the row work once per 128 routed rows, so the oracle's
+    time for the full step is E * t(F0 sample) + (M / rows) * t(rows sample); `value`
+    is the step's GEMM FLOPs over that time (the same unit as the GPU figure).
+    """
+    import numpy as np
+    import workloads
+    from oracle import layer as olayer
+
+    sample = workloads.LayerShape("one-expert sample", rows, shape.H, 1, 1, shape.I, "iid")
+    inp = workloads.layer_inputs(sample, seed=seed)
+    f = lambda t: t.float().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    w = olayer.quantize_weights(f(inp["w1"]), f(inp["w2"]))
+    t1 = time.perf_counter()
+    st = olayer.forward(f(inp["x"]), inp["topk_idx"].numpy(), inp["probs"].numpy(), w["w1q"], w["w1s"], w["w2q"],
+                        w["w2s"], 1)
+    olayer.backward(st, f(inp["dy"]), inp["probs"].numpy(), w["w1q"], w["w1s"], w["w2q"], w["w2s"])
+    t2 = time.perf_counter()
+    M = shape.T * shape.k
+    full_s = shape.E * (t1 - t0) + (M / rows) * (t2 - t1)
+    flops = 18 * M * shape.H * shape.I
+    cores = len(os.sched_getaffinity(0))
+    return {"value": round(flops / full_s / 1e12, 7), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"expert 0 only: F0 on its W1 [{2 * shape.I}x{shape.H}] and W2 [{shape.H}x{shape.I}] "
+                      f"({t1 - t0:.1f} s), F1..B8 on one {rows}-row group of its tokens ({t2 - t1:.1f} s); "
+                      f"scaled to the full step as {shape.E} x F0 + {M // rows} x rows = {full_s:.0f} s",
+            "sample_seconds": round(t2 - t0, 1)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only (single-GPU build); "
+                                   f"--gpus {args.gpus} is not supported"}))
+        sys.exit(2)
+    import torch
+    import workloads
+    from paper_2511_02302_amd.layer import ExpertLayerFP8
+
+    shape = {"dsv3": workloads.DSV3, "skew": workloads.SKEW, "tiny": workloads.TINY}[args.workload]
+    torch.cuda.set_device(0)
+    d = workloads.layer_inputs(shape, seed=0, device="cuda")
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
+    counts = workloads.expert_counts(d["topk_idx"], shape.E)
+    M = int(counts.sum())
+    costs = stage_costs(shape, M)
+    names = list(costs)
+
+    for _ in range(args.warmup):
+        run_step(L, d)
+    torch.cuda.synchronize()
+    timer = StageTimer(torch, names, args.steps)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(L, d, timer.ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    st_ms = timer.ms()
+
+    gemm_flops = sum(v for kind, v in costs.values() if kind == "mfma")
+    value = gemm_flops / (ms_step * 1e-3) / 1e12
+    stages = {}
+    for n in names:
+        kind, amount = costs[n]
+        t = st_ms[n]
+        if kind == "mfma":
+            ach = amount / (t * 1e-3) / 1e12
+            stages[n] = {"ms": round(t, 4), "TFLOP/s": round(ach, 1), "frac_mfma": round(ach / FP8_PEAK_TFLOPS, 3)}
+        else:
+            ach = amount / (t * 1e-3) / 1e9
+            stages[n] = {"ms": round(t, 4), "GB/s": round(ach, 1), "frac_hbm": round(ach / HBM_PEAK_GBS, 3)}
+    gemm_ms = sum(st_ms[n] for n in names if costs[n][0] == "mfma")
+    dom = max(names, key=lambda n: st_ms[n])
+    kind, amount = costs[dom]
+    if kind == "mfma":
+        ach = amount / (st_ms[dom] * 1e-3) / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / FP8_PEAK_TFLOPS, 4), "traffic": None,
+                "per_launch": {"flops": amount, "avg_ms": round(st_ms[dom], 4)}}
+    else:
+        ach = amount / (st_ms[dom] * 1e-3) / 1e9
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                "per_launch": {"bytes": amount, "avg_ms": round(st_ms[dom], 4)}}
+
+    rec = {
+        "metric": "FP8 MoE expert fwd+bwd TFLOP/s (% MFMA peak); quant/transpose GB/s (% HBM)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8_e4m3",
+        "data": "synthetic",
+        "config": {"workload": f"{shape.name} expert layer, fwd+bwd incl. 128x128 weight quant", "tokens": shape.T,
+                   "hidden": shape.H, "experts": shape.E, "top_k": shape.k, "intermediate": shape.I,
+                   "routed_rows": M, "routing": shape.routing},
+        "frac_mfma_step": round(value / FP8_PEAK_TFLOPS, 4),
+        "gemm_only": {"TFLOP/s": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
+                      "frac_mfma": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / FP8_PEAK_TFLOPS, 4),
+                      "ms": round(gemm_ms, 3)},
+        "roofline": roof,
+        "stages": stages,
+    }
+    if not args.no_cast_ops:
+        del L, d
+        torch.cuda.empty_cache()
+        rec["cast_ops"] = cast_ops(torch)
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(shape)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,249 @@
+// C ABI of the FP8-Flow-MoE expert-layer library: host-side argument validation,
+// error reporting, and dispatch to the gfx950 launchers.  Validation happens before
+// anything is enqueued; the library allocates no memory and keeps no state apart
+// from a thread-local error string and a per-device CU count.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/ff8.h"
+#include "ff8_launch.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) {
+    g_err[0] = '\0';
+    return FF8_OK;
+  }
+  return fail(FF8_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool mult128(int64_t v) { return v > 0 && v % 128 == 0; }
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+#define REQUIRE_PTR(p) \
+  if ((p) == nullptr) return fail(FF8_ERR_NULL, "%s: argument '%s' is NULL", __func__, #p)
+#define REQUIRE_SHAPE(cond) \
+  if (!(cond)) return fail(FF8_ERR_SHAPE, "%s: shape check failed: %s", __func__, #cond)
+#define REQUIRE_ARG(cond) \
+  if (!(cond)) return fail(FF8_ERR_ARG, "%s: argument check failed: %s", __func__, #cond)
+
+}  // namespace
+
+namespace ff8 {
+
+int device_cu_count() {
+  static std::mutex mu;
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+}  // namespace ff8
+
+extern "C" {
+
+int ff8_version(void) { return 100; }
+
+const char* ff8_status_string(int status) {
+  switch (status) {
+    case FF8_OK: return "ok";
+    case FF8_ERR_NULL: return "null pointer";
+    case FF8_ERR_SHAPE: return "bad shape";
+    case FF8_ERR_ARG: return "bad argument";
+    case FF8_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* ff8_last_error(void) { return g_err; }
+
+int ff8_quant_rowwise(const ff8_bf16* x, int64_t rows, int64_t cols, ff8_e4m3* q, float* s, void* stream) {
+  REQUIRE_PTR(x); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  REQUIRE_SHAPE(rows >= 1 && mult128(cols));
+  return hip_status(ff8::launch_quant_rowwise(x, rows, cols, q, s, as_stream(stream)), __func__);
+}
+
+int ff8_quant_block128(const ff8_bf16* w, int64_t rows, int64_t cols, ff8_e4m3* q, float* s, void* stream) {
+  REQUIRE_PTR(w); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  REQUIRE_SHAPE(mult128(rows) && mult128(cols));
+  return hip_status(ff8::launch_quant_block128(w, rows, cols, q, s, as_stream(stream)), __func__);
+}
+
+int64_t ff8_rows_bound(int64_t T, int k, int E) {
+  if (T < 0 || k < 1 || E < 1 || k > E) return -1;
+  const int64_t need = T * k + 127LL * E;
+  return (need + 127) / 128 * 128;
+}
+
+size_t ff8_permute_workspace_bytes(int64_t T, int k, int E) {
+  if (T < 0 || k < 1 || E < 1) return 0;
+  return ff8::permute_workspace_bytes(T, k, E);
+}
+
+int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                      const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
+                      int64_t M_cap, ff8_e4m3* q, float* s, void* workspace, size_t ws_bytes, void* stream) {
+  REQUIRE_ARG(reuse_map == 0 || reuse_map == 1);
+  REQUIRE_ARG(k >= 1 && E >= 1 && k <= E && E <= 1024);
+  REQUIRE_SHAPE(T >= 0 && mult128(H) && M_cap % 128 == 0);
+  REQUIRE_SHAPE(M_cap >= ff8_rows_bound(T, k, E));
+  REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
+  if (T > 0) REQUIRE_PTR(x);
+  REQUIRE_PTR(row_map); REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  hipStream_t st = as_stream(stream);
+  if (!reuse_map) {
+    if (T > 0) REQUIRE_PTR(topk_idx);
+    const size_t need = ff8::permute_workspace_bytes(T, k, E);
+    if (need > 0) REQUIRE_PTR(workspace);
+    REQUIRE_ARG(ws_bytes >= need);
+    const int rc = hip_status(ff8::launch_route(topk_idx, T, k, E, row_map, offsets, src_row, M_cap, workspace, st),
+                              "ff8_permute_quant(route)");
+    if (rc != FF8_OK) return rc;
+  }
+  return hip_status(ff8::launch_permute_quant(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st),
+                    __func__);
+}
+
+int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows, int64_t cols,
+                                const int32_t* offsets, int E, ff8_e4m3* qT, float* sT, void* stream) {
+  REQUIRE_PTR(q); REQUIRE_PTR(s); REQUIRE_PTR(qT); REQUIRE_PTR(sT);
+  REQUIRE_SHAPE(mult128(rows) && mult128(cols));
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_sat(q, s, rows, cols, offsets, E, qT, sT, as_stream(stream)), __func__);
+}
+
+static int gemm_common(const char* fn, const void* a, const void* as, const void* b, const void* bs,
+                       const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, const void* out) {
+  if (!a || !as || !b || !bs || !offsets || !out) return fail(FF8_ERR_NULL, "%s: a required pointer is NULL", fn);
+  if (E < 1) return fail(FF8_ERR_ARG, "%s: E must be >= 1", fn);
+  if (!mult128(M_cap) || !mult128(N) || !mult128(K))
+    return fail(FF8_ERR_SHAPE, "%s: M_cap, N and K must be positive multiples of 128", fn);
+  return FF8_OK;
+}
+
+int ff8_grouped_gemm_fprop(const ff8_e4m3* a, const float* a_s, const ff8_e4m3* w, const float* w_s,
+                           const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
+                           void* stream) {
+  const int rc = gemm_common(__func__, a, a_s, w, w_s, offsets, E, M_cap, N, K, out);
+  if (rc != FF8_OK) return rc;
+  return hip_status(ff8::launch_grouped_gemm(ff8::kFprop, a, a_s, w, w_s, offsets, E, M_cap, N, K, out, 0,
+                                             as_stream(stream)),
+                    __func__);
+}
+
+int ff8_grouped_gemm_dgrad(const ff8_e4m3* g, const float* g_s, const ff8_e4m3* w, const float* w_s,
+                           const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
+                           void* stream) {
+  const int rc = gemm_common(__func__, g, g_s, w, w_s, offsets, E, M_cap, N, K, out);
+  if (rc != FF8_OK) return rc;
+  return hip_status(ff8::launch_grouped_gemm(ff8::kDgrad, g, g_s, w, w_s, offsets, E, M_cap, N, K, out, 0,
+                                             as_stream(stream)),
+                    __func__);
+}
+
+int ff8_grouped_gemm_wgrad(const ff8_e4m3* gT, const float* gT_s, const ff8_e4m3* xT, const float* xT_s,
+                           const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, float* dw,
+                           int accumulate, void* stream) {
+  const int rc = gemm_common(__func__, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw);
+  if (rc != FF8_OK) return rc;
+  REQUIRE_ARG(accumulate == 0 || accumulate == 1);
+  return hip_status(ff8::launch_grouped_gemm(ff8::kWgrad, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw,
+                                             accumulate, as_stream(stream)),
+                    __func__);
+}
+
+int ff8_swiglu_quant(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I, ff8_e4m3* hq,
+                     float* hs, void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(hq); REQUIRE_PTR(hs);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_quant(a, offsets, E, M_cap, I, hq, hs, as_stream(stream)), __func__);
+}
+
+int ff8_swiglu_bwd_quant(const ff8_bf16* a, const ff8_bf16* dh, const int32_t* offsets, int E, int64_t M_cap,
+                         int64_t I, ff8_e4m3* daq, float* das, void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(dh); REQUIRE_PTR(daq); REQUIRE_PTR(das);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_bwd_quant(a, dh, offsets, E, M_cap, I, daq, das, as_stream(stream)),
+                    __func__);
+}
+
+int ff8_unpermute(const ff8_bf16* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k, int64_t H,
+                  int64_t M_cap, ff8_bf16* y, void* stream) {
+  REQUIRE_ARG(k >= 1);
+  REQUIRE_SHAPE(T >= 0 && mult128(H) && M_cap >= 1);
+  if (T > 0) {
+    REQUIRE_PTR(y_perm); REQUIRE_PTR(row_map); REQUIRE_PTR(y);
+  }
+  return hip_status(ff8::launch_unpermute(y_perm, row_map, row_w, T, k, H, M_cap, y, as_stream(stream)), __func__);
+}
+
+int ff8_cast_f32_to_e4m3(const float* x, int64_t n, ff8_e4m3* q, void* stream) {
+  REQUIRE_SHAPE(n >= 0);
+  if (n == 0) return FF8_OK;
+  REQUIRE_PTR(x); REQUIRE_PTR(q);
+  REQUIRE_ARG(((uintptr_t)x & 15) == 0 && ((uintptr_t)q & 3) == 0);
+  return hip_status(ff8::launch_cast_f32_e4m3(x, n, q, as_stream(stream)), __func__);
+}
+
+int ff8_cast_e4m3_to_f32(const ff8_e4m3* q, int64_t n, float* x, void* stream) {
+  REQUIRE_SHAPE(n >= 0);
+  if (n == 0) return FF8_OK;
+  REQUIRE_PTR(x); REQUIRE_PTR(q);
+  REQUIRE_ARG(((uintptr_t)x & 15) == 0 && ((uintptr_t)q & 3) == 0);
+  return hip_status(ff8::launch_cast_e4m3_f32(q, n, x, as_stream(stream)), __func__);
+}
+
+int ff8_baseline_dequant_rowwise(const ff8_e4m3* q, const float* s, int64_t rows, int64_t cols, ff8_bf16* out,
+                                 void* stream) {
+  REQUIRE_PTR(q); REQUIRE_PTR(s); REQUIRE_PTR(out);
+  REQUIRE_SHAPE(rows >= 1 && mult128(cols));
+  return hip_status(ff8::launch_dequant_rowwise(q, s, rows, cols, out, as_stream(stream)), __func__);
+}
+
+int ff8_baseline_transpose_bf16(const ff8_bf16* in, int64_t rows, int64_t cols, ff8_bf16* out, void* stream) {
+  REQUIRE_PTR(in); REQUIRE_PTR(out);
+  REQUIRE_SHAPE(rows > 0 && cols > 0 && rows % 64 == 0 && cols % 64 == 0);
+  return hip_status(ff8::launch_transpose_bf16(in, rows, cols, out, as_stream(stream)), __func__);
+}
+
+int ff8_baseline_swiglu_bf16(const ff8_bf16* a, const int32_t* offsets, int E, int64_t rows, int64_t I, ff8_bf16* h,
+                             void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(h);
+  REQUIRE_SHAPE(rows >= 1 && mult128(I));
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_bf16(a, offsets, E, rows, I, h, as_stream(stream)), __func__);
+}
+
+int ff8_baseline_copy(const void* src, void* dst, int64_t nbytes, void* stream) {
+  REQUIRE_PTR(src); REQUIRE_PTR(dst);
+  REQUIRE_SHAPE(nbytes > 0 && nbytes % 16 == 0);
+  return hip_status(ff8::launch_copy(src, dst, nbytes, as_stream(stream)), __func__);
+}
+
+}  // extern "C"

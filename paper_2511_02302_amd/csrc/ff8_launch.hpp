@@ -1,0 +1,49 @@
+// Host-side launchers of the gfx950 kernels.  Arguments are already validated by
+// the C ABI layer (ff8_api.cpp); each launcher only enqueues work on `stream`.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ff8 {
+
+hipError_t launch_quant_rowwise(const uint16_t* x, int64_t rows, int64_t cols, uint8_t* q, float* s,
+                                hipStream_t st);
+hipError_t launch_quant_block128(const uint16_t* w, int64_t rows, int64_t cols, uint8_t* q, float* s,
+                                 hipStream_t st);
+hipError_t launch_cast_f32_e4m3(const float* x, int64_t n, uint8_t* q, hipStream_t st);
+hipError_t launch_cast_e4m3_f32(const uint8_t* q, int64_t n, float* x, hipStream_t st);
+hipError_t launch_dequant_rowwise(const uint8_t* q, const float* s, int64_t rows, int64_t cols, uint16_t* out,
+                                  hipStream_t st);
+hipError_t launch_transpose_bf16(const uint16_t* in, int64_t rows, int64_t cols, uint16_t* out, hipStream_t st);
+hipError_t launch_copy(const void* src, void* dst, int64_t nbytes, hipStream_t st);
+
+hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
+                      uint8_t* qT, float* sT, hipStream_t st);
+
+size_t permute_workspace_bytes(int64_t T, int k, int E);
+hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int32_t* row_map, int32_t* offsets,
+                        int32_t* src_row, int64_t M_cap, void* workspace, hipStream_t st);
+hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                int64_t M_cap, uint8_t* q, float* s, hipStream_t st);
+hipError_t launch_unpermute(const uint16_t* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k,
+                            int64_t H, int64_t M_cap, uint16_t* y, hipStream_t st);
+
+hipError_t launch_swiglu_quant(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                               uint8_t* hq, float* hs, hipStream_t st);
+hipError_t launch_swiglu_bwd_quant(const uint16_t* a, const uint16_t* dh, const int32_t* offsets, int E,
+                                   int64_t M_cap, int64_t I, uint8_t* daq, float* das, hipStream_t st);
+hipError_t launch_swiglu_bf16(const uint16_t* a, const int32_t* offsets, int E, int64_t rows, int64_t I,
+                              uint16_t* h, hipStream_t st);
+
+enum GemmMode { kFprop = 0, kDgrad = 1, kWgrad = 2 };
+hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s, const uint8_t* b,
+                               const float* b_s, const int32_t* offsets, int E, int64_t M_cap, int64_t N,
+                               int64_t K, void* out, int accumulate, hipStream_t st);
+
+// Number of workgroups that fill the device (CU count x `per_cu`), cached per device.
+int device_cu_count();
+
+}  // namespace ff8

@@ -1,0 +1,180 @@
+// Scaling-aware FP8 transpose for gfx950 (paper section 3.1, Algorithm 1 and the
+// exponent-shift identity).
+//
+// One workgroup owns one 128-column tile of the input and kRB consecutive 128-row
+// blocks.  Per block:
+//   1. the 128 row scales of the tile give S_max (wave DPP max + LDS) and every row's
+//      shift k_i = log2(S_max) - log2(s_i) (integer: scales are powers of two);
+//   2. lane (sr, sc) loads an 8x8 byte sub-block (rows 8 sr.., bytes 8 sc..; 16 lanes
+//      read a full 128-byte row segment);
+//   3. rows with k_i > 0 are re-expressed at S_max: decode (exact), multiply by 2^-k
+//      (exact), hardware RNE encode -- equal to lowering the exponent field by k_i
+//      while it stays >= 1, and the nearest-even subnormal below that;
+//   4. the 8x8 sub-block is transposed in registers (v_perm_b32) and written to LDS
+//      in output order (XOR-swizzled 8-byte chunks, conflict-free);
+//   5. the 128x128 output block is streamed out with 16-byte stores, 8 lanes per
+//      128-byte output row segment.
+// The block's S_max is written to sT once per output row: kRB consecutive blocks
+// give kRB contiguous floats per row, so scale stores are 4*kRB bytes wide.
+
+#include "ff8_device.hpp"
+#include "ff8_launch.hpp"
+
+namespace ff8 {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kRB = 4;  // 128-row blocks per workgroup
+
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+  return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// 4x4 byte transpose: rows a, b, c, d (byte j of each = column j) -> columns.
+__device__ __forceinline__ void transpose4x4(uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t& w0,
+                                             uint32_t& w1, uint32_t& w2, uint32_t& w3) {
+  const uint32_t p = perm(b, a, 0x06020400u);  // a0 b0 a2 b2
+  const uint32_t q = perm(b, a, 0x07030501u);  // a1 b1 a3 b3
+  const uint32_t r = perm(d, c, 0x06020400u);  // c0 d0 c2 d2
+  const uint32_t s = perm(d, c, 0x07030501u);  // c1 d1 c3 d3
+  w0 = perm(r, p, 0x05040100u);                // a0 b0 c0 d0
+  w2 = perm(r, p, 0x07060302u);                // a2 b2 c2 d2
+  w1 = perm(s, q, 0x05040100u);                // a1 b1 c1 d1
+  w3 = perm(s, q, 0x07060302u);                // a3 b3 c3 d3
+}
+
+// Re-express 4 e4m3 bytes at a scale 2^k times larger.
+__device__ __forceinline__ uint32_t shift4(uint32_t w, float f) {
+  const f32x2 lo = dec_e4m3x2<false>(w), hi = dec_e4m3x2<true>(w);
+  return cvt_e4m3x4(lo[0] * f, lo[1] * f, hi[0] * f, hi[1] * f);
+}
+
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  const int xcd = bid & 7, slot = bid >> 3, q = n >> 3, r = n & 7;
+  return xcd * q + (xcd < r ? xcd : r) + slot;
+}
+
+__global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict__ q, const float* __restrict__ s,
+                                                       int64_t rows, int64_t cols, const int32_t* __restrict__ offsets,
+                                                       int E, int n_rb_groups, uint8_t* __restrict__ qT,
+                                                       float* __restrict__ sT) {
+  __shared__ uint32_t tile[128 * 128 / 4];  // output block, 128 rows x 128 bytes (swizzled 8-byte chunks)
+  __shared__ int kshift[128];
+  __shared__ uint32_t wmax[2];
+
+  const int n_cb = (int)(cols / kTile);
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int cb = logical / n_rb_groups;
+  const int rg = logical - cb * n_rb_groups;
+  const int64_t m_rows = active_rows(offsets, E, rows);
+  const int64_t n_rb = rows / kTile;
+  const int n_sb = (int)(rows / kTile);  // sT row stride (floats)
+
+  const int tid = threadIdx.x;
+  const int sr = tid >> 4, sc = tid & 15;
+  float smax_kept[kRB];
+
+#pragma unroll
+  for (int i = 0; i < kRB; ++i) smax_kept[i] = 0.0f;
+
+  for (int bi = 0; bi < kRB; ++bi) {
+    const int64_t rb = (int64_t)rg * kRB + bi;
+    if (rb >= n_rb || rb * kTile >= m_rows) break;  // uniform across the workgroup
+
+    // 1. S_max and per-row shifts.
+    int t_row = 0;
+    if (tid < 128) {
+      t_row = (int)(__float_as_uint(s[(rb * kTile + tid) * n_cb + cb]) >> 23) - 127;
+      const uint32_t m = max64_u32((uint32_t)(t_row + 256));
+      if ((tid & 63) == 0) wmax[tid >> 6] = m;
+    }
+    // 2. load the 8x8 sub-block (issued before the barrier to overlap latency).
+    const uint8_t* src = q + (rb * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
+    u32x2 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = ld8(src + (int64_t)i * cols);
+    __syncthreads();
+    const int t_max = (int)max(wmax[0], wmax[1]) - 256;
+    if (tid < 128) kshift[tid] = t_max - t_row;
+    smax_kept[bi] = exp2i(t_max);
+    __syncthreads();
+
+    // 3. exponent shift of rows below S_max.
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = kshift[sr * 8 + i];
+      if (k != 0) {
+        const float f = exp2i(-k);
+        v[i][0] = shift4(v[i][0], f);
+        v[i][1] = shift4(v[i][1], f);
+      }
+    }
+    // 4. transpose the 8x8 sub-block: column c of the input becomes output row 8 sc + c.
+    uint32_t o_lo[8], o_hi[8];
+    transpose4x4(v[0][0], v[1][0], v[2][0], v[3][0], o_lo[0], o_lo[1], o_lo[2], o_lo[3]);
+    transpose4x4(v[4][0], v[5][0], v[6][0], v[7][0], o_hi[0], o_hi[1], o_hi[2], o_hi[3]);
+    transpose4x4(v[0][1], v[1][1], v[2][1], v[3][1], o_lo[4], o_lo[5], o_lo[6], o_lo[7]);
+    transpose4x4(v[4][1], v[5][1], v[6][1], v[7][1], o_hi[4], o_hi[5], o_hi[6], o_hi[7]);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int orow = sc * 8 + c;
+      const int chunk = sr ^ (orow >> 3);  // orow >> 3 == sc
+      u32x2 w;
+      w[0] = o_lo[c];
+      w[1] = o_hi[c];
+      *reinterpret_cast<u32x2*>(&tile[orow * 32 + chunk * 2]) = w;
+    }
+    __syncthreads();
+
+    // 5. stream the output block: 8 lanes per 128-byte output row, 4 passes of 32 rows.
+    const int c16 = tid & 7;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int orow = (tid >> 3) + 32 * p;
+      const int sw = (orow >> 3) & 15;
+      const u32x2 a = *reinterpret_cast<const u32x2*>(&tile[orow * 32 + ((2 * c16) ^ sw) * 2]);
+      const u32x2 b = *reinterpret_cast<const u32x2*>(&tile[orow * 32 + ((2 * c16 + 1) ^ sw) * 2]);
+      u32x4 o;
+      o[0] = a[0];
+      o[1] = a[1];
+      o[2] = b[0];
+      o[3] = b[1];
+      st16(qT + ((int64_t)cb * kTile + orow) * rows + rb * kTile + c16 * 16, o);
+    }
+    __syncthreads();  // tile and kshift are reused by the next block
+  }
+
+  // Column-wise scales: every output row of the tile gets S_max of each block.
+  if (tid < 128) {
+    float* dst = sT + ((int64_t)cb * kTile + tid) * n_sb + (int64_t)rg * kRB;
+    const int64_t rb0 = (int64_t)rg * kRB;
+    int n_valid = 0;
+#pragma unroll
+    for (int bi = 0; bi < kRB; ++bi)
+      if (rb0 + bi < n_rb && (rb0 + bi) * kTile < m_rows) n_valid = bi + 1;
+    if (n_valid == kRB && (((uintptr_t)dst) & 15) == 0) {
+      u32x4 o;
+#pragma unroll
+      for (int bi = 0; bi < kRB; ++bi) o[bi] = __float_as_uint(smax_kept[bi]);
+      st16(dst, o);
+    } else {
+#pragma unroll
+      for (int bi = 0; bi < kRB; ++bi)
+        if (bi < n_valid) dst[bi] = smax_kept[bi];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
+                      uint8_t* qT, float* sT, hipStream_t st) {
+  const int64_t n_rb = rows / kTile;
+  const int n_groups = (int)((n_rb + kRB - 1) / kRB);
+  const int64_t blocks = (cols / kTile) * n_groups;
+  sat_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(q, s, rows, cols, offsets, E, n_groups, qT, sT);
+  return hipGetLastError();
+}
+
+}  // namespace ff8

@@ -1,0 +1,237 @@
+"""ctypes binding of libff8.so: one Python function per C entry point, same names.
+
+Argument marshalling only: each function checks dtypes, shapes, devices and
+contiguity of the torch tensors it is given, passes raw device pointers and the
+current HIP stream to the C ABI, and raises Ff8Error on a non-zero status.  No
+function allocates, computes or falls back to anything: if libff8.so is missing
+the first call raises.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libff8.so")
+_lib = None
+
+_c_i64 = ctypes.c_int64
+_c_int = ctypes.c_int
+_c_vp = ctypes.c_void_p
+_c_size = ctypes.c_size_t
+
+_SIGNATURES = {
+    "ff8_version": (_c_int, []),
+    "ff8_status_string": (ctypes.c_char_p, [_c_int]),
+    "ff8_last_error": (ctypes.c_char_p, []),
+    "ff8_quant_rowwise": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_quant_block128": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_rows_bound": (_c_i64, [_c_i64, _c_int, _c_int]),
+    "ff8_permute_workspace_bytes": (_c_size, [_c_i64, _c_int, _c_int]),
+    "ff8_permute_quant": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp, _c_vp,
+                                   _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_vp]),
+    "ff8_scaling_aware_transpose": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
+    "ff8_grouped_gemm_fprop": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
+                                        _c_vp]),
+    "ff8_grouped_gemm_dgrad": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
+                                        _c_vp]),
+    "ff8_grouped_gemm_wgrad": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
+                                        _c_int, _c_vp]),
+    "ff8_swiglu_quant": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_swiglu_bwd_quant": (_c_int, [_c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_unpermute": (_c_int, [_c_vp, _c_vp, _c_vp, _c_i64, _c_int, _c_i64, _c_i64, _c_vp, _c_vp]),
+    "ff8_cast_f32_to_e4m3": (_c_int, [_c_vp, _c_i64, _c_vp, _c_vp]),
+    "ff8_cast_e4m3_to_f32": (_c_int, [_c_vp, _c_i64, _c_vp, _c_vp]),
+    "ff8_baseline_dequant_rowwise": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_vp]),
+    "ff8_baseline_transpose_bf16": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp]),
+    "ff8_baseline_swiglu_bf16": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp]),
+    "ff8_baseline_copy": (_c_int, [_c_vp, _c_vp, _c_i64, _c_vp]),
+}
+
+EXPORTS = tuple(_SIGNATURES)
+
+
+class Ff8Error(RuntimeError):
+    pass
+
+
+def library_path():
+    return _LIB_PATH
+
+
+def load():
+    """Load libff8.so (once) and declare every entry point's signature."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2511_02302_amd.build`")
+        lib = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _check(status, name):
+    if status != 0:
+        lib = load()
+        raise Ff8Error(f"{name}: {lib.ff8_status_string(status).decode()} ({lib.ff8_last_error().decode()})")
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t, dtype, name, ndim=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+_bf16, _u8, _f32, _i32 = torch.bfloat16, torch.uint8, torch.float32, torch.int32
+
+
+def ff8_version():
+    return load().ff8_version()
+
+
+def ff8_rows_bound(T, k, E):
+    return int(load().ff8_rows_bound(T, k, E))
+
+
+def ff8_permute_workspace_bytes(T, k, E):
+    return int(load().ff8_permute_workspace_bytes(T, k, E))
+
+
+def ff8_quant_rowwise(x, q, s, stream=None):
+    rows, cols = x.shape
+    _check(load().ff8_quant_rowwise(_ptr(x, _bf16, "x", 2), rows, cols, _ptr(q, _u8, "q"), _ptr(s, _f32, "s"),
+                                    _stream(stream)), "ff8_quant_rowwise")
+
+
+def ff8_quant_block128(w, q, s, stream=None):
+    rows, cols = w.reshape(-1, w.shape[-1]).shape
+    _check(load().ff8_quant_block128(_ptr(w, _bf16, "w"), rows, cols, _ptr(q, _u8, "q"), _ptr(s, _f32, "s"),
+                                     _stream(stream)), "ff8_quant_block128")
+
+
+def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src_row, q, s, workspace=None,
+                      stream=None):
+    T, H = x.shape
+    M_cap = q.shape[0]
+    ws = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().ff8_permute_quant(
+        _ptr(x, _bf16, "x", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E, _ptr(topk_idx, _i32, "topk_idx"),
+        int(reuse_map), _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
+        _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2),
+        None if workspace is None else ctypes.c_void_p(workspace.data_ptr()), ws, _stream(stream)),
+        "ff8_permute_quant")
+
+
+def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):
+    rows, cols = q.shape
+    _check(load().ff8_scaling_aware_transpose(
+        _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2), rows, cols, _ptr(offsets, _i32, "offsets"), E,
+        _ptr(qT, _u8, "qT", 2), _ptr(sT, _f32, "sT", 2), _stream(stream)), "ff8_scaling_aware_transpose")
+
+
+def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):
+    M_cap, K = a.shape
+    E, N, _ = w.shape
+    _check(load().ff8_grouped_gemm_fprop(
+        _ptr(a, _u8, "a", 2), _ptr(a_s, _f32, "a_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, _f32, "w_s"),
+        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)),
+        "ff8_grouped_gemm_fprop")
+
+
+def ff8_grouped_gemm_dgrad(g, g_s, w, w_s, offsets, out, stream=None):
+    M_cap, N = g.shape
+    E, _, K = w.shape
+    _check(load().ff8_grouped_gemm_dgrad(
+        _ptr(g, _u8, "g", 2), _ptr(g_s, _f32, "g_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, _f32, "w_s"),
+        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)),
+        "ff8_grouped_gemm_dgrad")
+
+
+def ff8_grouped_gemm_wgrad(gT, gT_s, xT, xT_s, offsets, dw, accumulate=False, stream=None):
+    N, M_cap = gT.shape
+    K = xT.shape[0]
+    E = dw.shape[0]
+    _check(load().ff8_grouped_gemm_wgrad(
+        _ptr(gT, _u8, "gT", 2), _ptr(gT_s, _f32, "gT_s"), _ptr(xT, _u8, "xT", 2), _ptr(xT_s, _f32, "xT_s"),
+        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(dw, _f32, "dw", 3), int(bool(accumulate)),
+        _stream(stream)), "ff8_grouped_gemm_wgrad")
+
+
+def ff8_swiglu_quant(a, hq, hs, offsets=None, E=0, stream=None):
+    M_cap, I2 = a.shape
+    _check(load().ff8_swiglu_quant(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
+                                   _ptr(hq, _u8, "hq", 2), _ptr(hs, _f32, "hs", 2), _stream(stream)),
+           "ff8_swiglu_quant")
+
+
+def ff8_swiglu_bwd_quant(a, dh, daq, das, offsets=None, E=0, stream=None):
+    M_cap, I2 = a.shape
+    _check(load().ff8_swiglu_bwd_quant(_ptr(a, _bf16, "a", 2), _ptr(dh, _bf16, "dh", 2),
+                                       _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2, _ptr(daq, _u8, "daq", 2),
+                                       _ptr(das, _f32, "das", 2), _stream(stream)), "ff8_swiglu_bwd_quant")
+
+
+def ff8_unpermute(y_perm, row_map, row_w, y, stream=None):
+    M_cap, H = y_perm.shape
+    T, k = row_map.shape
+    _check(load().ff8_unpermute(_ptr(y_perm, _bf16, "y_perm", 2), _ptr(row_map, _i32, "row_map", 2),
+                                _ptr(row_w, _f32, "row_w"), T, k, H, M_cap, _ptr(y, _bf16, "y", 2),
+                                _stream(stream)), "ff8_unpermute")
+
+
+def ff8_cast_f32_to_e4m3(x, q, stream=None):
+    _check(load().ff8_cast_f32_to_e4m3(_ptr(x, _f32, "x"), x.numel(), _ptr(q, _u8, "q"), _stream(stream)),
+           "ff8_cast_f32_to_e4m3")
+
+
+def ff8_cast_e4m3_to_f32(q, x, stream=None):
+    _check(load().ff8_cast_e4m3_to_f32(_ptr(q, _u8, "q"), q.numel(), _ptr(x, _f32, "x"), _stream(stream)),
+           "ff8_cast_e4m3_to_f32")
+
+
+def ff8_baseline_dequant_rowwise(q, s, out, stream=None):
+    rows, cols = q.shape
+    _check(load().ff8_baseline_dequant_rowwise(_ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2), rows, cols,
+                                               _ptr(out, _bf16, "out", 2), _stream(stream)),
+           "ff8_baseline_dequant_rowwise")
+
+
+def ff8_baseline_transpose_bf16(x, out, stream=None):
+    rows, cols = x.shape
+    _check(load().ff8_baseline_transpose_bf16(_ptr(x, _bf16, "x", 2), rows, cols, _ptr(out, _bf16, "out", 2),
+                                              _stream(stream)), "ff8_baseline_transpose_bf16")
+
+
+def ff8_baseline_swiglu_bf16(a, h, offsets=None, E=0, stream=None):
+    rows, I2 = a.shape
+    _check(load().ff8_baseline_swiglu_bf16(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, rows,
+                                           I2 // 2, _ptr(h, _bf16, "h", 2), _stream(stream)),
+           "ff8_baseline_swiglu_bf16")
+
+
+def ff8_baseline_copy(src, dst, stream=None):
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < n:
+        raise ValueError("dst is smaller than src")
+    _check(load().ff8_baseline_copy(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()), n,
+                                    _stream(stream)), "ff8_baseline_copy")

@@ -1,0 +1,116 @@
+"""FP8-Flow-MoE expert layer, forward and backward, on one GPU.
+
+The layer follows the casting-free dataflow of the paper (section 3.2): X and dY are
+quantized once, inside the fused permute (the two explicit casts); the SwiGLU and its
+backward twin emit FP8 directly; the weight-gradient GEMMs take column-wise operands
+made by the scaling-aware transpose from the row-wise FP8 tensors already in memory.
+BF16 stays only at the fc1 output (feeding the activation) and at the fc2 output
+(feeding the combine in the forward and the dispatch in the backward).
+
+Every step is one or more calls into libff8.so through the ctypes binding; torch
+only provides device memory (all buffers are allocated once, in __init__) and the
+stream.
+"""
+
+from dataclasses import dataclass
+
+import torch
+
+from . import ff8
+
+
+@dataclass
+class Dims:
+    T: int
+    H: int
+    E: int
+    k: int
+    I: int
+
+    @property
+    def m_cap(self):
+        return ff8.ff8_rows_bound(self.T, self.k, self.E)
+
+
+def _empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+class ExpertLayerFP8:
+    """Buffers and step sequence of one expert layer (E local experts, top-k routing)."""
+
+    def __init__(self, T, H, E, k, I, device="cuda"):
+        self.d = d = Dims(T, H, E, k, I)
+        self.device = dev = torch.device(device)
+        M = self.M_cap = d.m_cap
+        u8, f32, bf16, i32 = torch.uint8, torch.float32, torch.bfloat16, torch.int32
+        b = self.buf = {}
+        # weights (F0 outputs)
+        b["w1q"] = _empty((E, 2 * I, H), u8, dev)
+        b["w1s"] = _empty((E, 2 * I // 128, H // 128), f32, dev)
+        b["w2q"] = _empty((E, H, I), u8, dev)
+        b["w2s"] = _empty((E, H // 128, I // 128), f32, dev)
+        # routing
+        b["row_map"] = _empty((T, k), i32, dev)
+        b["offsets"] = _empty((E + 1,), i32, dev)
+        b["src_row"] = _empty((M,), i32, dev)
+        b["ws"] = _empty((max(1, ff8.ff8_permute_workspace_bytes(T, k, E)),), u8, dev)
+        # forward
+        b["xq"] = _empty((M, H), u8, dev)
+        b["xs"] = _empty((M, H // 128), f32, dev)
+        b["a"] = _empty((M, 2 * I), bf16, dev)
+        b["hq"] = _empty((M, I), u8, dev)
+        b["hs"] = _empty((M, I // 128), f32, dev)
+        b["y_perm"] = _empty((M, H), bf16, dev)
+        b["y"] = _empty((T, H), bf16, dev)
+        # backward
+        b["dyq"] = _empty((M, H), u8, dev)
+        b["dys"] = _empty((M, H // 128), f32, dev)
+        b["dh"] = _empty((M, I), bf16, dev)
+        b["daq"] = _empty((M, 2 * I), u8, dev)
+        b["das"] = _empty((M, 2 * I // 128), f32, dev)
+        b["dx_perm"] = _empty((M, H), bf16, dev)
+        b["dx"] = _empty((T, H), bf16, dev)
+        for name, cols in (("x", H), ("h", I), ("dy", H), ("da", 2 * I)):
+            b[name + "Tq"] = _empty((cols, M), u8, dev)
+            b[name + "Ts"] = _empty((cols, M // 128), f32, dev)
+        b["dw1"] = _empty((E, 2 * I, H), f32, dev)
+        b["dw2"] = _empty((E, H, I), f32, dev)
+
+    # ---- F0 ----
+    def quantize_weights(self, w1, w2):
+        b = self.buf
+        ff8.ff8_quant_block128(w1, b["w1q"], b["w1s"])
+        ff8.ff8_quant_block128(w2, b["w2q"], b["w2s"])
+
+    # ---- F1..F5 ----
+    def forward(self, x, topk_idx, probs):
+        b, d = self.buf, self.d
+        ff8.ff8_permute_quant(x, None, d.k, d.E, topk_idx, False, b["row_map"], b["offsets"], b["src_row"],
+                              b["xq"], b["xs"], b["ws"])
+        ff8.ff8_grouped_gemm_fprop(b["xq"], b["xs"], b["w1q"], b["w1s"], b["offsets"], b["a"])
+        ff8.ff8_swiglu_quant(b["a"], b["hq"], b["hs"], b["offsets"], d.E)
+        ff8.ff8_grouped_gemm_fprop(b["hq"], b["hs"], b["w2q"], b["w2s"], b["offsets"], b["y_perm"])
+        ff8.ff8_unpermute(b["y_perm"], b["row_map"], probs, b["y"])
+        return b["y"]
+
+    # ---- B1..B8 ----
+    def backward(self, dy, probs):
+        b, d = self.buf, self.d
+        off = b["offsets"]
+        ff8.ff8_permute_quant(dy, probs, d.k, d.E, None, True, b["row_map"], off, b["src_row"], b["dyq"], b["dys"])
+        ff8.ff8_grouped_gemm_dgrad(b["dyq"], b["dys"], b["w2q"], b["w2s"], off, b["dh"])
+        ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, d.E)
+        ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"])
+        ff8.ff8_unpermute(b["dx_perm"], b["row_map"], None, b["dx"])
+        for name in ("x", "h", "dy", "da"):
+            ff8.ff8_scaling_aware_transpose(b[name + "q"], b[name + "s"], b[name + "Tq"], b[name + "Ts"], off, d.E)
+        ff8.ff8_grouped_gemm_wgrad(b["dyTq"], b["dyTs"], b["hTq"], b["hTs"], off, b["dw2"])
+        ff8.ff8_grouped_gemm_wgrad(b["daTq"], b["daTs"], b["xTq"], b["xTs"], off, b["dw1"])
+        return b["dx"], b["dw1"], b["dw2"]
+
+    def step(self, x, topk_idx, probs, dy, w1, w2):
+        """One pass of the whole hot path: F0, F1..F5, B1..B8."""
+        self.quantize_weights(w1, w2)
+        self.forward(x, topk_idx, probs)
+        return self.backward(dy, probs)

@@ -1,0 +1,325 @@
+"""Parity of the expert-layer kernels (permute, grouped GEMMs, SwiGLU, unpermute) and of
+the whole layer against the CPU oracle, stage by stage (GPU)."""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import codec, quant, sat, moe
+from oracle import layer as olayer
+from paper_2511_02302_amd import ff8
+from paper_2511_02302_amd.layer import ExpertLayerFP8
+
+from test_gpu_kernels import dev, host, f64, rel_frob, poisoned, untouched
+
+pytestmark = pytest.mark.gpu
+
+GEMM_TOL = 2e-3   # max relative Frobenius error of a GEMM output against the float64 oracle
+
+
+def _skewed_routing(T, k, E, seed):
+    """Routing with zero-token experts, tiny experts and one dominant expert."""
+    rng = np.random.default_rng(seed)
+    p = np.array([0.5, 0.0, 0.3, 0.02] + [0.18 / max(1, E - 5)] * (E - 5) + [0.0])[:E]
+    p = p / p.sum()
+    idx = np.stack([rng.choice(E, size=k, replace=False, p=p) for _ in range(T)]).astype(np.int32)
+    return torch.from_numpy(idx)
+
+
+CASES = {
+    "tiny": (workloads.TINY, None),
+    "ragged": (workloads.LayerShape("ragged T300 H384 E6 k2 I384", 300, 384, 6, 2, 384, "iid"), 7),
+}
+
+
+def _inputs(case):
+    shape, skew_seed = CASES[case]
+    inp = workloads.layer_inputs(shape, seed=11)
+    if skew_seed is not None:
+        inp["topk_idx"] = _skewed_routing(shape.T, shape.k, shape.E, skew_seed)
+    return shape, inp
+
+
+def _routing_device(shape, inp):
+    M_cap = ff8.ff8_rows_bound(shape.T, shape.k, shape.E)
+    row_map = poisoned((shape.T, shape.k), torch.int32)
+    offsets = poisoned((shape.E + 1,), torch.int32)
+    src_row = poisoned((M_cap,), torch.int32)
+    ws = torch.empty(max(1, ff8.ff8_permute_workspace_bytes(shape.T, shape.k, shape.E)), dtype=torch.uint8,
+                     device="cuda")
+    return M_cap, row_map, offsets, src_row, ws
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_permute_quant_build_and_reuse(case):
+    shape, inp = _inputs(case)
+    M_cap, row_map, offsets, src_row, ws = _routing_device(shape, inp)
+    q = poisoned((M_cap, shape.H), torch.uint8)
+    s = poisoned((M_cap, shape.H // 128), torch.float32)
+    ff8.ff8_permute_quant(dev(inp["x"]), None, shape.k, shape.E, dev(inp["topk_idx"]), False, row_map, offsets,
+                          src_row, q, s, ws)
+    torch.cuda.synchronize()
+    counts, w_off, w_map, w_src = moe.route(host(inp["topk_idx"]), shape.E)
+    m_pad = int(w_off[-1])
+    assert np.array_equal(host(offsets), w_off)
+    assert np.array_equal(host(row_map), w_map)
+    assert np.array_equal(host(src_row)[:m_pad], w_src)
+    assert untouched(src_row[m_pad:])
+    wq, ws_ = moe.permute_quant_rows(f64(inp["x"]), w_src, shape.k)
+    assert np.array_equal(host(q[:m_pad]), wq)
+    assert np.array_equal(host(s[:m_pad]), ws_)
+    assert untouched(q[m_pad:]) and untouched(s[m_pad:])
+    # reuse mode with routing weights (the backward's dY cast)
+    dq = poisoned((M_cap, shape.H), torch.uint8)
+    dsc = poisoned((M_cap, shape.H // 128), torch.float32)
+    ff8.ff8_permute_quant(dev(inp["dy"]), dev(inp["probs"]), shape.k, shape.E, None, True, row_map, offsets,
+                          src_row, dq, dsc)
+    torch.cuda.synchronize()
+    wq2, ws2 = moe.permute_quant_rows(f64(inp["dy"]), w_src, shape.k, row_w=host(inp["probs"]))
+    assert np.array_equal(host(dq[:m_pad]), wq2)
+    assert np.array_equal(host(dsc[:m_pad]), ws2)
+    assert untouched(dq[m_pad:])
+
+
+def test_permute_deterministic_and_dropped_slots():
+    shape = workloads.LayerShape("drop", 700, 256, 5, 3, 256, "iid")
+    inp = workloads.layer_inputs(shape, seed=3)
+    idx = inp["topk_idx"].clone()
+    idx[::7, 1] = -1
+    M_cap, row_map, offsets, src_row, ws = _routing_device(shape, inp)
+    outs = []
+    for _ in range(2):
+        q = torch.zeros((M_cap, shape.H), dtype=torch.uint8, device="cuda")
+        s = torch.zeros((M_cap, shape.H // 128), dtype=torch.float32, device="cuda")
+        ff8.ff8_permute_quant(dev(inp["x"]), None, shape.k, shape.E, dev(idx), False, row_map, offsets, src_row,
+                              q, s, ws)
+        outs.append((host(q).copy(), host(row_map).copy()))
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+    _, w_off, w_map, w_src = moe.route(host(idx), shape.E)
+    assert np.array_equal(host(row_map), w_map)
+    assert np.array_equal(host(offsets), w_off)
+
+
+def _quantized_weights(shape, inp):
+    E, H, I = shape.E, shape.H, shape.I
+    w1q = torch.empty((E, 2 * I, H), dtype=torch.uint8, device="cuda")
+    w1s = torch.empty((E, 2 * I // 128, H // 128), dtype=torch.float32, device="cuda")
+    w2q = torch.empty((E, H, I), dtype=torch.uint8, device="cuda")
+    w2s = torch.empty((E, H // 128, I // 128), dtype=torch.float32, device="cuda")
+    ff8.ff8_quant_block128(dev(inp["w1"]), w1q, w1s)
+    ff8.ff8_quant_block128(dev(inp["w2"]), w2q, w2s)
+    return w1q, w1s, w2q, w2s
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_grouped_gemms(case):
+    shape, inp = _inputs(case)
+    E, H, I, T, k = shape.E, shape.H, shape.I, shape.T, shape.k
+    M_cap, row_map, offsets, src_row, ws = _routing_device(shape, inp)
+    xq = torch.empty((M_cap, H), dtype=torch.uint8, device="cuda")
+    xs = torch.empty((M_cap, H // 128), dtype=torch.float32, device="cuda")
+    ff8.ff8_permute_quant(dev(inp["x"]), None, k, E, dev(inp["topk_idx"]), False, row_map, offsets, src_row, xq, xs,
+                          ws)
+    w1q, w1s, w2q, w2s = _quantized_weights(shape, inp)
+    off = host(offsets).astype(np.int64)
+    m_pad = int(off[-1])
+    # fprop: A = Xq . W1^T
+    a = poisoned((M_cap, 2 * I), torch.bfloat16)
+    ff8.ff8_grouped_gemm_fprop(xq, xs, w1q, w1s, offsets, a)
+    torch.cuda.synchronize()
+    want = moe.grouped_gemm_fprop(host(xq), host(xs), host(w1q), host(w1s), off)
+    got = f64(a[:m_pad])
+    assert rel_frob(got, want) < GEMM_TOL
+    assert rel_frob(got, codec.bf16_round(want)) < 1e-3
+    assert untouched(a[m_pad:])
+    # dgrad: dX = G . W1 with a random row-wise quantized G of width 2I
+    g = workloads.randn_bf16((M_cap, 2 * I), 1.0, seed=5)
+    gq_np, gs_np = quant.quant_rowwise(f64(g))
+    gq, gs = dev(torch.from_numpy(gq_np)), dev(torch.from_numpy(gs_np))
+    dx = poisoned((M_cap, H), torch.bfloat16)
+    ff8.ff8_grouped_gemm_dgrad(gq, gs, w1q, w1s, offsets, dx)
+    torch.cuda.synchronize()
+    want = moe.grouped_gemm_dgrad(gq_np, gs_np, host(w1q), host(w1s), off)
+    assert rel_frob(f64(dx[:m_pad]), want) < GEMM_TOL
+    assert untouched(dx[m_pad:])
+    # dgrad on fc2's weight (contraction over H)
+    g2 = workloads.randn_bf16((M_cap, H), 1.0, seed=6)
+    g2q_np, g2s_np = quant.quant_rowwise(f64(g2))
+    dh = poisoned((M_cap, I), torch.bfloat16)
+    ff8.ff8_grouped_gemm_dgrad(dev(torch.from_numpy(g2q_np)), dev(torch.from_numpy(g2s_np)), w2q, w2s, offsets, dh)
+    torch.cuda.synchronize()
+    want = moe.grouped_gemm_dgrad(g2q_np, g2s_np, host(w2q), host(w2s), off)
+    assert rel_frob(f64(dh[:m_pad]), want) < GEMM_TOL
+    # wgrad: dW1[e] = G_e^T X_e from column-wise operands (scaling-aware transposes)
+    gT = torch.empty((2 * I, M_cap), dtype=torch.uint8, device="cuda")
+    gTs = torch.empty((2 * I, M_cap // 128), dtype=torch.float32, device="cuda")
+    xT = torch.empty((H, M_cap), dtype=torch.uint8, device="cuda")
+    xTs = torch.empty((H, M_cap // 128), dtype=torch.float32, device="cuda")
+    ff8.ff8_scaling_aware_transpose(gq, gs, gT, gTs, offsets, E)
+    ff8.ff8_scaling_aware_transpose(xq, xs, xT, xTs, offsets, E)
+    dw = torch.full((E, 2 * I, H), 7.0, dtype=torch.float32, device="cuda")
+    ff8.ff8_grouped_gemm_wgrad(gT, gTs, xT, xTs, offsets, dw, accumulate=False)
+    torch.cuda.synchronize()
+    want = moe.grouped_gemm_wgrad(host(gT), host(gTs), host(xT), host(xTs), off)
+    assert rel_frob(host(dw), want) < GEMM_TOL
+    for e in range(E):
+        if off[e + 1] == off[e]:
+            assert bool((dw[e] == 0).all()), e
+    # accumulate = 1 adds (and leaves empty experts untouched)
+    ff8.ff8_grouped_gemm_wgrad(gT, gTs, xT, xTs, offsets, dw, accumulate=True)
+    torch.cuda.synchronize()
+    assert rel_frob(host(dw), 2 * want) < GEMM_TOL
+
+
+def _swiglu_check(got_q, got_s, want_q, want_s, exact_vals, err_bound):
+    """Both sides quantize the same activation; the device evaluates it in float32.
+
+    err_bound[i] bounds |device value - exact value| for element i (float32 evaluation
+    error, taken against the magnitude of the terms before any cancellation).  Then:
+    a scale may differ only where the tile amax is within the tile's bound of a
+    power-of-two edge 448 * 2^T; a byte may differ only by one code and only where the
+    exact scaled value is within its bound of a rounding midpoint; and the dequantized
+    tensors agree within 2e-3 relative Frobenius.
+    """
+    gq, gs = np.asarray(got_q), np.asarray(got_s)
+    assert rel_frob(quant.dequant_rowwise(gq, gs), quant.dequant_rowwise(want_q, want_s)) < 2e-3
+    rows, cols = gq.shape
+    amax = np.abs(exact_vals).reshape(rows, cols // 128, 128).max(axis=2)
+    tile_bound = err_bound.reshape(rows, cols // 128, 128).max(axis=2)
+    t = quant.exponent_of_scale(want_s)
+    edge = np.abs(amax - 448.0 * np.ldexp(1.0, t)) <= tile_bound
+    edge |= np.abs(amax - 448.0 * np.ldexp(1.0, t - 1)) <= tile_bound
+    sdiff = gs != want_s
+    assert not np.any(sdiff & ~edge), np.argwhere(sdiff & ~edge)[:5]
+    same_scale = np.repeat(~sdiff, 128, axis=1)
+    bdiff = (gq != want_q) & same_scale
+    assert bdiff.mean() < 1e-3, bdiff.mean()
+    if bdiff.any():
+        sc = np.repeat(want_s.astype(np.float64), 128, axis=1)[bdiff]
+        a = np.abs(exact_vals[bdiff]) / sc
+        mags = codec.e4m3_decode(np.arange(127, dtype=np.uint8))
+        hi = np.clip(np.searchsorted(mags, a), 1, 126)
+        mid = (mags[hi - 1] + mags[hi]) / 2
+        near = np.abs(a - mid) <= err_bound[bdiff] / sc
+        assert near.all(), (a[~near][:5], mid[~near][:5], (err_bound[bdiff] / sc)[~near][:5])
+        steps = (gq[bdiff].astype(np.int64) & 0x7F) - (want_q[bdiff].astype(np.int64) & 0x7F)
+        assert np.all(np.abs(steps) <= 1)
+
+
+# float32 evaluation of exp, reciprocal and a few products: well under 64 ulp of the
+# pre-cancellation magnitude for |g| <= 16 (exp's error grows like |g| ulp).
+F32_EVAL = 64 * 2.0 ** -24
+
+
+def _swiglu_bounds(a64, dh64):
+    I = a64.shape[1] // 2
+    g, u = a64[:, :I], a64[:, I:]
+    sig = 1.0 / (1.0 + np.exp(-g))
+    fwd = F32_EVAL * np.abs(g * sig * u) + 1e-30
+    dg = F32_EVAL * np.abs(dh64 * u * sig) * (1.0 + np.abs(g) * (1.0 - sig)) + 1e-30
+    du = F32_EVAL * np.abs(dh64 * g * sig) + 1e-30
+    return fwd, np.concatenate([dg, du], axis=1)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_swiglu_fwd_bwd(case):
+    shape, inp = _inputs(case)
+    I, E = shape.I, shape.E
+    M_cap = 1024
+    a = workloads.randn_bf16((M_cap, 2 * I), 2.0, seed=8)
+    dh = workloads.randn_bf16((M_cap, I), 1.0, seed=9)
+    offsets = dev(torch.tensor([0, 256, 256, 640, 896][: min(5, E + 1)] + [896] * max(0, E + 1 - 5),
+                               dtype=torch.int32))
+    m_pad = 896
+    hq = poisoned((M_cap, I), torch.uint8)
+    hs = poisoned((M_cap, I // 128), torch.float32)
+    ff8.ff8_swiglu_quant(dev(a), hq, hs, offsets, E)
+    daq = poisoned((M_cap, 2 * I), torch.uint8)
+    das = poisoned((M_cap, 2 * I // 128), torch.float32)
+    ff8.ff8_swiglu_bwd_quant(dev(a), dev(dh), daq, das, offsets, E)
+    torch.cuda.synchronize()
+    a64, dh64 = f64(a)[:m_pad], f64(dh)[:m_pad]
+    h = moe.swiglu(a64)
+    b_fwd, b_bwd = _swiglu_bounds(a64, dh64)
+    wq, ws = quant.quant_rowwise(h)
+    _swiglu_check(host(hq[:m_pad]), host(hs[:m_pad]), wq, ws, h, b_fwd)
+    assert untouched(hq[m_pad:]) and untouched(hs[m_pad:])
+    da = moe.swiglu_bwd(a64, dh64)
+    wq2, ws2 = quant.quant_rowwise(da)
+    _swiglu_check(host(daq[:m_pad]), host(das[:m_pad]), wq2, ws2, da, b_bwd)
+    assert untouched(daq[m_pad:])
+
+
+@pytest.mark.parametrize("k", [1, 2, 8])
+def test_unpermute(k):
+    T, H, E = 500, 256, 8
+    shape = workloads.LayerShape("u", T, H, E, k, 128, "iid")
+    idx, probs = workloads.routing(shape, seed=k)
+    idx = idx.clone()
+    if k > 1:
+        idx[::5, 0] = -1
+    _, off, row_map, _ = moe.route(host(idx), E)
+    M_cap = ff8.ff8_rows_bound(T, k, E)
+    yp = workloads.randn_bf16((M_cap, H), 1.0, seed=4)
+    for w in (None, probs):
+        y = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+        ff8.ff8_unpermute(dev(yp), dev(torch.from_numpy(row_map.astype(np.int32))), None if w is None else dev(w), y)
+        torch.cuda.synchronize()
+        want = moe.unpermute(f64(yp), row_map, None if w is None else host(w))
+        got = f64(y)
+        if k == 1 and w is None:
+            assert np.array_equal(got, want)
+        ulp = np.ldexp(1.0, np.frexp(np.maximum(np.abs(want), 1e-30))[1] - 8)
+        assert np.all(np.abs(got - want) <= ulp + 1e-6), np.max(np.abs(got - want) / ulp)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_layer_stagewise(case):
+    """Whole forward+backward through ExpertLayerFP8; every stage is checked against the
+    oracle applied to the GPU's own upstream outputs (no error compounding)."""
+    shape, inp = _inputs(case)
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
+    d = {k: dev(v) for k, v in inp.items()}
+    L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
+    torch.cuda.synchronize()
+    b = {k: v for k, v in L.buf.items()}
+    off = host(b["offsets"]).astype(np.int64)
+    m_pad = int(off[-1])
+    w = olayer.quantize_weights(f64(inp["w1"]), f64(inp["w2"]))
+    for n in ("w1q", "w1s", "w2q", "w2s"):
+        assert np.array_equal(host(b[n]), w[n]), n
+    counts, w_off, w_map, w_src = moe.route(host(inp["topk_idx"]), shape.E)
+    assert np.array_equal(off, w_off) and np.array_equal(host(b["row_map"]), w_map)
+    xq, xs = moe.permute_quant_rows(f64(inp["x"]), w_src, shape.k)
+    assert np.array_equal(host(b["xq"][:m_pad]), xq) and np.array_equal(host(b["xs"][:m_pad]), xs)
+    A = moe.grouped_gemm_fprop(xq, xs, w["w1q"], w["w1s"], off)
+    assert rel_frob(f64(b["a"][:m_pad]), A) < GEMM_TOL
+    a_gpu = f64(b["a"][:m_pad])
+    h = moe.swiglu(a_gpu)
+    hq, hs = quant.quant_rowwise(h)
+    _swiglu_check(host(b["hq"][:m_pad]), host(b["hs"][:m_pad]), hq, hs, h, _swiglu_bounds(a_gpu, a_gpu[:, :1])[0])
+    Y = moe.grouped_gemm_fprop(host(b["hq"]), host(b["hs"]), w["w2q"], w["w2s"], off)
+    assert rel_frob(f64(b["y_perm"][:m_pad]), Y) < GEMM_TOL
+    y = moe.unpermute(f64(b["y_perm"][:m_pad]), w_map, host(inp["probs"]))
+    assert rel_frob(f64(b["y"]), y) < 1e-3
+    dyq, dys = moe.permute_quant_rows(f64(inp["dy"]), w_src, shape.k, row_w=host(inp["probs"]))
+    assert np.array_equal(host(b["dyq"][:m_pad]), dyq) and np.array_equal(host(b["dys"][:m_pad]), dys)
+    dH = moe.grouped_gemm_dgrad(dyq, dys, w["w2q"], w["w2s"], off)
+    assert rel_frob(f64(b["dh"][:m_pad]), dH) < GEMM_TOL
+    dh_gpu = f64(b["dh"][:m_pad])
+    da = moe.swiglu_bwd(a_gpu, dh_gpu)
+    daq, das = quant.quant_rowwise(da)
+    _swiglu_check(host(b["daq"][:m_pad]), host(b["das"][:m_pad]), daq, das, da, _swiglu_bounds(a_gpu, dh_gpu)[1])
+    dXp = moe.grouped_gemm_dgrad(host(b["daq"][:m_pad]), host(b["das"][:m_pad]), w["w1q"], w["w1s"], off)
+    assert rel_frob(f64(b["dx_perm"][:m_pad]), dXp) < GEMM_TOL
+    dx = moe.unpermute(f64(b["dx_perm"][:m_pad]), w_map, None)
+    assert rel_frob(f64(b["dx"]), dx) < 1e-3
+    for name in ("x", "h", "dy", "da"):
+        qT, sT = sat.scaling_aware_transpose(host(b[name + "q"][:m_pad]), host(b[name + "s"][:m_pad]))
+        assert np.array_equal(host(b[name + "Tq"][:, :m_pad]), qT), name
+        assert np.array_equal(host(b[name + "Ts"][:, : m_pad // 128]), sT), name
+    dW2 = moe.grouped_gemm_wgrad(host(b["dyTq"]), host(b["dyTs"]), host(b["hTq"]), host(b["hTs"]), off)
+    assert rel_frob(host(b["dw2"]), dW2) < GEMM_TOL
+    dW1 = moe.grouped_gemm_wgrad(host(b["daTq"]), host(b["daTs"]), host(b["xTq"]), host(b["xTs"]), off)
+    assert rel_frob(host(b["dw1"]), dW1) < GEMM_TOL
