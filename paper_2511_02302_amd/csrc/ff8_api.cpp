@@ -142,6 +142,11 @@ static int gemm_common(const char* fn, const void* a, const void* as, const void
   if (E < 1) return fail(FF8_ERR_ARG, "%s: E must be >= 1", fn);
   if (!mult128(M_cap) || !mult128(N) || !mult128(K))
     return fail(FF8_ERR_SHAPE, "%s: M_cap, N and K must be positive multiples of 128", fn);
+  // the kernels address each operand tensor (one expert's weight, the token-major
+  // activations) with 32-bit byte offsets
+  const int64_t lim = (int64_t)1 << 32;
+  if (M_cap * (N > K ? N : K) >= lim || N * K >= lim)
+    return fail(FF8_ERR_SHAPE, "%s: an operand exceeds 4 GiB (M_cap*max(N,K) and N*K must be < 2^32)", fn);
   return FF8_OK;
 }
 

@@ -8,18 +8,26 @@
 //   dgrad: p = k (W_e columns),     q = token row m, k = n     -> out[m, k] bf16
 //   wgrad: p = k (xT rows),         q = n (gT rows), k = token -> dw[e, n, k] fp32
 //
-// MFMA: v_mfma_scale_f32_32x32x64_f8f6f4 (e4m3 x e4m3).  The library's scales are
-// powers of two, i.e. exactly E8M0 values (the fp32 exponent field), so each 128-wide
-// K block's scales are applied by the matrix core itself, per P row and per Q column,
-// inside the float32 accumulation -- no VALU scale-promotion pass.
+// Matrix core: v_mfma_scale_f32_32x32x64_f8f6f4 (e4m3 x e4m3, fp32 accumulate).  The
+// library's scales are powers of two, i.e. exactly E8M0 values (the fp32 exponent
+// field), so the per-128 block scales of both operands are applied by the MFMA itself,
+// per P row and per Q column, inside the fp32 accumulation -- no VALU promotion pass.
 //
-// Tiling: 256 (p) x 256 (q) x 128 (k) per workgroup, 4 waves in 2 x 2, each wave
-// 128 x 128 = 4 x 4 MFMA tiles (256 accumulator registers).  LDS holds two stages of
-// both operand tiles (2 x 64 KB) plus their E8M0 scale bytes; global loads for step
-// k+1 are in flight while step k runs on the matrix cores.  K-major tiles use a 16-byte
-// XOR swizzle (chunk ^ row%8), so the 16-byte fragment reads are bank-conflict-free.
-// dgrad reads W_e in its stored [n][k] orientation with ds_read_b64_tr_b8, which
-// transposes 8x8 byte blocks across lanes on the way out of LDS.
+// Tiling: 256 (p) x 256 (q) per workgroup, 4 waves in 2 x 2, each wave 128 x 128 =
+// 4 x 4 MFMA tiles (256 accumulators in AGPRs).  K advances 128 per stage (one scale
+// block), in two half-steps of 64 (16 MFMAs each).
+// Data movement is sized for the L2, whose request rate is the binding limit: every
+// operand row segment of a stage is one whole 128-byte line, loaded by
+// global_load_lds_dwordx4 straight into LDS (8 lanes per line, no register staging);
+// the scales of four K blocks arrive in one batch (four lanes per row line).  Two
+// stage buffers: the DMA of stage s+2 is issued, spread over the MFMAs, during the
+// second half of stage s, once a barrier has shown every wave done with stage s's
+// buffer and stage s+1 landed.  Fragments are double buffered in VGPRs (one set per
+// half-step), and LDS reads are threaded one or two per MFMA.
+// K-major tiles (128-byte rows) use the 16-byte XOR swizzle chunk ^ ((r ^ r>>3) & 7),
+// conflict-free for the fragment reads.  dgrad reads W_e in its stored [n][k]
+// orientation (256-byte rows) with ds_read_b64_tr_b8, which transposes 8x8 byte
+// blocks across lanes; its rows use the swizzle chunk ^ ((2j ^ j>>2) & 15), j = n%8.
 //
 // Grouped scheduling is on the device: tiles are counted per expert from offsets
 // (no host sync); surplus workgroups of the host-sized grid exit at once.
@@ -33,12 +41,31 @@ namespace {
 
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 constexpr int kThreads = 256;
-constexpr int kTP = 256;  // p tile
-constexpr int kTQ = 256;  // q tile
-constexpr int kTK = 128;  // k step (one scale block)
-constexpr int kStageBytes = kTP * kTK + kTQ * kTK;  // 64 KB
+constexpr int kTP = 256;   // p tile
+constexpr int kTQ = 256;   // q tile
+constexpr int kBK = 128;   // k per stage (one scale block)
+constexpr int kBQ = 8;     // q tiles per XCD block
+constexpr int kBP = 4;     // p tiles per XCD block
+static_assert(kBQ * kBP == 32, "an XCD block is the 32 workgroups one XCD runs at once");
+constexpr int kTileBytes = kTP * kBK;  // 32 KB per operand per stage
+constexpr int kScaleBatch = 4;         // K blocks per scale batch
+
+__shared__ __attribute__((aligned(1024))) uint8_t g_st0[2 * kTileBytes], g_st1[2 * kTileBytes];  // [P | Q]
+__shared__ __attribute__((aligned(1024))) float g_sc[2][2 * kTP * kScaleBatch];  // [P rows x 4 | Q rows x 4]
+__shared__ int g_cum[1025];
+
+template <int B> __device__ __forceinline__ uint8_t* stage_buf() {
+  if constexpr (B == 0) return g_st0; else return g_st1;
+}
+template <int B> __device__ __forceinline__ uint32_t stage_lds() {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)stage_buf<B>();
+}
+__device__ __forceinline__ uint32_t scale_lds(int b) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float*)&g_sc[b][0];
+}
 
 struct GemmArgs {
   const uint8_t* P;   // fprop: w; dgrad: w; wgrad: xT
@@ -56,244 +83,367 @@ struct GemmArgs {
   int accumulate;
 };
 
-__device__ __forceinline__ int xcd_remap(int bid, int n) {
-  const int xcd = bid & 7, slot = bid >> 3, q = n >> 3, r = n & 7;
-  return xcd * q + (xcd < r ? xcd : r) + slot;
+// K-major stage tile: 256 rows x 128 bytes, 16-byte chunk c of row r at c ^ kswz(r).
+__device__ __forceinline__ int kswz(int r) { return (r ^ (r >> 3)) & 7; }
+// dgrad weight stage tile: 128 rows (n) x 256 bytes, chunk c of row n at c ^ wswz(n % 8).
+__device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
+
+// LDS DMA: each lane loads 16 (or 4) bytes from sbase + voff into LDS at M0 + 16 * lane
+// (or 4 * lane).  Issued through inline asm so that the compiler does not serialize the
+// pipeline with conservative waits; the kernel waits for its own DMA (vmcnt) before the
+// barrier that publishes a stage.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" : : "{m0}"(lds_off), "v"(voff), "s"(sbase) : "memory");
+}
+__device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dword %1, %2" : : "{m0}"(lds_off), "v"(voff), "s"(sbase) : "memory");
 }
 
-__device__ __forceinline__ uint32_t e8m0(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
+__device__ __forceinline__ uint32_t e8m0(float s) { return __float_as_uint(s) >> 23; }
 
-// One scaled MFMA on sub-tile (A, B); the opsel byte selectors must be constants.
-template <int A, int B>
-__device__ __forceinline__ void mma(f32x16 (&acc)[4][4], const i32x8 (&fp)[4], const i32x8 (&fq)[4], int sp, int sq) {
-  acc[A][B] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp[A], fq[B], acc[A][B], 0, 0, A, sp, B, sq);
-}
-template <int A>
-__device__ __forceinline__ void mma_row(f32x16 (&acc)[4][4], const i32x8 (&fp)[4], const i32x8 (&fq)[4], int sp,
-                                        int sq) {
-  mma<A, 0>(acc, fp, fq, sp, sq);
-  mma<A, 1>(acc, fp, fq, sp, sq);
-  mma<A, 2>(acc, fp, fq, sp, sq);
-  mma<A, 3>(acc, fp, fq, sp, sq);
+__device__ __forceinline__ i32x8 with_half(i32x8 f, const u32x4& x, int half) {
+  f[4 * half + 0] = (int)x[0];
+  f[4 * half + 1] = (int)x[1];
+  f[4 * half + 2] = (int)x[2];
+  f[4 * half + 3] = (int)x[3];
+  return f;
 }
 
-__device__ __forceinline__ int kmaj_off(int r, int c) { return r * kTK + ((c ^ (r & 7)) << 4); }
-__device__ __forceinline__ int wt_off(int n, int c) { return n * kTP + ((c ^ (n & 7)) << 4); }
+// Per-thread state of one workgroup tile.
+template <int MODE>
+struct Tile {
+  f32x16 acc[4][4];
+  i32x8 fpA[4], fqA[4], fpB[4], fqB[4];  // set A: first half-step, set B: second
+  int sp, sq;          // packed E8M0 scales of the stage being multiplied
+  uint32_t scp, scq;   // packed scales of the next stage, assembled while it is read
+  // DMA sources: wave-uniform bases, per-lane 32-bit byte offsets
+  const uint8_t* p_base;
+  const uint8_t* q_base;
+  const float* sp_base;
+  const float* sq_base;
+  uint32_t p_off[8], q_off[8];   // tile DMA instruction i, stage 0
+  uint32_t sp_off[4], sq_off[4]; // scale DMA instruction i, K block 0 (before the lane's block index)
+  int64_t p_kstep;               // bytes per stage of the P source
+  int sp_kb;                     // floats per K block of the P scale source (q scales: 1)
+  int wave, lane, wp, wq;
+  int64_t nk;
+
+  // Tile DMA instruction I (0..15) of stage ks into stage buffer B: 0-7 P, 8-15 Q.
+  template <int B, int I>
+  __device__ __forceinline__ void dma_tile(int64_t ks) {
+    const uint32_t base = stage_lds<B>() + (uint32_t)wave * 8192u;  // the wave's 8 KB slice of each tile
+    if constexpr (I < 8) dma16(p_base + ks * p_kstep, p_off[I], base + I * 1024);
+    else dma16(q_base + ks * kBK, q_off[I - 8], base + kTileBytes + (I - 8) * 1024);
+  }
+  // Scale DMA instruction I (0..7) of batch b (K blocks 4b..4b+3, clamped to the last
+  // block): 0-3 P, 4-7 Q.  Lane l loads block 4b + l%4 of tile row (wave*4+i)*16 + l/4.
+  template <int I>
+  __device__ __forceinline__ void dma_scale(int64_t b) {
+    int64_t kb = b * kScaleBatch + (lane & 3);
+    kb = kb < nk ? kb : nk - 1;
+    const uint32_t lbase = scale_lds((int)(b & 1)) + (uint32_t)wave * 1024u;
+    if constexpr (I < 4) dma4(sp_base, sp_off[I] + (uint32_t)(kb * sp_kb * 4), lbase + I * 256);
+    else dma4(sq_base, sq_off[I - 4] + (uint32_t)(kb * 4), lbase + kTP * kScaleBatch * 4 + (I - 4) * 256);
+  }
+
+  // Fragment read J of half h of stage buffer B into register set kSetA.
+  //   fprop / wgrad: J 0..15, 16-byte reads: J < 8 -> fq[J/2] half J%2, else fp[(J-8)/2].
+  //   dgrad: J 0..7 as above for fq; J 8..23 -> fp[(J-8)/4], transposing read (J-8)%4.
+  template <int B, int H, bool kSetA, int J>
+  __device__ __forceinline__ void read_op() {
+    i32x8 (&fp)[4] = kSetA ? fpA : fpB;
+    i32x8 (&fq)[4] = kSetA ? fqA : fqB;
+    const int l31 = lane & 31, g = lane >> 5;
+    const uint8_t* P = stage_buf<B>();
+    const uint8_t* Q = stage_buf<B>() + kTileBytes;
+    if constexpr (J < 8) {
+      const int r = 128 * wq + 32 * (J / 2) + l31;
+      const u32x4 x = *reinterpret_cast<const u32x4*>(Q + r * kBK + (((4 * H + 2 * g + (J % 2)) ^ kswz(r)) << 4));
+      fq[J / 2] = with_half(fq[J / 2], x, J % 2);
+    } else if constexpr (MODE != kDgrad) {
+      const int a = (J - 8) / 2, half = (J - 8) % 2;
+      const int r = 128 * wp + 32 * a + l31;
+      const u32x4 x = *reinterpret_cast<const u32x4*>(P + r * kBK + (((4 * H + 2 * g + half) ^ kswz(r)) << 4));
+      fp[a] = with_half(fp[a], x, half);
+    } else {
+      const int a = (J - 8) / 4, rr = (J - 8) % 4;
+      const int gg = lane >> 4, hh = lane & 1, ii = (lane & 15) >> 1;
+      const int kl = 128 * wp + 32 * a + 16 * (gg & 1) + 8 * hh;
+      const int n = 64 * H + 32 * (gg >> 1) + 8 * rr + ii;
+      const uint8_t* addr = P + n * kTP + (((kl >> 4) ^ wswz(ii)) << 4) + (kl & 15);
+      const i32x2 t =
+          __builtin_amdgcn_ds_read_tr8_b64_v2i32((i32x2 __attribute__((address_space(3)))*)((lds_u8*)addr));
+      fp[a][2 * rr] = t[0];
+      fp[a][2 * rr + 1] = t[1];
+    }
+  }
+  static constexpr int kFragReads = (MODE == kDgrad) ? 24 : 16;
+  template <int B, int H, bool kSetA, int J>
+  __device__ __forceinline__ void read_all_from() {
+    if constexpr (J < kFragReads) {
+      read_op<B, H, kSetA, J>();
+      read_all_from<B, H, kSetA, J + 1>();
+    }
+  }
+  // Scale read R (0..7) of stage ks: R < 4 -> the P row 128 wp + 32 R + l of this lane,
+  // else the Q row 128 wq + 32 (R-4) + l; byte R%4 of the packed word.
+  template <int R>
+  __device__ __forceinline__ void read_scale(int64_t ks) {
+    const float* S = &g_sc[(ks >> 2) & 1][0];
+    const int j = (int)(ks & 3), l31 = lane & 31;
+    if constexpr (R < 4) {
+      const uint32_t v = e8m0(S[(128 * wp + 32 * R + l31) * kScaleBatch + j]);
+      scp = (R == 0) ? v : (scp | (v << (8 * R)));
+    } else {
+      const uint32_t v = e8m0(S[kTP * kScaleBatch + (128 * wq + 32 * (R - 4) + l31) * kScaleBatch + j]);
+      scq = (R == 4) ? v : (scq | (v << (8 * (R - 4))));
+    }
+  }
+
+  template <bool kSetA, int I>
+  __device__ __forceinline__ void mfma_op() {
+    i32x8 (&fp)[4] = kSetA ? fpA : fpB;
+    i32x8 (&fq)[4] = kSetA ? fqA : fqB;
+    constexpr int A = I / 4, Bq = I % 4;
+    acc[A][Bq] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp[A], fq[Bq], acc[A][Bq], 0, 0, A, sp, Bq, sq);
+  }
+
+  // First half-step of stage ks (buffer B): MFMAs on set A, reads of the second half
+  // (same buffer) into set B.
+  template <int B, int I>
+  __device__ __forceinline__ void half0_from(int64_t ks) {
+    if constexpr (I < 16) {
+      mfma_op<true, I>();
+      if constexpr (MODE == kDgrad) {
+        if constexpr (I < 8) read_op<B, 1, false, I>();
+        read_op<B, 1, false, 8 + I>();
+      } else {
+        read_op<B, 1, false, I>();
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      half0_from<B, I + 1>(ks);
+    }
+  }
+  // Second half-step: MFMAs on set B with the DMA of stage ks+2 into buffer B (free
+  // now), the scale batch of the next four stages when ks % 4 == 0, and the reads of
+  // stage ks+1's first half (other buffer) and scales, threaded between them.
+  template <int B, int S4, int I>
+  __device__ __forceinline__ void half1_from(int64_t ks_dma, int64_t ks_next) {
+    if constexpr (I < 16) {
+      mfma_op<false, I>();
+      dma_tile<B, I>(ks_dma);
+      if constexpr (S4 == 0 && I < 8) dma_scale<I>((ks_next >> 2) + 1);
+      if constexpr (MODE == kDgrad) {
+        if constexpr (I < 8) read_op<1 - B, 0, true, I>();
+        read_op<1 - B, 0, true, 8 + I>();
+      } else {
+        read_op<1 - B, 0, true, I>();
+      }
+      if constexpr (I >= 8) read_scale<I - 8>(ks_next);
+      __builtin_amdgcn_sched_barrier(0);
+      half1_from<B, S4, I + 1>(ks_dma, ks_next);
+    }
+  }
+
+  // Stage ks, S4 = ks % 4 (buffer S4 % 2).  Between the halves, wait for this wave's DMA
+  // (stage ks+1, and the scale batch) and its reads of stage ks, then barrier: stage
+  // ks+1 is visible to all and buffer ks % 2 is free for stage ks+2.  Stages past the
+  // end are reloads of the last one (in bounds, never multiplied).
+  template <int S4>
+  __device__ __forceinline__ void stage(int64_t ks) {
+    constexpr int B = S4 % 2;
+    half0_from<B, 0>(ks);
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    half1_from<B, S4, 0>(ks + 2 < nk ? ks + 2 : nk - 1, ks + 1);
+    sp = (int)scp;
+    sq = (int)scq;
+  }
+};
 
 template <int MODE>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  uint8_t* sc_base = smem + 2 * kStageBytes;  // [2][512] scale bytes: sP then sQ
-  __shared__ int cum[1025];
+  const int tid = threadIdx.x;
+  Tile<MODE> T;
+  T.lane = tid & 63;
+  T.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  T.wp = T.wave & 1;
+  T.wq = T.wave >> 1;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wp = wave & 1, wq = wave >> 1;
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  // ---- tile order ----
+  // Workgroups are dispatched round-robin over the 8 XCDs (32 CUs each).  Each XCD
+  // works on blocks of kBQ x kBP = 32 tiles (q-tiles x p-tiles), so its 32 resident
+  // workgroups share 8 q panels and 4 p panels per K step in its L2; consecutive blocks
+  // go to consecutive XCDs with the p-block fastest, so the 8 XCDs together sweep one
+  // 16 x 16-tile window (about one expert) at a time and its operands stay in the MALL.
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int blk = (slot >> 5) * 8 + xcd, w_in = slot & 31;
+  const int n_pb = (g.n_pt + kBP - 1) / kBP;
+  const int qb = blk / n_pb, pb = blk - qb * n_pb;
+  const int qg = qb * kBQ + w_in / kBP;  // global q-tile index
+  const int pt = pb * kBP + w_in % kBP;
+  if (pt >= g.n_pt) return;
 
-  // ---- tile decode ----
-  int e, pt;
-  int64_t q0, q_end, k0, nk;
+  // ---- tile decode (uniform) ----
+  int e;
+  int64_t q0, q_end, k0;
   if (MODE != kWgrad) {
-    for (int i = tid; i < g.E; i += kThreads) cum[i + 1] = (g.offsets[i + 1] - g.offsets[i] + kTQ - 1) / kTQ;
-    __syncthreads();
-    if (tid == 0) {
-      int acc = 0;
-      cum[0] = 0;
-      for (int i = 1; i <= g.E; ++i) {
-        acc += cum[i];
-        cum[i] = acc;
+    // cumulative 256-row tile counts per expert: one wave, 64 experts per pass
+    if (tid < 64) {
+      int carry = 0;
+      for (int base = 0; base < g.E; base += 64) {
+        const int i = base + tid;
+        int v = i < g.E ? (g.offsets[i + 1] - g.offsets[i] + kTQ - 1) / kTQ : 0;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const int u = __shfl_up(v, d);
+          if (tid >= d) v += u;
+        }
+        if (i < g.E) g_cum[i + 1] = carry + v;
+        carry += __shfl(v, 63);
       }
+      if (tid == 0) g_cum[0] = 0;
     }
     __syncthreads();
-    pt = logical % g.n_pt;
-    const int qg = logical / g.n_pt;
-    if (qg >= cum[g.E]) return;
+    if (qg >= g_cum[g.E]) return;
     int lo = 0, hi = g.E - 1;  // largest e with cum[e] <= qg
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      if (cum[mid] <= qg) lo = mid; else hi = mid - 1;
+      if (g_cum[mid] <= qg) lo = mid; else hi = mid - 1;
     }
-    e = lo;
-    q0 = g.offsets[e] + (int64_t)(qg - cum[e]) * kTQ;
-    q_end = g.offsets[e + 1];
+    e = __builtin_amdgcn_readfirstlane(lo);
+    const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
+    const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
+    const int c0 = __builtin_amdgcn_readfirstlane(g_cum[e]);
+    q0 = o0 + (int64_t)(qg - c0) * kTQ;
+    q_end = o1;
     k0 = 0;
-    nk = g.Kdim / kTK;
+    T.nk = g.Kdim / kBK;
   } else {
-    const int per_e = g.n_pt * g.n_qt;
-    e = logical / per_e;
-    const int rem = logical - e * per_e;
-    const int qt = rem / g.n_pt;
-    pt = rem - qt * g.n_pt;
+    if (qg >= g.E * g.n_qt) return;
+    e = qg / g.n_qt;
+    const int qt = qg - e * g.n_qt;
     q0 = (int64_t)qt * kTQ;
     q_end = g.Nq;
-    k0 = g.offsets[e];
-    nk = (g.offsets[e + 1] - k0) / kTK;
+    const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
+    const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
+    k0 = o0;
+    T.nk = (o1 - o0) / kBK;
   }
   const int64_t p0 = (int64_t)pt * kTP;
+  const int lane = T.lane, wave = T.wave;
 
-  // ---- global load assignment ----
-  // Q tile (always K-major): rows q0 + (tid>>3) + 32 i, 16-byte chunk tid & 7.
+  // ---- DMA sources (lane l of tile DMA instruction i writes LDS bytes 16 l .. of 1 KB) ----
   const int64_t q_ld = (MODE == kWgrad) ? g.M_cap : g.Kdim;
-  const int64_t q_rows_max = (MODE == kWgrad) ? g.Nq : g.M_cap;
-  const uint8_t* qptr[8];
+  const int64_t q_rows = (MODE == kWgrad) ? g.Nq : g.M_cap;
+  T.q_base = g.Q + k0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    int64_t r = q0 + (tid >> 3) + 32 * i;
-    r = r < q_rows_max ? r : q_rows_max - 1;
-    qptr[i] = g.Q + r * q_ld + k0 + (tid & 7) * 16;
+    const int r = (wave * 8 + i) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ kswz(r);
+    int64_t row = q0 + r;
+    row = row < q_rows ? row : q_rows - 1;
+    T.q_off[i] = (uint32_t)(row * q_ld + c * 16);
   }
-  // P tile: fprop / wgrad K-major rows p0 + (tid>>3) + 32 i; dgrad W rows n (16 per pass).
-  const uint8_t* pptr[8];
-  int64_t p_step;  // bytes to advance per k step
   if (MODE == kDgrad) {
-    const uint8_t* w = g.P + (int64_t)e * g.Kdim * g.Np;  // W_e [N = Kdim][K = Np]
+    T.p_base = g.P + (int64_t)e * g.Kdim * g.Np;  // W_e [N = Kdim][K = Np]
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int n = (tid >> 4) + 16 * i;
-      int64_t col = p0 + (tid & 15) * 16;
+      const int n = (wave * 8 + i) * 4 + (lane >> 4);
+      const int c = (lane & 15) ^ wswz(n & 7);
+      int64_t col = p0 + c * 16;
       col = col < g.Np ? col : g.Np - 16;
-      pptr[i] = w + (int64_t)n * g.Np + col;
+      T.p_off[i] = (uint32_t)((int64_t)n * g.Np + col);
     }
-    p_step = (int64_t)kTK * g.Np;
+    T.p_kstep = (int64_t)kBK * g.Np;
   } else {
     const int64_t p_ld = (MODE == kWgrad) ? g.M_cap : g.Kdim;
-    const uint8_t* base = (MODE == kFprop) ? g.P + (int64_t)e * g.Np * g.Kdim : g.P;
+    T.p_base = ((MODE == kFprop) ? g.P + (int64_t)e * g.Np * g.Kdim : g.P) + k0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      int64_t r = p0 + (tid >> 3) + 32 * i;
-      r = r < g.Np ? r : g.Np - 1;
-      pptr[i] = base + r * p_ld + k0 + (tid & 7) * 16;
+      const int r = (wave * 8 + i) * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ kswz(r);
+      int64_t row = p0 + r;
+      row = row < g.Np ? row : g.Np - 1;
+      T.p_off[i] = (uint32_t)(row * p_ld + c * 16);
     }
-    p_step = kTK;
+    T.p_kstep = kBK;
   }
-  // Scales: thread tid loads the P scale of p0 + tid and the Q scale of q0 + tid.
-  const float* sp_ptr;
-  int64_t sp_step;
+  // Scale DMA: instruction i of wave w, lane l -> tile row (w*4 + i)*16 + l/4, K block
+  // (batch*4 + l%4); LDS float index (row * 4 + l%4) of the batch buffer.
   {
-    int64_t p = p0 + tid;
-    p = p < g.Np ? p : g.Np - 1;
+    const int64_t q_sld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;
+    T.sq_base = g.sQ + k0 / kTile;
     if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
-      sp_ptr = g.sP + ((int64_t)e * (g.Np / kTile) + p / kTile) * (g.Kdim / kTile);
-      sp_step = 1;
-    } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]: block (n/128, p/128)
-      sp_ptr = g.sP + (int64_t)e * (g.Kdim / kTile) * (g.Np / kTile) + p / kTile;
-      sp_step = g.Np / kTile;
+      T.sp_base = g.sP + (int64_t)e * (g.Np / kTile) * (g.Kdim / kTile);
+      T.sp_kb = 1;
+    } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]
+      T.sp_base = g.sP + (int64_t)e * (g.Kdim / kTile) * (g.Np / kTile);
+      T.sp_kb = (int)(g.Np / kTile);
     } else {  // xT_s [Np][M_cap/128]
-      sp_ptr = g.sP + p * (g.M_cap / kTile) + k0 / kTile;
-      sp_step = 1;
+      T.sp_base = g.sP + k0 / kTile;
+      T.sp_kb = 1;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = (wave * 4 + i) * 16 + (lane >> 2);
+      int64_t p = p0 + r;
+      p = p < g.Np ? p : g.Np - 1;
+      int64_t q = q0 + r;
+      q = q < q_rows ? q : q_rows - 1;
+      if (MODE == kFprop) T.sp_off[i] = (uint32_t)((p / kTile) * (g.Kdim / kTile) * 4);
+      else if (MODE == kDgrad) T.sp_off[i] = (uint32_t)((p / kTile) * 4);
+      else T.sp_off[i] = (uint32_t)(p * (g.M_cap / kTile) * 4);
+      T.sq_off[i] = (uint32_t)(q * q_sld * 4);
     }
   }
-  const float* sq_ptr;
-  {
-    int64_t q = q0 + tid;
-    q = q < q_rows_max ? q : q_rows_max - 1;
-    const int64_t ld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;
-    sq_ptr = g.sQ + q * ld + k0 / kTile;
-  }
-  const int sc_idx = (tid & 31) * 8 + (tid >> 5);  // LDS byte of p (or q) = tid
 
-  // ---- accumulators ----
-  f32x16 acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+      for (int v = 0; v < 16; ++v) T.acc[a][b][v] = 0.0f;
 
-  u32x4 rp[8], rq[8];
-  float rsp = 0.f, rsq = 0.f;
-
-  auto gload = [&](int64_t ks) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) rq[i] = ld16(qptr[i] + ks * kTK);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) rp[i] = ld16(pptr[i] + ks * p_step);
-    rsp = sp_ptr[ks * sp_step];
-    rsq = sq_ptr[ks];
-  };
-  auto lstore = [&](int s) {
-    uint8_t* P_l = (smem + s * kStageBytes);
-    uint8_t* Q_l = (smem + s * kStageBytes) + kTP * kTK;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<u32x4*>(Q_l + kmaj_off((tid >> 3) + 32 * i, tid & 7)) = rq[i];
-    if (MODE == kDgrad) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        *reinterpret_cast<u32x4*>(P_l + wt_off((tid >> 4) + 16 * i, tid & 15)) = rp[i];
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        *reinterpret_cast<u32x4*>(P_l + kmaj_off((tid >> 3) + 32 * i, tid & 7)) = rp[i];
-    }
-    uint8_t* sc = sc_base + s * 512;
-    sc[sc_idx] = (uint8_t)e8m0(rsp);
-    sc[256 + sc_idx] = (uint8_t)e8m0(rsq);
-  };
-
+  const int64_t nk = T.nk;
   if (nk > 0) {
-    gload(0);
-    lstore(0);
-  }
-  __syncthreads();
-
-  for (int64_t ks = 0; ks < nk; ++ks) {
-    const int cur = (int)(ks & 1);
-    if (ks + 1 < nk) gload(ks + 1);
-    const uint8_t* P_l = (smem + cur * kStageBytes);
-    const uint8_t* Q_l = (smem + cur * kStageBytes) + kTP * kTK;
-    const uint8_t* sc = sc_base + cur * 512;
-    const int scale_p = *reinterpret_cast<const int*>(sc + (lane & 31) * 8 + 4 * wp);
-    const int scale_q = *reinterpret_cast<const int*>(sc + 256 + (lane & 31) * 8 + 4 * wq);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      i32x8 fp[4], fq[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int r = 128 * wq + 32 * a + (lane & 31);
-        const int c0 = 4 * h + 2 * (lane >> 5);
-        const u32x4 x0 = *reinterpret_cast<const u32x4*>(Q_l + kmaj_off(r, c0));
-        const u32x4 x1 = *reinterpret_cast<const u32x4*>(Q_l + kmaj_off(r, c0 + 1));
-        fq[a] = i32x8{(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3], (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
-      }
-      if (MODE == kDgrad) {
-        const int gg = lane >> 4, hh = lane & 1, ii = (lane & 15) >> 1;
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const int kl = 128 * wp + 32 * a + 16 * (gg & 1) + 8 * hh;
-          i32x8 f;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int n = 64 * h + 32 * (gg >> 1) + 8 * r + ii;
-            const uint8_t* addr = P_l + n * kTP + (((kl >> 4) ^ (n & 7)) << 4) + (kl & 15);
-            const i32x2 t = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-                (i32x2 __attribute__((address_space(3)))*)((__attribute__((address_space(3))) uint8_t*)(addr)));
-            f[2 * r] = t[0];
-            f[2 * r + 1] = t[1];
-          }
-          fp[a] = f;
-        }
-      } else {
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const int r = 128 * wp + 32 * a + (lane & 31);
-          const int c0 = 4 * h + 2 * (lane >> 5);
-          const u32x4 x0 = *reinterpret_cast<const u32x4*>(P_l + kmaj_off(r, c0));
-          const u32x4 x1 = *reinterpret_cast<const u32x4*>(P_l + kmaj_off(r, c0 + 1));
-          fp[a] = i32x8{(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3], (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
-        }
-      }
-      mma_row<0>(acc, fp, fq, scale_p, scale_q);
-      mma_row<1>(acc, fp, fq, scale_p, scale_q);
-      mma_row<2>(acc, fp, fq, scale_p, scale_q);
-      mma_row<3>(acc, fp, fq, scale_p, scale_q);
+    // prologue: stages 0 and 1, scale batch 0; then stage 0's first-half fragments
+    T.template dma_tile<0, 0>(0); T.template dma_tile<0, 1>(0); T.template dma_tile<0, 2>(0);
+    T.template dma_tile<0, 3>(0); T.template dma_tile<0, 4>(0); T.template dma_tile<0, 5>(0);
+    T.template dma_tile<0, 6>(0); T.template dma_tile<0, 7>(0); T.template dma_tile<0, 8>(0);
+    T.template dma_tile<0, 9>(0); T.template dma_tile<0, 10>(0); T.template dma_tile<0, 11>(0);
+    T.template dma_tile<0, 12>(0); T.template dma_tile<0, 13>(0); T.template dma_tile<0, 14>(0);
+    T.template dma_tile<0, 15>(0);
+    const int64_t s1 = nk > 1 ? 1 : 0;
+    T.template dma_tile<1, 0>(s1); T.template dma_tile<1, 1>(s1); T.template dma_tile<1, 2>(s1);
+    T.template dma_tile<1, 3>(s1); T.template dma_tile<1, 4>(s1); T.template dma_tile<1, 5>(s1);
+    T.template dma_tile<1, 6>(s1); T.template dma_tile<1, 7>(s1); T.template dma_tile<1, 8>(s1);
+    T.template dma_tile<1, 9>(s1); T.template dma_tile<1, 10>(s1); T.template dma_tile<1, 11>(s1);
+    T.template dma_tile<1, 12>(s1); T.template dma_tile<1, 13>(s1); T.template dma_tile<1, 14>(s1);
+    T.template dma_tile<1, 15>(s1);
+    T.template dma_scale<0>(0); T.template dma_scale<1>(0); T.template dma_scale<2>(0);
+    T.template dma_scale<3>(0); T.template dma_scale<4>(0); T.template dma_scale<5>(0);
+    T.template dma_scale<6>(0); T.template dma_scale<7>(0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    T.template read_all_from<0, 0, true, 0>();
+    T.template read_scale<0>(0); T.template read_scale<1>(0); T.template read_scale<2>(0);
+    T.template read_scale<3>(0); T.template read_scale<4>(0); T.template read_scale<5>(0);
+    T.template read_scale<6>(0); T.template read_scale<7>(0);
+    T.sp = (int)T.scp;
+    T.sq = (int)T.scq;
+    for (int64_t ks = 0; ks < nk; ks += 4) {
+      T.template stage<0>(ks);
+      if (ks + 1 < nk) T.template stage<1>(ks + 1);
+      if (ks + 2 < nk) T.template stage<2>(ks + 2);
+      if (ks + 3 < nk) T.template stage<3>(ks + 3);
     }
-    if (ks + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs land before the workgroup retires
   }
 
   // ---- epilogue ----
+  const int wp = T.wp, wq = T.wq;
   if (MODE == kWgrad) {
     if (nk == 0 && g.accumulate) return;
     float* dw = static_cast<float*>(g.out) + (int64_t)e * g.Nq * g.Np;
@@ -312,10 +462,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
           if (g.accumulate) {
             const u32x4 old = ld16(dst);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(__uint_as_float(old[j]) + acc[a][b][4 * gr + j]);
+            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(__uint_as_float(old[j]) + T.acc[a][b][4 * gr + j]);
           } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(acc[a][b][4 * gr + j]);
+            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(T.acc[a][b][4 * gr + j]);
           }
           st16(dst, o);
         }
@@ -333,12 +483,20 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
           const int64_t p = p0 + 128 * wp + 32 * a + 8 * gr + 4 * (lane >> 5);
           if (p >= g.Np) continue;
           u32x2 o;
-          o[0] = pack_bf16x2(acc[a][b][4 * gr + 0], acc[a][b][4 * gr + 1]);
-          o[1] = pack_bf16x2(acc[a][b][4 * gr + 2], acc[a][b][4 * gr + 3]);
+          o[0] = pack_bf16x2(T.acc[a][b][4 * gr + 0], T.acc[a][b][4 * gr + 1]);
+          o[1] = pack_bf16x2(T.acc[a][b][4 * gr + 2], T.acc[a][b][4 * gr + 3]);
           st8(out + q * g.Np + p, o);
         }
       }
   }
+}
+
+// Workgroups for n_qg q-tiles x n_pt p-tiles in XCD blocks of kBQ x kBP (whole rounds of
+// 8 blocks, one per XCD); tiles past the edges exit at once.
+unsigned grid_blocks(int n_pt, int n_qg) {
+  const int64_t n_pb = (n_pt + kBP - 1) / kBP, n_qb = (n_qg + kBQ - 1) / kBQ;
+  const int64_t rounds = (n_pb * n_qb + 7) / 8;
+  return (unsigned)(rounds * 8 * kBQ * kBP);
 }
 
 }  // namespace
@@ -352,30 +510,24 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
   g.E = E;
   g.M_cap = M_cap;
   g.accumulate = accumulate;
-  const size_t smem = 2 * kStageBytes + 2 * 512;
+  g.P = b; g.sP = b_s; g.Q = a; g.sQ = a_s;
   unsigned grid;
   if (mode == kFprop) {  // out[m, n] = a[m, :] . w[e, n, :]
-    g.P = b; g.sP = b_s; g.Q = a; g.sQ = a_s;
     g.Np = N; g.Kdim = K;
     g.n_pt = (int)((N + kTP - 1) / kTP);
-    grid = (unsigned)(g.n_pt * ((M_cap + kTQ - 1) / kTQ + (E + 1) / 2));
-    (void)hipFuncSetAttribute((const void*)grouped_gemm_kernel<kFprop>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    grouped_gemm_kernel<kFprop><<<grid, kThreads, smem, st>>>(g);
+    grid = grid_blocks(g.n_pt, (int)((M_cap + kTQ - 1) / kTQ + (E + 1) / 2));
+    grouped_gemm_kernel<kFprop><<<grid, kThreads, 0, st>>>(g);
   } else if (mode == kDgrad) {  // out[m, k] = g[m, :] . w[e, :, k]
-    g.P = b; g.sP = b_s; g.Q = a; g.sQ = a_s;
     g.Np = K; g.Kdim = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
-    grid = (unsigned)(g.n_pt * ((M_cap + kTQ - 1) / kTQ + (E + 1) / 2));
-    (void)hipFuncSetAttribute((const void*)grouped_gemm_kernel<kDgrad>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    grouped_gemm_kernel<kDgrad><<<grid, kThreads, smem, st>>>(g);
+    grid = grid_blocks(g.n_pt, (int)((M_cap + kTQ - 1) / kTQ + (E + 1) / 2));
+    grouped_gemm_kernel<kDgrad><<<grid, kThreads, 0, st>>>(g);
   } else {  // dw[e, n, k] = sum_m gT[n, m] xT[k, m]
-    g.P = b; g.sP = b_s; g.Q = a; g.sQ = a_s;
     g.Np = K; g.Nq = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
     g.n_qt = (int)((N + kTQ - 1) / kTQ);
-    grid = (unsigned)(E * g.n_pt * g.n_qt);
-    (void)hipFuncSetAttribute((const void*)grouped_gemm_kernel<kWgrad>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    grouped_gemm_kernel<kWgrad><<<grid, kThreads, smem, st>>>(g);
+    grid = grid_blocks(g.n_pt, E * g.n_qt);
+    grouped_gemm_kernel<kWgrad><<<grid, kThreads, 0, st>>>(g);
   }
   return hipGetLastError();
 }
