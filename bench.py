@@ -19,6 +19,7 @@ bounded sample of the same layer.
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -27,6 +28,15 @@ sys.path.insert(0, ROOT)
 
 FP8_PEAK_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
 HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_expert_layer_dsv3.md")
+CSRC = os.path.join(ROOT, "paper_2511_02302_amd", "csrc")
+# Kernel source each stage runs; the measured traffic of a stage is only reported while
+# the hash of its source (and the shared device header) still matches the measurement.
+STAGE_SOURCE = {"F0_weight_quant": "quant.hip", "F1_permute_quant": "permute.hip", "F2_fc1_fprop": "gemm.hip",
+                "F3_swiglu_quant": "swiglu.hip", "F4_fc2_fprop": "gemm.hip", "F5_unpermute": "permute.hip",
+                "B1_permute_quant_dy": "permute.hip", "B2_fc2_dgrad": "gemm.hip", "B3_swiglu_bwd_quant": "swiglu.hip",
+                "B4_fc1_dgrad": "gemm.hip", "B5_unpermute": "permute.hip", "B6_sat_x4": "sat.hip",
+                "B7_fc2_wgrad": "gemm.hip", "B8_fc1_wgrad": "gemm.hip"}
 
 
 def parse():
@@ -177,11 +187,39 @@ def cast_ops(torch, reps=20):
     return out
 
 
-def cpu_baseline(shape, rows=128, seed=0):
+def source_hash(stage):
+    import hashlib
+    h = hashlib.sha256()
+    for f in (STAGE_SOURCE[stage], "ff8_device.hpp"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(stage):
+    """HBM bytes per launch of `stage` from the committed rocprofv3 counter summary.
+
+    The summary lists, per stage, FETCH_SIZE and WRITE_SIZE already scaled by the
+    copy-kernel calibration, and the source hash of the kernel when they were taken.
+    Returns None when there is no measurement or the kernel source has changed since.
+    """
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    for m in re.finditer(r"^traffic (\S+) (\S+) fetch_bytes=(\d+) write_bytes=(\d+)$", text, re.M):
+        name, digest, fetch, write = m.group(1), m.group(2), int(m.group(3)), int(m.group(4))
+        if name == stage:
+            return fetch + write if digest == source_hash(stage) else None
+    return None
+
+
+def cpu_baseline(shape, rows=768, seed=0):
     """The float64 oracle, as it stands, on a bounded sample of the workload.
 
     Sample: expert 0 of the layer -- its 128x128 weight quantization (F0 for one
-    expert) and one 128-row group of its routed tokens through F1..B8.  The full step
+    expert) and `rows` routed tokens of it (six 128-row groups) through F1..B8.  The full step
     runs F0 once per expert and the row work once per 128 routed rows, so the oracle's
     time for the full step is E * t(F0 sample) + (M / rows) * t(rows sample); `value`
     is the step's GEMM FLOPs over that time (the same unit as the GPU figure).
@@ -206,8 +244,8 @@ def cpu_baseline(shape, rows=128, seed=0):
     cores = len(os.sched_getaffinity(0))
     return {"value": round(flops / full_s / 1e12, 7), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
             "sample": f"expert 0 only: F0 on its W1 [{2 * shape.I}x{shape.H}] and W2 [{shape.H}x{shape.I}] "
-                      f"({t1 - t0:.1f} s), F1..B8 on one {rows}-row group of its tokens ({t2 - t1:.1f} s); "
-                      f"scaled to the full step as {shape.E} x F0 + {M // rows} x rows = {full_s:.0f} s",
+                      f"({t1 - t0:.1f} s), F1..B8 on {rows} of its routed rows ({t2 - t1:.1f} s); "
+                      f"scaled to the full step as {shape.E} x F0 + {M / rows:.1f} x rows = {full_s:.0f} s",
             "sample_seconds": round(t2 - t0, 1)}
 
 
@@ -260,12 +298,12 @@ def main():
     if kind == "mfma":
         ach = amount / (st_ms[dom] * 1e-3) / 1e12
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(ach / FP8_PEAK_TFLOPS, 4), "traffic": None,
+                "frac": round(ach / FP8_PEAK_TFLOPS, 4), "traffic": measured_traffic(dom),
                 "per_launch": {"flops": amount, "avg_ms": round(st_ms[dom], 4)}}
     else:
         ach = amount / (st_ms[dom] * 1e-3) / 1e9
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom),
                 "per_launch": {"bytes": amount, "avg_ms": round(st_ms[dom], 4)}}
 
     rec = {

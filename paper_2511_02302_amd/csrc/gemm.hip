@@ -52,6 +52,7 @@ constexpr int kBP = 4;     // p tiles per XCD block
 static_assert(kBQ * kBP == 32, "an XCD block is the 32 workgroups one XCD runs at once");
 constexpr int kTileBytes = kTP * kBK;  // 32 KB per operand per stage
 constexpr int kScaleBatch = 4;         // K blocks per scale batch
+constexpr int kDmaPerSlot = 1;         // tile DMA instructions issued per MFMA slot
 
 __shared__ __attribute__((aligned(1024))) uint8_t g_st0[2 * kTileBytes], g_st1[2 * kTileBytes];  // [P | Q]
 __shared__ __attribute__((aligned(1024))) float g_sc[2][2 * kTP * kScaleBatch];  // [P rows x 4 | Q rows x 4]
@@ -114,8 +115,11 @@ template <int MODE>
 struct Tile {
   f32x16 acc[4][4];
   i32x8 fpA[4], fqA[4], fpB[4], fqB[4];  // set A: first half-step, set B: second
-  int sp, sq;          // packed E8M0 scales of the stage being multiplied
-  uint32_t scp, scq;   // packed scales of the next stage, assembled while it is read
+  // Packed E8M0 scales of the current batch of four K blocks, per K block: byte R of
+  // cp[j] is the scale of this lane's P row 128 wp + 32 R + l (cq: Q rows); np/nq are
+  // the next batch, assembled during the last stage of the current one.
+  uint32_t cp[4], cq[4], np[4], nq[4];
+  u32x4 rsp[4], rsq[4];  // raw fp32 scale rows of the next batch, between read and pack
   // DMA sources: wave-uniform bases, per-lane 32-bit byte offsets
   const uint8_t* p_base;
   const uint8_t* q_base;
@@ -178,6 +182,7 @@ struct Tile {
     }
   }
   static constexpr int kFragReads = (MODE == kDgrad) ? 24 : 16;
+  static constexpr int kReadsPerSlot = kFragReads / 8;
   template <int B, int H, bool kSetA, int J>
   __device__ __forceinline__ void read_all_from() {
     if constexpr (J < kFragReads) {
@@ -185,61 +190,79 @@ struct Tile {
       read_all_from<B, H, kSetA, J + 1>();
     }
   }
-  // Scale read R (0..7) of stage ks: R < 4 -> the P row 128 wp + 32 R + l of this lane,
-  // else the Q row 128 wq + 32 (R-4) + l; byte R%4 of the packed word.
-  template <int R>
-  __device__ __forceinline__ void read_scale(int64_t ks) {
-    const float* S = &g_sc[(ks >> 2) & 1][0];
-    const int j = (int)(ks & 3), l31 = lane & 31;
-    if constexpr (R < 4) {
-      const uint32_t v = e8m0(S[(128 * wp + 32 * R + l31) * kScaleBatch + j]);
-      scp = (R == 0) ? v : (scp | (v << (8 * R)));
-    } else {
-      const uint32_t v = e8m0(S[kTP * kScaleBatch + (128 * wq + 32 * (R - 4) + l31) * kScaleBatch + j]);
-      scq = (R == 4) ? v : (scq | (v << (8 * (R - 4))));
-    }
+  // Scales of batch b (LDS buffer b % 2, rows of four K-block floats): read the four
+  // rows of one operand this lane multiplies (kQ: Q rows) into raw[R][j] ...
+  template <bool kQ>
+  __device__ __forceinline__ void read_scale_rows(int64_t b, u32x4 (&raw)[4]) {
+    const u32x4* S = reinterpret_cast<const u32x4*>(&g_sc[b & 1][0]);
+    const int l31 = lane & 31;
+#pragma unroll
+    for (int R = 0; R < 4; ++R)
+      raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : S[128 * wp + 32 * R + l31];
+  }
+  // ... and pack them: word j holds the E8M0 byte (the fp32 exponent field of a
+  // positive power of two) of row R in byte R.
+  __device__ __forceinline__ static void pack_scales(const u32x4 (&raw)[4], uint32_t (&dst)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      dst[j] = (raw[0][j] >> 23) | ((raw[1][j] >> 15) & 0xff00u) | ((raw[2][j] >> 7) & 0xff0000u) |
+               ((raw[3][j] << 1) & 0xff000000u);
   }
 
-  template <bool kSetA, int I>
+  template <bool kSetA, int S4, int I>
   __device__ __forceinline__ void mfma_op() {
     i32x8 (&fp)[4] = kSetA ? fpA : fpB;
     i32x8 (&fq)[4] = kSetA ? fqA : fqB;
     constexpr int A = I / 4, Bq = I % 4;
-    acc[A][Bq] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp[A], fq[Bq], acc[A][Bq], 0, 0, A, sp, Bq, sq);
+    acc[A][Bq] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp[A], fq[Bq], acc[A][Bq], 0, 0, A, (int)cp[S4], Bq,
+                                                                   (int)cq[S4]);
   }
-
-  // First half-step of stage ks (buffer B): MFMAs on set A, reads of the second half
-  // (same buffer) into set B.
-  template <int B, int I>
-  __device__ __forceinline__ void half0_from(int64_t ks) {
-    if constexpr (I < 16) {
-      mfma_op<true, I>();
-      if constexpr (MODE == kDgrad) {
-        if constexpr (I < 8) read_op<B, 1, false, I>();
-        read_op<B, 1, false, 8 + I>();
-      } else {
-        read_op<B, 1, false, I>();
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      half0_from<B, I + 1>(ks);
+  // Tile DMA instructions of second-half slot I (kDmaPerSlot per slot from slot 0), and
+  // the scale batch's eight spread over the same slots.
+  template <int B, int S4, int I, int D>
+  __device__ __forceinline__ void dma_slot(int64_t ks_dma, int64_t ks_next) {
+    if constexpr (D < kDmaPerSlot && kDmaPerSlot * I + D < 16) {
+      dma_tile<B, kDmaPerSlot * I + D>(ks_dma);
+      if constexpr (S4 == 0 && (kDmaPerSlot * I + D) % 2 == 0) dma_scale<(kDmaPerSlot * I + D) / 2>((ks_next >> 2) + 1);
+      dma_slot<B, S4, I, D + 1>(ks_dma, ks_next);
     }
   }
-  // Second half-step: MFMAs on set B with the DMA of stage ks+2 into buffer B (free
-  // now), the scale batch of the next four stages when ks % 4 == 0, and the reads of
-  // stage ks+1's first half (other buffer) and scales, threaded between them.
+  template <int B, int H, bool kSetA, int I>
+  __device__ __forceinline__ void reads_of_slot() {
+    if constexpr (I < 8) {
+      read_op<B, H, kSetA, kReadsPerSlot * I>();
+      read_op<B, H, kSetA, kReadsPerSlot * I + 1>();
+      if constexpr (kReadsPerSlot == 3) read_op<B, H, kSetA, kReadsPerSlot * I + 2>();
+    }
+  }
+
+  // First half-step of stage ks (buffer B): MFMAs on set A; the reads of the second
+  // half (same buffer) into set B go out over the first eight MFMAs, so that they have
+  // landed by the barrier.
+  template <int B, int S4, int I>
+  __device__ __forceinline__ void half0_from() {
+    if constexpr (I < 16) {
+      mfma_op<true, S4, I>();
+      reads_of_slot<B, 1, false, I>();
+      __builtin_amdgcn_sched_barrier(0);
+      half0_from<B, S4, I + 1>();
+    }
+  }
+  // Second half-step: MFMAs on set B.  The DMA of stage ks+2 into buffer B (free now)
+  // and, when ks % 4 == 0, the next scale batch are issued over the first four MFMAs,
+  // giving them the rest of this stage and the first half of the next to land; the
+  // reads of stage ks+1's first half (other buffer) into set A follow over the first
+  // eight; in the last stage of a batch the next batch's scales are read and packed.
   template <int B, int S4, int I>
   __device__ __forceinline__ void half1_from(int64_t ks_dma, int64_t ks_next) {
     if constexpr (I < 16) {
-      mfma_op<false, I>();
-      dma_tile<B, I>(ks_dma);
-      if constexpr (S4 == 0 && I < 8) dma_scale<I>((ks_next >> 2) + 1);
-      if constexpr (MODE == kDgrad) {
-        if constexpr (I < 8) read_op<1 - B, 0, true, I>();
-        read_op<1 - B, 0, true, 8 + I>();
-      } else {
-        read_op<1 - B, 0, true, I>();
-      }
-      if constexpr (I >= 8) read_scale<I - 8>(ks_next);
+      mfma_op<false, S4, I>();
+      dma_slot<B, S4, I, 0>(ks_dma, ks_next);
+      reads_of_slot<1 - B, 0, true, I>();
+      if constexpr (S4 == 3 && I == 8) read_scale_rows<false>(ks_next >> 2, rsp);
+      if constexpr (S4 == 3 && I == 9) read_scale_rows<true>(ks_next >> 2, rsq);
+      if constexpr (S4 == 3 && I == 12) pack_scales(rsp, np);
+      if constexpr (S4 == 3 && I == 14) pack_scales(rsq, nq);
       __builtin_amdgcn_sched_barrier(0);
       half1_from<B, S4, I + 1>(ks_dma, ks_next);
     }
@@ -252,13 +275,18 @@ struct Tile {
   template <int S4>
   __device__ __forceinline__ void stage(int64_t ks) {
     constexpr int B = S4 % 2;
-    half0_from<B, 0>(ks);
+    half0_from<B, S4, 0>();
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     half1_from<B, S4, 0>(ks + 2 < nk ? ks + 2 : nk - 1, ks + 1);
-    sp = (int)scp;
-    sq = (int)scq;
+    if constexpr (S4 == 3) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        cp[j] = np[j];
+        cq[j] = nq[j];
+      }
+    }
   }
 };
 
@@ -428,11 +456,13 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     T.template read_all_from<0, 0, true, 0>();
-    T.template read_scale<0>(0); T.template read_scale<1>(0); T.template read_scale<2>(0);
-    T.template read_scale<3>(0); T.template read_scale<4>(0); T.template read_scale<5>(0);
-    T.template read_scale<6>(0); T.template read_scale<7>(0);
-    T.sp = (int)T.scp;
-    T.sq = (int)T.scq;
+    {
+      u32x4 raw[4];
+      T.template read_scale_rows<false>(0, raw);
+      T.pack_scales(raw, T.cp);
+      T.template read_scale_rows<true>(0, raw);
+      T.pack_scales(raw, T.cq);
+    }
     for (int64_t ks = 0; ks < nk; ks += 4) {
       T.template stage<0>(ks);
       if (ks + 1 < nk) T.template stage<1>(ks + 1);
