@@ -53,6 +53,7 @@ static_assert(kBQ * kBP == 32, "an XCD block is the 32 workgroups one XCD runs a
 constexpr int kTileBytes = kTP * kBK;  // 32 KB per operand per stage
 constexpr int kScaleBatch = 4;         // K blocks per scale batch
 constexpr int kDmaPerSlot = 1;         // tile DMA instructions issued per MFMA slot
+constexpr int kReadSlots = 8;          // MFMA slots of a half-step that carry fragment reads
 
 __shared__ __attribute__((aligned(1024))) uint8_t g_st0[2 * kTileBytes], g_st1[2 * kTileBytes];  // [P | Q]
 __shared__ __attribute__((aligned(1024))) float g_sc[2][2 * kTP * kScaleBatch];  // [P rows x 4 | Q rows x 4]
@@ -182,7 +183,6 @@ struct Tile {
     }
   }
   static constexpr int kFragReads = (MODE == kDgrad) ? 24 : 16;
-  static constexpr int kReadsPerSlot = kFragReads / 8;
   template <int B, int H, bool kSetA, int J>
   __device__ __forceinline__ void read_all_from() {
     if constexpr (J < kFragReads) {
@@ -227,13 +227,19 @@ struct Tile {
       dma_slot<B, S4, I, D + 1>(ks_dma, ks_next);
     }
   }
+  // Fragment reads of MFMA slot I: the half-step's kFragReads reads spread evenly over
+  // its first kReadSlots slots.
+  template <int B, int H, bool kSetA, int J, int JEnd>
+  __device__ __forceinline__ void reads_range() {
+    if constexpr (J < JEnd) {
+      read_op<B, H, kSetA, J>();
+      reads_range<B, H, kSetA, J + 1, JEnd>();
+    }
+  }
   template <int B, int H, bool kSetA, int I>
   __device__ __forceinline__ void reads_of_slot() {
-    if constexpr (I < 8) {
-      read_op<B, H, kSetA, kReadsPerSlot * I>();
-      read_op<B, H, kSetA, kReadsPerSlot * I + 1>();
-      if constexpr (kReadsPerSlot == 3) read_op<B, H, kSetA, kReadsPerSlot * I + 2>();
-    }
+    if constexpr (I < kReadSlots)
+      reads_range<B, H, kSetA, I * kFragReads / kReadSlots, (I + 1) * kFragReads / kReadSlots>();
   }
 
   // First half-step of stage ks (buffer B): MFMAs on set A; the reads of the second
@@ -473,51 +479,77 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   }
 
   // ---- epilogue ----
+  // The accumulators go out through LDS so that every global store instruction writes
+  // whole 128-byte lines (16 lanes per 256-byte bf16 row, 32 lanes per 512-byte fp32
+  // row) instead of 16-byte pieces of 32 rows.  Each wave stages its own 128 x 128
+  // sub-tile ([q][p], p contiguous) in 32 KB of the stage buffers, 16-byte chunks of row
+  // q XOR-swizzled by q, which keeps both the fragment-order writes and the row-order
+  // reads free of bank conflicts.  The barrier first retires every wave's last reads of
+  // the stage buffers (and, through each wave's own final vmcnt wait, their DMA).
   const int wp = T.wp, wq = T.wq;
+  if (MODE == kWgrad && nk == 0 && g.accumulate) return;
+  __syncthreads();
+  lds_u8* const region = (lds_u8*)((wave < 2) ? g_st0 : g_st1) + (wave & 1) * 32768;
+  const int l31 = lane & 31, h = lane >> 5;
+  const bool p_ok = p0 + 128 * wp < g.Np;  // Np is a multiple of 128: whole-wave predicate
   if (MODE == kWgrad) {
-    if (nk == 0 && g.accumulate) return;
-    float* dw = static_cast<float*>(g.out) + (int64_t)e * g.Nq * g.Np;
+    float* dw = static_cast<float*>(g.out) + (int64_t)e * g.Nq * g.Np + p0 + 128 * wp;
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int bh = 0; bh < 2; ++bh) {
+      // rows ql = 32 (b - 2 bh) + l31 of 512 bytes; chunk c = p / 4 = 8a + 2gr + h
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int64_t q = q0 + 128 * wq + 32 * b + (lane & 31);
-        if (q >= q_end) continue;
+      for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-        for (int gr = 0; gr < 4; ++gr) {
-          const int64_t p = p0 + 128 * wp + 32 * a + 8 * gr + 4 * (lane >> 5);
-          if (p >= g.Np) continue;
-          float* dst = dw + q * g.Np + p;
-          u32x4 o;
-          if (g.accumulate) {
-            const u32x4 old = ld16(dst);
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(__uint_as_float(old[j]) + T.acc[a][b][4 * gr + j]);
-          } else {
+          for (int gr = 0; gr < 4; ++gr) {
+            const int ql = 32 * bb + l31, c = 8 * a + 2 * gr + h;
+            u32x4 o;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(T.acc[a][b][4 * gr + j]);
+            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(T.acc[a][2 * bh + bb][4 * gr + j]);
+            *(__attribute__((address_space(3))) u32x4*)(region + ql * 512 + ((c ^ (ql & 31)) << 4)) = o;
           }
+#pragma unroll 4
+      for (int it = 0; it < 32; ++it) {
+        const int ql = 2 * it + h, c = l31;
+        const u32x4 v = *(__attribute__((address_space(3))) u32x4*)(region + ql * 512 + ((c ^ (ql & 31)) << 4));
+        const int64_t q = q0 + 128 * wq + 64 * bh + ql;
+        if (!p_ok || q >= q_end) continue;
+        float* dst = dw + q * g.Np + 4 * c;
+        if (g.accumulate) {
+          const u32x4 old = ld16(dst);
+          u32x4 o;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(__uint_as_float(old[j]) + __uint_as_float(v[j]));
           st16(dst, o);
+        } else {
+          st16(dst, v);
         }
       }
+    }
   } else {
-    uint16_t* out = static_cast<uint16_t*>(g.out);
+    uint16_t* out = static_cast<uint16_t*>(g.out) + p0 + 128 * wp;
+    // rows q = 32b + l31 of 256 bytes; 8-byte piece (p = 32a + 8gr + 4h) in chunk 4a + gr, half h
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int64_t q = q0 + 128 * wq + 32 * b + (lane & 31);
-        if (q >= q_end) continue;
+      for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int gr = 0; gr < 4; ++gr) {
-          const int64_t p = p0 + 128 * wp + 32 * a + 8 * gr + 4 * (lane >> 5);
-          if (p >= g.Np) continue;
+          const int ql = 32 * b + l31, m = 4 * a + gr;
           u32x2 o;
           o[0] = pack_bf16x2(T.acc[a][b][4 * gr + 0], T.acc[a][b][4 * gr + 1]);
           o[1] = pack_bf16x2(T.acc[a][b][4 * gr + 2], T.acc[a][b][4 * gr + 3]);
-          st8(out + q * g.Np + p, o);
+          *(__attribute__((address_space(3))) u32x2*)(region + ql * 256 + ((m ^ (ql & 15)) << 4) + 8 * h) = o;
         }
-      }
+#pragma unroll 4
+    for (int it = 0; it < 32; ++it) {
+      const int ql = 4 * it + (lane >> 4), c = lane & 15;
+      const u32x4 v = *(__attribute__((address_space(3))) u32x4*)(region + ql * 256 + ((c ^ (ql & 15)) << 4));
+      const int64_t q = q0 + 128 * wq + ql;
+      if (!p_ok || q >= q_end) continue;
+      st16(out + q * g.Np + 8 * c, v);
+    }
   }
 }
 
