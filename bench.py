@@ -215,7 +215,7 @@ def measured_traffic(stage):
     return None
 
 
-def cpu_baseline(shape, rows=768, seed=0):
+def cpu_baseline(shape, rows=2048, seed=0):
     """The float64 oracle, as it stands, on a bounded sample of the workload.
 
     Sample: expert 0 of the layer -- its 128x128 weight quantization (F0 for one
