@@ -86,11 +86,25 @@ __device__ __forceinline__ uint32_t max64_u32(uint32_t v) {
 }
 __device__ __forceinline__ uint32_t abs_bits(float f) { return __float_as_uint(f) & 0x7FFFFFFFu; }
 
-// Non-temporal-free plain vector loads/stores.
+// Plain vector loads/stores.
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
 __device__ __forceinline__ u32x2 ld8(const void* p) { return *reinterpret_cast<const u32x2*>(p); }
 __device__ __forceinline__ void st8(void* p, const u32x2& v) { *reinterpret_cast<u32x2*>(p) = v; }
+// Streaming (non-temporal) vector loads/stores for data touched once: the lines are
+// marked for early eviction instead of displacing reusable data in L2 / MALL.
+__device__ __forceinline__ u32x4 ldnt16(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ void stnt16(void* p, const u32x4& v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+__device__ __forceinline__ u32x2 ldnt8(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+}
+__device__ __forceinline__ void stnt8(void* p, const u32x2& v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x2*>(p));
+}
 
 // Quantize 8 values that belong to one 1x128 tile shared by 16 consecutive lanes:
 // tile amax across the 16 lanes, power-of-two scale, RNE e4m3.  Returns the 8 bytes

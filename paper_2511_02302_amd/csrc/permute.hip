@@ -127,14 +127,14 @@ __global__ __launch_bounds__(kThreads) void permute_quant_kernel(const uint16_t*
   for (int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x; it < n_items; it += stride) {
     const int64_t t = it / cpr, c = it - t * cpr;
     float v[8];
-    unpack_bf16x8(ld16(x + t * H + c * 8), v);
+    unpack_bf16x8(ldnt16(x + t * H + c * 8), v);
     if (!kWeighted) {
       int tq;
       const u32x2 r = quant8_tile16(v, tq);
       for (int j = 0; j < k; ++j) {
         const int row = row_map[t * k + j];
         if (row >= 0 && row < M_cap) {  // uniform across the 16 lanes of a tile
-          st8(q + (int64_t)row * H + c * 8, r);
+          stnt8(q + (int64_t)row * H + c * 8, r);
           if (leader) s[(int64_t)row * sh + (c >> 4)] = exp2i(tq);
         }
       }
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kThreads) void permute_quant_kernel(const uint16_t*
           for (int i = 0; i < 8; ++i) vw[i] = w * v[i];
           int tq;
           const u32x2 r = quant8_tile16(vw, tq);
-          st8(q + (int64_t)row * H + c * 8, r);
+          stnt8(q + (int64_t)row * H + c * 8, r);
           if (leader) s[(int64_t)row * sh + (c >> 4)] = exp2i(tq);
         }
       }
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __res
   const u32x4 z = {0u, 0u, 0u, 0u};
   for (int64_t i = threadIdx.x; i < (int64_t)np * c16; i += kThreads) {
     const int64_t r = r0 + pad_rows[i / c16];
-    st16(q + r * H + (i % c16) * 16, z);
+    stnt16(q + r * H + (i % c16) * 16, z);
   }
   for (int64_t i = threadIdx.x; i < (int64_t)np * sh; i += kThreads) {
     const int64_t r = r0 + pad_rows[i / sh];
@@ -197,7 +197,7 @@ __global__ __launch_bounds__(kThreads) void unpermute_kernel(const uint16_t* __r
       const int row = row_map[t * k + j];
       if (row < 0 || row >= M_cap) continue;
       float v[8];
-      unpack_bf16x8(ld16(y_perm + (int64_t)row * H + c * 8), v);
+      unpack_bf16x8(ldnt16(y_perm + (int64_t)row * H + c * 8), v);
       if (kWeighted) {
         const float w = row_w[t * k + j];
 #pragma unroll
@@ -210,9 +210,11 @@ __global__ __launch_bounds__(kThreads) void unpermute_kernel(const uint16_t* __r
     u32x4 o;
 #pragma unroll
     for (int i = 0; i < 4; ++i) o[i] = pack_bf16x2(acc[2 * i], acc[2 * i + 1]);
-    st16(y + t * H + c * 8, o);
+    stnt16(y + t * H + c * 8, o);
   }
 }
+
+constexpr int kStreamBlocksPerCU = 1 << 20;  // grid cap of the permute / unpermute kernels (none: one pass)
 
 int grid_for(int64_t items, int max_per_cu) {
   int64_t need = (items + kThreads - 1) / kThreads;
@@ -244,7 +246,7 @@ hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T
                                 int64_t M_cap, uint8_t* q, float* s, hipStream_t st) {
   const int64_t items = T * (H / 8);
   if (items > 0) {
-    const int grid = grid_for(items, 16);
+    const int grid = grid_for(items, kStreamBlocksPerCU);
     if (row_w)
       permute_quant_kernel<true><<<grid, kThreads, 0, st>>>(x, row_w, T, H, k, row_map, M_cap, q, s);
     else
@@ -258,7 +260,7 @@ hipError_t launch_unpermute(const uint16_t* y_perm, const int32_t* row_map, cons
                             int64_t H, int64_t M_cap, uint16_t* y, hipStream_t st) {
   const int64_t items = T * (H / 8);
   if (items == 0) return hipSuccess;
-  const int grid = grid_for(items, 16);
+  const int grid = grid_for(items, kStreamBlocksPerCU);
   if (row_w)
     unpermute_kernel<true><<<grid, kThreads, 0, st>>>(y_perm, row_map, row_w, T, k, H, M_cap, y);
   else

@@ -15,6 +15,7 @@ namespace ff8 {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kStreamBlocksPerCU = 1 << 20;  // streaming kernels: one tile per workgroup, no grid-stride cap
 
 int grid_for(int64_t work_items, int per_block, int max_per_cu) {
   int64_t need = (work_items + per_block - 1) / per_block;
@@ -32,7 +33,7 @@ __global__ __launch_bounds__(kThreads) void quant_rowwise_kernel(const uint16_t*
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t c = c0 + (int64_t)u * kThreads;
-      if (c < n_chunks) w[u] = ld16(x + c * 8);
+      if (c < n_chunks) w[u] = ldnt16(x + c * 8);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -42,7 +43,7 @@ __global__ __launch_bounds__(kThreads) void quant_rowwise_kernel(const uint16_t*
         unpack_bf16x8(w[u], v);
         int t;
         const u32x2 r = quant8_tile16(v, t);
-        st8(q + c * 8, r);
+        stnt8(q + c * 8, r);
         if ((threadIdx.x & 15) == 0) s[c >> 4] = exp2i(t);
       }
     }
@@ -63,7 +64,7 @@ __global__ __launch_bounds__(kThreads) void quant_block128_kernel(const uint16_t
   uint32_t m = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    v[i] = ld16(w + base + (int64_t)i * 16 * cols);
+    v[i] = ldnt16(w + base + (int64_t)i * 16 * cols);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       m = max(m, abs_bits(bf16_lo(v[i][j])));
@@ -83,7 +84,7 @@ __global__ __launch_bounds__(kThreads) void quant_block128_kernel(const uint16_t
     u32x2 r;
     r[0] = cvt_e4m3x4(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv);
     r[1] = cvt_e4m3x4(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv);
-    st8(q + base + (int64_t)i * 16 * cols, r);
+    stnt8(q + base + (int64_t)i * 16 * cols, r);
   }
   if (threadIdx.x == 0) s[blk] = exp2i(t);
 }
@@ -95,7 +96,7 @@ __global__ __launch_bounds__(kThreads) void cast_f32_e4m3_kernel(const float* __
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i * 4 < n; i += stride) {
     if (i * 4 + 4 <= n) {
-      const u32x4 w = ld16(x + i * 4);
+      const u32x4 w = ldnt16(x + i * 4);
       float f[4];
       uint32_t nanmask = 0;
 #pragma unroll
@@ -130,7 +131,7 @@ __global__ __launch_bounds__(kThreads) void cast_e4m3_f32_kernel(const uint8_t* 
       o[1] = __float_as_uint(a[1]);
       o[2] = __float_as_uint(b[0]);
       o[3] = __float_as_uint(b[1]);
-      st16(x + i * 4, o);
+      stnt16(x + i * 4, o);
     } else {
       for (int64_t j = i * 4; j < n; ++j) x[j] = dec_e4m3x2<false>((uint32_t)q[j])[0];
     }
@@ -142,7 +143,7 @@ __global__ __launch_bounds__(kThreads) void dequant_rowwise_kernel(const uint8_t
                                                                    uint16_t* __restrict__ out) {
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < n_chunks; c += stride) {
-    const u32x2 b = ld8(q + c * 8);
+    const u32x2 b = ldnt8(q + c * 8);
     const float sc = s[c >> 4];
     u32x4 o;
 #pragma unroll
@@ -151,7 +152,7 @@ __global__ __launch_bounds__(kThreads) void dequant_rowwise_kernel(const uint8_t
       o[2 * j] = pack_bf16x2(lo[0] * sc, lo[1] * sc);
       o[2 * j + 1] = pack_bf16x2(hi[0] * sc, hi[1] * sc);
     }
-    st16(out + c * 8, o);
+    stnt16(out + c * 8, o);
   }
 }
 
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void transpose_bf16_kernel(const uint16_t
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = ty + 16 * i;
-    const u32x2 v = ld8(in + (rb * 64 + r) * cols + cb * 64 + tx * 4);
+    const u32x2 v = ldnt8(in + (rb * 64 + r) * cols + cb * 64 + tx * 4);
     tile[r][tx * 4 + 0] = v[0] & 0xFFFF;
     tile[r][tx * 4 + 1] = v[0] >> 16;
     tile[r][tx * 4 + 2] = v[1] & 0xFFFF;
@@ -178,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void transpose_bf16_kernel(const uint16_t
     u32x2 v;
     v[0] = (uint32_t)tile[tx * 4 + 0][c] | ((uint32_t)tile[tx * 4 + 1][c] << 16);
     v[1] = (uint32_t)tile[tx * 4 + 2][c] | ((uint32_t)tile[tx * 4 + 3][c] << 16);
-    st8(out + (cb * 64 + c) * rows + rb * 64 + tx * 4, v);
+    stnt8(out + (cb * 64 + c) * rows + rb * 64 + tx * 4, v);
   }
 }
 
@@ -190,10 +191,10 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(const u32x4* __restrict_
     u32x4 v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (c0 + u * kThreads < n16) v[u] = src[c0 + u * kThreads];
+      if (c0 + u * kThreads < n16) v[u] = ldnt16(src + c0 + u * kThreads);
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (c0 + u * kThreads < n16) dst[c0 + u * kThreads] = v[u];
+      if (c0 + u * kThreads < n16) stnt16(dst + c0 + u * kThreads, v[u]);
   }
 }
 
@@ -203,7 +204,7 @@ hipError_t launch_quant_rowwise(const uint16_t* x, int64_t rows, int64_t cols, u
                                 hipStream_t st) {
   const int64_t n_chunks = rows * cols / 8;
   constexpr int U = 4;
-  const int grid = grid_for(n_chunks, kThreads * U, 16);
+  const int grid = grid_for(n_chunks, kThreads * U, kStreamBlocksPerCU);
   quant_rowwise_kernel<U><<<grid, kThreads, 0, st>>>(x, n_chunks, q, s);
   return hipGetLastError();
 }
@@ -241,7 +242,7 @@ hipError_t launch_transpose_bf16(const uint16_t* in, int64_t rows, int64_t cols,
 hipError_t launch_copy(const void* src, void* dst, int64_t nbytes, hipStream_t st) {
   const int64_t n16 = nbytes / 16;
   constexpr int U = 4;
-  copy_kernel<U><<<grid_for(n16, kThreads * U, 16), kThreads, 0, st>>>(
+  copy_kernel<U><<<grid_for(n16, kThreads * U, kStreamBlocksPerCU), kThreads, 0, st>>>(
       reinterpret_cast<const u32x4*>(src), n16, reinterpret_cast<u32x4*>(dst));
   return hipGetLastError();
 }

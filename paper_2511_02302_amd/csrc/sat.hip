@@ -2,20 +2,21 @@
 // exponent-shift identity).
 //
 // One workgroup owns one 128-column tile of the input and kRB consecutive 128-row
-// blocks.  Per block:
-//   1. the 128 row scales of the tile give S_max (wave DPP max + LDS) and every row's
-//      shift k_i = log2(S_max) - log2(s_i) (integer: scales are powers of two);
-//   2. lane (sr, sc) loads an 8x8 byte sub-block (rows 8 sr.., bytes 8 sc..; 16 lanes
-//      read a full 128-byte row segment);
-//   3. rows with k_i > 0 are re-expressed at S_max: decode (exact), multiply by 2^-k
-//      (exact), hardware RNE encode -- equal to lowering the exponent field by k_i
-//      while it stays >= 1, and the nearest-even subnormal below that;
-//   4. the 8x8 sub-block is transposed in registers (v_perm_b32) and written to LDS
-//      in output order (XOR-swizzled 8-byte chunks, conflict-free);
-//   5. the 128x128 output block is streamed out with 16-byte stores, 8 lanes per
-//      128-byte output row segment.
-// The block's S_max is written to sT once per output row: kRB consecutive blocks
-// give kRB contiguous floats per row, so scale stores are 4*kRB bytes wide.
+// blocks; column tiles are the fastest-varying index of the grid, so the workgroups an
+// XCD runs together read the same rows (their scale lines and DRAM pages once).
+//   1. up front, the row scales of all kRB blocks give every row's exponent (to LDS)
+//      and each block's S_max (wave DPP max + LDS), behind a single barrier;
+//   2. per block, lane (sr, sc) holds an 8x8 byte sub-block (rows 8 sr.., bytes 8 sc..;
+//      16 lanes read a full 128-byte row segment), loaded one block ahead;
+//   3. rows with k_i = log2(S_max) - log2(s_i) > 0 are re-expressed at S_max: decode
+//      (exact), multiply by 2^-k (exact), hardware RNE encode -- equal to lowering the
+//      exponent field by k_i while it stays >= 1, and the nearest-even subnormal below;
+//   4. the 8x8 sub-block is transposed in registers (v_perm_b32) and written to LDS in
+//      output order (XOR-swizzled 8-byte chunks, conflict-free);
+//   5. the 128x128 output block is streamed out with 16-byte non-temporal stores, 8
+//      lanes per 128-byte output row segment.
+// The block's S_max is written to sT once per output row: kRB consecutive blocks give
+// kRB contiguous floats per row, so scale stores are 4*kRB bytes wide.
 
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
@@ -60,62 +61,79 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
                                                        int E, int n_rb_groups, uint8_t* __restrict__ qT,
                                                        float* __restrict__ sT) {
   __shared__ uint32_t tile[128 * 128 / 4];  // output block, 128 rows x 128 bytes (swizzled 8-byte chunks)
-  __shared__ int kshift[128];
-  __shared__ uint32_t wmax[2];
+  __shared__ int t_rows[kRB][128];          // scale exponent of every input row of every block
+  __shared__ uint32_t wmax[kRB][2];
 
   const int n_cb = (int)(cols / kTile);
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int cb = logical / n_rb_groups;
-  const int rg = logical - cb * n_rb_groups;
+  // column tiles fastest: the workgroups an XCD runs together share the same input rows,
+  // so each row's scale line and DRAM pages are fetched once for all its column tiles
+  const int rg = logical / n_cb;
+  const int cb = logical - rg * n_cb;
+  (void)n_rb_groups;
   const int64_t m_rows = active_rows(offsets, E, rows);
   const int64_t n_rb = rows / kTile;
   const int n_sb = (int)(rows / kTile);  // sT row stride (floats)
+  const int64_t rb0 = (int64_t)rg * kRB;
+  int n_valid = 0;  // blocks of this group that hold data (uniform)
+#pragma unroll
+  for (int bi = 0; bi < kRB; ++bi)
+    if (rb0 + bi < n_rb && (rb0 + bi) * kTile < m_rows) n_valid = bi + 1;
 
   const int tid = threadIdx.x;
   const int sr = tid >> 4, sc = tid & 15;
-  float smax_kept[kRB];
 
+  // 1. All blocks' row scales up front: per-row exponents to LDS, S_max per block by a
+  //    wave DPP max and a 2-entry LDS max; one barrier for the whole group.
+  if (tid < 128) {
 #pragma unroll
-  for (int i = 0; i < kRB; ++i) smax_kept[i] = 0.0f;
-
-  for (int bi = 0; bi < kRB; ++bi) {
-    const int64_t rb = (int64_t)rg * kRB + bi;
-    if (rb >= n_rb || rb * kTile >= m_rows) break;  // uniform across the workgroup
-
-    // 1. S_max and per-row shifts.
-    int t_row = 0;
-    if (tid < 128) {
-      t_row = (int)(__float_as_uint(s[(rb * kTile + tid) * n_cb + cb]) >> 23) - 127;
+    for (int bi = 0; bi < kRB; ++bi) {
+      int t_row = -256;
+      if (bi < n_valid) t_row = (int)(__float_as_uint(s[((rb0 + bi) * kTile + tid) * n_cb + cb]) >> 23) - 127;
+      t_rows[bi][tid] = t_row;
       const uint32_t m = max64_u32((uint32_t)(t_row + 256));
-      if ((tid & 63) == 0) wmax[tid >> 6] = m;
+      if ((tid & 63) == 0) wmax[bi][tid >> 6] = m;
     }
-    // 2. load the 8x8 sub-block (issued before the barrier to overlap latency).
-    const uint8_t* src = q + (rb * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
-    u32x2 v[8];
+  }
+  // first block's data in flight across the barrier
+  u32x2 v[8];
+  {
+    const uint8_t* src = q + (rb0 * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
+    if (n_valid > 0) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = ld8(src + (int64_t)i * cols);
-    __syncthreads();
-    const int t_max = (int)max(wmax[0], wmax[1]) - 256;
-    if (tid < 128) kshift[tid] = t_max - t_row;
-    smax_kept[bi] = exp2i(t_max);
-    __syncthreads();
+      for (int i = 0; i < 8; ++i) v[i] = ld8(src + (int64_t)i * cols);
+    }
+  }
+  __syncthreads();
 
-    // 3. exponent shift of rows below S_max.
+  for (int bi = 0; bi < n_valid; ++bi) {
+    const int64_t rb = rb0 + bi;
+    const int t_max = (int)max(wmax[bi][0], wmax[bi][1]) - 256;
+    // 2. rows below S_max are re-expressed at S_max: decode (exact), times 2^-k (exact),
+    //    RNE encode -- the exponent-field decrement, and nearest-even below the normals.
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int k = kshift[sr * 8 + i];
+      const int k = t_max - t_rows[bi][sr * 8 + i];
       if (k != 0) {
-        const float f = exp2i(-k);
+        // every e4m3 value is below 2^9, so any k >= 19 sends it to a signed zero; the
+        // clamp keeps 2^-k a normal float for the block's full 253-octave range
+        const float f = exp2i(-min(k, 64));
         v[i][0] = shift4(v[i][0], f);
         v[i][1] = shift4(v[i][1], f);
       }
     }
-    // 4. transpose the 8x8 sub-block: column c of the input becomes output row 8 sc + c.
+    // 3. transpose the 8x8 sub-block: column c of the input becomes output row 8 sc + c.
     uint32_t o_lo[8], o_hi[8];
     transpose4x4(v[0][0], v[1][0], v[2][0], v[3][0], o_lo[0], o_lo[1], o_lo[2], o_lo[3]);
     transpose4x4(v[4][0], v[5][0], v[6][0], v[7][0], o_hi[0], o_hi[1], o_hi[2], o_hi[3]);
     transpose4x4(v[0][1], v[1][1], v[2][1], v[3][1], o_lo[4], o_lo[5], o_lo[6], o_lo[7]);
     transpose4x4(v[4][1], v[5][1], v[6][1], v[7][1], o_hi[4], o_hi[5], o_hi[6], o_hi[7]);
+    // next block's data in flight while this one goes through LDS
+    if (bi + 1 < n_valid) {
+      const uint8_t* src = q + ((rb + 1) * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = ld8(src + (int64_t)i * cols);
+    }
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int orow = sc * 8 + c;
@@ -127,7 +145,8 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
     }
     __syncthreads();
 
-    // 5. stream the output block: 8 lanes per 128-byte output row, 4 passes of 32 rows.
+    // 4. stream the output block: 8 lanes per 128-byte output row, 4 passes of 32 rows;
+    //    streaming stores (the transposed tensor is consumed much later, by wgrad).
     const int c16 = tid & 7;
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
@@ -140,28 +159,21 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
       o[1] = a[1];
       o[2] = b[0];
       o[3] = b[1];
-      st16(qT + ((int64_t)cb * kTile + orow) * rows + rb * kTile + c16 * 16, o);
+      stnt16(qT + ((int64_t)cb * kTile + orow) * rows + rb * kTile + c16 * 16, o);
     }
-    __syncthreads();  // tile and kshift are reused by the next block
+    __syncthreads();  // the tile is rewritten by the next block
   }
 
-  // Column-wise scales: every output row of the tile gets S_max of each block.
+  // 5. column-wise scales: every output row of the tile gets S_max of each block.
   if (tid < 128) {
-    float* dst = sT + ((int64_t)cb * kTile + tid) * n_sb + (int64_t)rg * kRB;
-    const int64_t rb0 = (int64_t)rg * kRB;
-    int n_valid = 0;
-#pragma unroll
-    for (int bi = 0; bi < kRB; ++bi)
-      if (rb0 + bi < n_rb && (rb0 + bi) * kTile < m_rows) n_valid = bi + 1;
-    if (n_valid == kRB && (((uintptr_t)dst) & 15) == 0) {
+    float* dst = sT + ((int64_t)cb * kTile + tid) * n_sb + rb0;
+    if (kRB == 4 && n_valid == kRB && (((uintptr_t)dst) & 15) == 0) {  // one 16-byte store
       u32x4 o;
 #pragma unroll
-      for (int bi = 0; bi < kRB; ++bi) o[bi] = __float_as_uint(smax_kept[bi]);
+      for (int bi = 0; bi < kRB; ++bi) o[bi] = __float_as_uint(exp2i((int)max(wmax[bi][0], wmax[bi][1]) - 256));
       st16(dst, o);
     } else {
-#pragma unroll
-      for (int bi = 0; bi < kRB; ++bi)
-        if (bi < n_valid) dst[bi] = smax_kept[bi];
+      for (int bi = 0; bi < n_valid; ++bi) dst[bi] = exp2i((int)max(wmax[bi][0], wmax[bi][1]) - 256);
     }
   }
 }

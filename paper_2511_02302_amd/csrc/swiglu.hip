@@ -27,13 +27,13 @@ __global__ __launch_bounds__(kThreads) void swiglu_quant_kernel(const uint16_t* 
     const int64_t m = it / cpr, c = it - m * cpr;
     const uint16_t* row = a + m * 2 * I + c * 8;
     float g[8], u[8], h[8];
-    unpack_bf16x8(ld16(row), g);
-    unpack_bf16x8(ld16(row + I), u);
+    unpack_bf16x8(ldnt16(row), g);
+    unpack_bf16x8(ldnt16(row + I), u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) h[i] = g[i] * sigmoid(g[i]) * u[i];
     int t;
     const u32x2 r = quant8_tile16(h, t);
-    st8(hq + m * I + c * 8, r);
+    stnt8(hq + m * I + c * 8, r);
     if ((threadIdx.x & 15) == 0) hs[m * sh + (c >> 4)] = exp2i(t);
   }
 }
@@ -51,9 +51,9 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_kernel(const uint16
     const int64_t m = it / cpr, c = it - m * cpr;
     const uint16_t* row = a + m * 2 * I + c * 8;
     float g[8], u[8], d[8], dg[8], du[8];
-    unpack_bf16x8(ld16(row), g);
-    unpack_bf16x8(ld16(row + I), u);
-    unpack_bf16x8(ld16(dh + m * I + c * 8), d);
+    unpack_bf16x8(ldnt16(row), g);
+    unpack_bf16x8(ldnt16(row + I), u);
+    unpack_bf16x8(ldnt16(dh + m * I + c * 8), d);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float sg = sigmoid(g[i]);
@@ -65,8 +65,8 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_kernel(const uint16
     const u32x2 rg = quant8_tile16(dg, tg);
     const u32x2 ru = quant8_tile16(du, tu);
     uint8_t* out = daq + m * 2 * I + c * 8;
-    st8(out, rg);
-    st8(out + I, ru);
+    stnt8(out, rg);
+    stnt8(out + I, ru);
     if ((threadIdx.x & 15) == 0) {
       das[m * sh + (c >> 4)] = exp2i(tg);
       das[m * sh + I / kTile + (c >> 4)] = exp2i(tu);
@@ -84,19 +84,21 @@ __global__ __launch_bounds__(kThreads) void swiglu_bf16_kernel(const uint16_t* _
     const int64_t m = it / cpr, c = it - m * cpr;
     const uint16_t* row = a + m * 2 * I + c * 8;
     float g[8], u[8];
-    unpack_bf16x8(ld16(row), g);
-    unpack_bf16x8(ld16(row + I), u);
+    unpack_bf16x8(ldnt16(row), g);
+    unpack_bf16x8(ldnt16(row + I), u);
     u32x4 o;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       o[i] = pack_bf16x2(g[2 * i] * sigmoid(g[2 * i]) * u[2 * i], g[2 * i + 1] * sigmoid(g[2 * i + 1]) * u[2 * i + 1]);
-    st16(h + m * I + c * 8, o);
+    stnt16(h + m * I + c * 8, o);
   }
 }
 
+constexpr int kStreamBlocksPerCU = 1 << 20;  // grid cap of the SwiGLU kernels (none: one pass)
+
 int grid_for(int64_t items) {
   int64_t need = (items + kThreads - 1) / kThreads;
-  const int64_t cap = (int64_t)device_cu_count() * 16;
+  const int64_t cap = (int64_t)device_cu_count() * kStreamBlocksPerCU;
   if (need < 1) need = 1;
   return (int)(need < cap ? need : cap);
 }

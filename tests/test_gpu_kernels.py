@@ -160,6 +160,27 @@ def test_sat_bit_exact(rows, cols, n_rows):
     assert untouched(qT[:, n_rows:]) and untouched(sT[:, n_rows // 128:])
 
 
+def test_sat_extreme_row_range():
+    """Rows of one block whose scales differ by up to 2^139: shifts of 18, 19 and >= 128
+    (underflow to the nearest subnormal, to signed zero, and far beyond the float range of
+    2^-k) must all match the oracle's exact enc(dec(b) * 2^-k)."""
+    g = torch.Generator().manual_seed(7)
+    x = torch.randn((256, 256), generator=g)
+    octaves = [20, -118, 2, 1, 0, -50, -100, 12, -126, 20 - 17, 20 - 18]
+    for r, o in enumerate(octaves):
+        x[r] *= 2.0 ** o
+        x[128 + r] *= -(2.0 ** o)
+    x = x.to(torch.bfloat16)
+    q, s = quant.quant_rowwise(f64(x))
+    qT = poisoned((256, 256), torch.uint8)
+    sT = poisoned((256, 2), torch.float32)
+    ff8.ff8_scaling_aware_transpose(dev(torch.from_numpy(q)), dev(torch.from_numpy(s)), qT, sT)
+    torch.cuda.synchronize()
+    wqT, wsT = sat.scaling_aware_transpose(q, s)
+    assert np.array_equal(host(qT), wqT)
+    assert np.array_equal(host(sT), wsT)
+
+
 def test_sat_full_size_sampled_blocks():
     rows, cols = workloads.CAST_X
     x = workloads.outlier_activation(rows, cols, seed=0, device="cuda")
