@@ -11,9 +11,11 @@
 //                  padding rows' src_row = -1;
 //   route_assign : one wave per chunk walks its tokens 64 at a time; a 64-bit LDS
 //                  ballot mask per expert gives each pair its rank among earlier lanes.
-// Then permute_quant reads each token row ONCE, quantizes it 1x128 (16 lanes per tile,
-// DPP amax), and writes it to each of its k rows; with routing weights each copy is
-// scaled (float32 product) and quantized separately.  pad_fill writes the padding rows.
+// Then permute_quant reads each token row ONCE (one workgroup per token, 16 elements per
+// lane, 8 lanes per 1x128 tile, DPP amax), quantizes it and writes it to each of its k
+// rows; with routing weights each copy is scaled (float32 product) and quantized
+// separately.  pad_fill writes the padding rows.  unpermute gathers a token's k rows the
+// same way and sums them in slot order.
 
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
@@ -24,6 +26,7 @@ namespace {
 
 constexpr int kChunk = 256;  // tokens per routing chunk
 constexpr int kThreads = 256;
+constexpr int kRowThreadsMax = 512;  // one-token workgroups (permute, unpermute)
 
 int64_t n_chunks_of(int64_t T) { return (T + kChunk - 1) / kChunk; }
 
@@ -111,31 +114,52 @@ __global__ __launch_bounds__(64) void route_assign_kernel(const int32_t* __restr
   }
 }
 
-// Work item (t, c): token t, 8-element chunk c of its row.  16 consecutive items share a
-// 128-element tile (H / 8 is a multiple of 16), so the tile amax stays a 16-lane reduction.
+// One workgroup per token: lane c covers 16 elements (two 16-byte loads) of the row, 8
+// lanes one 128-element tile (8-lane DPP amax).  The token's k destination rows and
+// weights are workgroup-uniform (scalar loads); every copy is one 16-byte store per lane,
+// so a wave writes 1 KB contiguous of one destination row.
+__device__ __forceinline__ uint32_t max8_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+  return v;
+}
+// 16 values of one tile shared by 8 consecutive lanes -> 16 e4m3 bytes and the exponent.
+__device__ __forceinline__ u32x4 quant16_tile8(const float* v, int& t_out) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) m = max(m, abs_bits(v[i]));
+  m = max8_u32(m);
+  const int t = scale_exponent(__uint_as_float(m));
+  const float inv = exp2i(-t);
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = cvt_e4m3x4(v[4 * i] * inv, v[4 * i + 1] * inv, v[4 * i + 2] * inv, v[4 * i + 3] * inv);
+  t_out = t;
+  return r;
+}
+
 template <bool kWeighted>
-__global__ __launch_bounds__(kThreads) void permute_quant_kernel(const uint16_t* __restrict__ x,
-                                                                 const float* __restrict__ row_w, int64_t T,
-                                                                 int64_t H, int k, const int32_t* __restrict__ row_map,
-                                                                 int64_t M_cap, uint8_t* __restrict__ q,
-                                                                 float* __restrict__ s) {
-  const int64_t cpr = H / 8;  // chunks per row
-  const int64_t n_items = T * cpr;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  const int64_t sh = H / kTile;
-  const bool leader = (threadIdx.x & 15) == 0;
-  for (int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x; it < n_items; it += stride) {
-    const int64_t t = it / cpr, c = it - t * cpr;
-    float v[8];
-    unpack_bf16x8(ldnt16(x + t * H + c * 8), v);
+__global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uint16_t* __restrict__ x,
+                                                                       const float* __restrict__ row_w, int64_t H,
+                                                                       int k, const int32_t* __restrict__ row_map,
+                                                                       int64_t M_cap, uint8_t* __restrict__ q,
+                                                                       float* __restrict__ s) {
+  const int64_t t = blockIdx.x;
+  const int64_t n16 = H / 16, sh = H / kTile;
+  for (int64_t c = threadIdx.x; c < n16; c += blockDim.x) {  // uniform per 8-lane tile
+    const bool leader = (c & 7) == 0;
+    float v[16];
+    unpack_bf16x8(ldnt16(x + t * H + c * 16), v);
+    unpack_bf16x8(ldnt16(x + t * H + c * 16 + 8), v + 8);
     if (!kWeighted) {
       int tq;
-      const u32x2 r = quant8_tile16(v, tq);
+      const u32x4 r = quant16_tile8(v, tq);
       for (int j = 0; j < k; ++j) {
         const int row = row_map[t * k + j];
-        if (row >= 0 && row < M_cap) {  // uniform across the 16 lanes of a tile
-          stnt8(q + (int64_t)row * H + c * 8, r);
-          if (leader) s[(int64_t)row * sh + (c >> 4)] = exp2i(tq);
+        if (row >= 0 && row < M_cap) {
+          stnt16(q + (int64_t)row * H + c * 16, r);
+          if (leader) s[(int64_t)row * sh + (c >> 3)] = exp2i(tq);
         }
       }
     } else {
@@ -143,13 +167,13 @@ __global__ __launch_bounds__(kThreads) void permute_quant_kernel(const uint16_t*
         const int row = row_map[t * k + j];
         if (row >= 0 && row < M_cap) {
           const float w = row_w[t * k + j];
-          float vw[8];
+          float vw[16];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) vw[i] = w * v[i];
+          for (int i = 0; i < 16; ++i) vw[i] = w * v[i];
           int tq;
-          const u32x2 r = quant8_tile16(vw, tq);
-          stnt8(q + (int64_t)row * H + c * 8, r);
-          if (leader) s[(int64_t)row * sh + (c >> 4)] = exp2i(tq);
+          const u32x4 r = quant16_tile8(vw, tq);
+          stnt16(q + (int64_t)row * H + c * 16, r);
+          if (leader) s[(int64_t)row * sh + (c >> 3)] = exp2i(tq);
         }
       }
     }
@@ -182,45 +206,64 @@ __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __res
   }
 }
 
+// One workgroup per token: lane c sums 16 elements of the token's k rows in slot order
+// (float32, routing weight applied per slot when given), one bf16 rounding.  Up to
+// kUnrollK slots are loaded before the sum so that their reads are in flight together.
+constexpr int kUnrollK = 8;
 template <bool kWeighted>
-__global__ __launch_bounds__(kThreads) void unpermute_kernel(const uint16_t* __restrict__ y_perm,
-                                                             const int32_t* __restrict__ row_map,
-                                                             const float* __restrict__ row_w, int64_t T, int k,
-                                                             int64_t H, int64_t M_cap, uint16_t* __restrict__ y) {
-  const int64_t cpr = H / 8;
-  const int64_t n_items = T * cpr;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  for (int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x; it < n_items; it += stride) {
-    const int64_t t = it / cpr, c = it - t * cpr;
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < k; ++j) {
-      const int row = row_map[t * k + j];
-      if (row < 0 || row >= M_cap) continue;
-      float v[8];
-      unpack_bf16x8(ldnt16(y_perm + (int64_t)row * H + c * 8), v);
-      if (kWeighted) {
-        const float w = row_w[t * k + j];
+__global__ __launch_bounds__(kRowThreadsMax) void unpermute_kernel(const uint16_t* __restrict__ y_perm,
+                                                                   const int32_t* __restrict__ row_map,
+                                                                   const float* __restrict__ row_w, int k, int64_t H,
+                                                                   int64_t M_cap, uint16_t* __restrict__ y) {
+  const int64_t t = blockIdx.x;
+  const int64_t n16 = H / 16;
+  for (int64_t c = threadIdx.x; c < n16; c += blockDim.x) {
+    float acc[16];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] = fmaf(w, v[i], acc[i]);
-      } else {
+    for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+    for (int j0 = 0; j0 < k; j0 += kUnrollK) {
+      u32x4 a[kUnrollK], b[kUnrollK];
+      int rows[kUnrollK];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] += v[i];
+      for (int jj = 0; jj < kUnrollK; ++jj) {
+        const int j = j0 + jj;
+        rows[jj] = (j < k) ? row_map[t * k + j] : -1;
+        if (rows[jj] >= 0 && rows[jj] < M_cap) {
+          a[jj] = ldnt16(y_perm + (int64_t)rows[jj] * H + c * 16);
+          b[jj] = ldnt16(y_perm + (int64_t)rows[jj] * H + c * 16 + 8);
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < kUnrollK; ++jj) {
+        if (rows[jj] < 0 || rows[jj] >= M_cap) continue;
+        float v[16];
+        unpack_bf16x8(a[jj], v);
+        unpack_bf16x8(b[jj], v + 8);
+        if (kWeighted) {
+          const float w = row_w[t * k + j0 + jj];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[i] = fmaf(w, v[i], acc[i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[i] += v[i];
+        }
       }
     }
-    u32x4 o;
+    u32x4 o0, o1;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = pack_bf16x2(acc[2 * i], acc[2 * i + 1]);
-    stnt16(y + t * H + c * 8, o);
+    for (int i = 0; i < 4; ++i) {
+      o0[i] = pack_bf16x2(acc[2 * i], acc[2 * i + 1]);
+      o1[i] = pack_bf16x2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
+    }
+    stnt16(y + t * H + c * 16, o0);
+    stnt16(y + t * H + c * 16 + 8, o1);
   }
 }
 
-constexpr int kStreamBlocksPerCU = 1 << 20;  // grid cap of the permute / unpermute kernels (none: one pass)
-
-int grid_for(int64_t items, int max_per_cu) {
-  int64_t need = (items + kThreads - 1) / kThreads;
-  const int64_t cap = (int64_t)device_cu_count() * max_per_cu;
-  if (need < 1) need = 1;
-  return (int)(need < cap ? need : cap);
+// Threads of a one-token workgroup: one lane per 16 elements, whole waves, at most 512.
+unsigned row_threads(int64_t H) {
+  int64_t n = (H / 16 + 63) / 64 * 64;
+  return (unsigned)(n < kRowThreadsMax ? n : kRowThreadsMax);
 }
 
 }  // namespace
@@ -244,13 +287,11 @@ hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int32_
 hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                                 const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                 int64_t M_cap, uint8_t* q, float* s, hipStream_t st) {
-  const int64_t items = T * (H / 8);
-  if (items > 0) {
-    const int grid = grid_for(items, kStreamBlocksPerCU);
+  if (T > 0) {
     if (row_w)
-      permute_quant_kernel<true><<<grid, kThreads, 0, st>>>(x, row_w, T, H, k, row_map, M_cap, q, s);
+      permute_quant_kernel<true><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
     else
-      permute_quant_kernel<false><<<grid, kThreads, 0, st>>>(x, row_w, T, H, k, row_map, M_cap, q, s);
+      permute_quant_kernel<false><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
   }
   pad_fill_kernel<<<(unsigned)(M_cap / kTile), kThreads, 0, st>>>(offsets, E, src_row, H, q, s);
   return hipGetLastError();
@@ -258,13 +299,11 @@ hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T
 
 hipError_t launch_unpermute(const uint16_t* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k,
                             int64_t H, int64_t M_cap, uint16_t* y, hipStream_t st) {
-  const int64_t items = T * (H / 8);
-  if (items == 0) return hipSuccess;
-  const int grid = grid_for(items, kStreamBlocksPerCU);
+  if (T == 0) return hipSuccess;
   if (row_w)
-    unpermute_kernel<true><<<grid, kThreads, 0, st>>>(y_perm, row_map, row_w, T, k, H, M_cap, y);
+    unpermute_kernel<true><<<(unsigned)T, row_threads(H), 0, st>>>(y_perm, row_map, row_w, k, H, M_cap, y);
   else
-    unpermute_kernel<false><<<grid, kThreads, 0, st>>>(y_perm, row_map, row_w, T, k, H, M_cap, y);
+    unpermute_kernel<false><<<(unsigned)T, row_threads(H), 0, st>>>(y_perm, row_map, row_w, k, H, M_cap, y);
   return hipGetLastError();
 }
 
