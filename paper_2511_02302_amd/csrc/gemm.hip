@@ -54,6 +54,7 @@ constexpr int kTileBytes = kTP * kBK;  // 32 KB per operand per stage
 constexpr int kScaleBatch = 4;         // K blocks per scale batch
 constexpr int kDmaPerSlot = 1;         // tile DMA instructions issued per MFMA slot
 constexpr int kReadSlots = 8;          // MFMA slots of a half-step that carry fragment reads
+constexpr bool kBufferDma = true;      // MUBUF LDS DMA (false: global_load_lds)
 // Rotate each XCD block's K order (memory-channel spread).  Measured: +5.6% for fprop,
 // whose two operands are row-major over K; -1% / -3% for dgrad / wgrad, which keep it off.
 template <int MODE> constexpr bool kStaggerK = (MODE == kFprop);
@@ -93,15 +94,40 @@ __device__ __forceinline__ int kswz(int r) { return (r ^ (r >> 3)) & 7; }
 // dgrad weight stage tile: 128 rows (n) x 256 bytes, chunk c of row n at c ^ wswz(n % 8).
 __device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
 
-// LDS DMA: each lane loads 16 (or 4) bytes from sbase + voff into LDS at M0 + 16 * lane
-// (or 4 * lane).  Issued through inline asm so that the compiler does not serialize the
-// pipeline with conservative waits; the kernel waits for its own DMA (vmcnt) before the
-// barrier that publishes a stage.
-__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" : : "{m0}"(lds_off), "v"(voff), "s"(sbase) : "memory");
+// LDS DMA: each lane loads 16 (or 4) bytes from base + soff + voff into LDS at M0 + 16 *
+// lane (or 4 * lane).  Issued through inline asm so that the compiler does not serialize
+// the pipeline with conservative waits; the kernel waits for its own DMA (vmcnt) before
+// the barrier that publishes a stage.  Two encodings: MUBUF (buffer_load ... lds, a
+// 128-bit resource per operand; base in the resource, stage offset in soffset) and
+// global (global_load_lds_*, 64-bit scalar base).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+// Raw (stride 0) buffer resource: loads at offsets >= `bytes` return zeros.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0xFFFFFFFFu) {
+  const uint64_t a = (uint64_t)base;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));  // stride 0
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;   // raw 32-bit data format
+  return r;
 }
-__device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dword %1, %2" : : "{m0}"(lds_off), "v"(voff), "s"(sbase) : "memory");
+__device__ __forceinline__ void dma16(const void* sbase, const i32x4& rsrc, uint32_t soff, uint32_t voff,
+                                      uint32_t lds_off) {
+  if constexpr (kBufferDma)
+    asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc),
+                 "s"(soff) : "memory");
+  else
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" : : "{m0}"(lds_off), "v"(voff),
+                 "s"((const uint8_t*)sbase + soff) : "memory");
+}
+// Range-checked scale DMA (always MUBUF: tail lanes may point past the scale tensor).
+__device__ __forceinline__ void dma4r(const i32x4& rsrc, uint32_t soff, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc),
+               "s"(soff) : "memory");
+}
+__device__ __forceinline__ void dma16r(const i32x4& rsrc, uint32_t soff, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc),
+               "s"(soff) : "memory");
 }
 
 __device__ __forceinline__ uint32_t e8m0(float s) { return __float_as_uint(s) >> 23; }
@@ -129,10 +155,14 @@ struct Tile {
   const uint8_t* q_base;
   const float* sp_base;
   const float* sq_base;
+  i32x4 p_rsrc, q_rsrc, sp_rsrc, sq_rsrc;  // MUBUF resources of the four bases
   uint32_t p_off[8], q_off[8];   // tile DMA instruction i, stage 0
-  uint32_t sp_off[4], sq_off[4]; // scale DMA instruction i, K block 0 (before the lane's block index)
+  uint32_t sp_off, sq_off;       // scale DMA: this lane's source offset at K block 0
   int64_t p_kstep;               // bytes per stage of the P source
   int sp_kb;                     // floats per K block of the P scale source (q scales: 1)
+  // fprop / dgrad: a wave's 128 P rows are one 128x128 weight block, so its P scale is one
+  // value per K block (stored compactly as [tile half][4 K blocks]); wgrad: one per row.
+  static constexpr bool kBlockP = (MODE != kWgrad);
   int wave, lane, wp, wq;
   int64_t nk;
   int64_t k_rot;  // K stages this tile's loop is rotated by (a multiple of the scale batch)
@@ -147,19 +177,25 @@ struct Tile {
   __device__ __forceinline__ void dma_tile(int64_t ks) {
     const uint32_t base = stage_lds<B>() + (uint32_t)wave * 8192u;  // the wave's 8 KB slice of each tile
     const int64_t kp = __builtin_amdgcn_readfirstlane((int)kphys(ks));  // uniform: keep the base scalar
-    if constexpr (I < 8) dma16(p_base + kp * p_kstep, p_off[I], base + I * 1024);
-    else dma16(q_base + kp * kBK, q_off[I - 8], base + kTileBytes + (I - 8) * 1024);
+    if constexpr (I < 8) dma16(p_base, p_rsrc, (uint32_t)(kp * p_kstep), p_off[I], base + I * 1024);
+    else dma16(q_base, q_rsrc, (uint32_t)(kp * kBK), q_off[I - 8], base + kTileBytes + (I - 8) * 1024);
   }
-  // Scale DMA instruction I (0..7) of batch b (K blocks 4b..4b+3, clamped to the last
-  // block): 0-3 P, 4-7 Q.  Lane l loads block 4b + l%4 of tile row (wave*4+i)*16 + l/4.
-  template <int I>
-  __device__ __forceinline__ void dma_scale(int64_t b) {
-    int64_t kb = b * kScaleBatch + (lane & 3);
-    kb = kb < nk ? kb : nk - 1;
-    kb = kphys(kb);
-    const uint32_t lbase = scale_lds((int)(b & 1)) + (uint32_t)wave * 1024u;
-    if constexpr (I < 4) dma4(sp_base, sp_off[I] + (uint32_t)(kb * sp_kb * 4), lbase + I * 256);
-    else dma4(sq_base, sq_off[I - 4] + (uint32_t)(kb * 4), lbase + kTP * kScaleBatch * 4 + (I - 4) * 256);
+  // Scale DMA of batch b (K blocks 4b..4b+3) into batch buffer b % 2, rows of four floats:
+  // the P instruction (kBlockP: 8 lanes carry the two weight blocks' 4 floats, the rest
+  // duplicate them; else lane l carries tile row 64 wave + l) and the Q instruction (lane
+  // l carries tile row 64 wave + l).  Batches are rotated with the K order (k_rot is a
+  // multiple of the batch); blocks past the last K block read neighbouring rows or zeros
+  // (range-checked resources) and are never multiplied.
+  __device__ __forceinline__ void dma_scale_p(int64_t b) {
+    const uint32_t lbase = scale_lds((int)(b & 1));
+    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)kphys(b * kScaleBatch));
+    if constexpr (kBlockP) dma4r(sp_rsrc, kb0 * (uint32_t)sp_kb * 4u, sp_off, lbase);
+    else dma16r(sp_rsrc, kb0 * 4u, sp_off, lbase + (uint32_t)wave * 1024u);
+  }
+  __device__ __forceinline__ void dma_scale_q(int64_t b) {
+    const uint32_t lbase = scale_lds((int)(b & 1)) + kTP * kScaleBatch * 4;
+    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)kphys(b * kScaleBatch));
+    dma16r(sq_rsrc, kb0 * 4u, sq_off, lbase + (uint32_t)wave * 1024u);
   }
 
   // Fragment read J of half h of stage buffer B into register set kSetA.
@@ -209,7 +245,7 @@ struct Tile {
     const int l31 = lane & 31;
 #pragma unroll
     for (int R = 0; R < 4; ++R)
-      raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : S[128 * wp + 32 * R + l31];
+      raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : (kBlockP ? S[wp] : S[128 * wp + 32 * R + l31]);
   }
   // ... and pack them: word j holds the E8M0 byte (the fp32 exponent field of a
   // positive power of two) of row R in byte R.
@@ -234,7 +270,8 @@ struct Tile {
   __device__ __forceinline__ void dma_slot(int64_t ks_dma, int64_t ks_next) {
     if constexpr (D < kDmaPerSlot && kDmaPerSlot * I + D < 16) {
       dma_tile<B, kDmaPerSlot * I + D>(ks_dma);
-      if constexpr (S4 == 0 && (kDmaPerSlot * I + D) % 2 == 0) dma_scale<(kDmaPerSlot * I + D) / 2>((ks_next >> 2) + 1);
+      if constexpr (S4 == 0 && kDmaPerSlot * I + D == 1) dma_scale_p((ks_next >> 2) + 1);
+      if constexpr (S4 == 0 && kDmaPerSlot * I + D == 3) dma_scale_q((ks_next >> 2) + 1);
       dma_slot<B, S4, I, D + 1>(ks_dma, ks_next);
     }
   }
@@ -415,34 +452,45 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     }
     T.p_kstep = kBK;
   }
-  // Scale DMA: instruction i of wave w, lane l -> tile row (w*4 + i)*16 + l/4, K block
-  // (batch*4 + l%4); LDS float index (row * 4 + l%4) of the batch buffer.
+  // Scale DMA sources (resources range-checked to the end of each scale tensor).
   {
-    const int64_t q_sld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;
+    const int64_t q_sld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;  // floats per Q scale row
     T.sq_base = g.sQ + k0 / kTile;
+    const int64_t sq_total = q_rows * q_sld;
+    int64_t sp_total;
     if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
       T.sp_base = g.sP + (int64_t)e * (g.Np / kTile) * (g.Kdim / kTile);
       T.sp_kb = 1;
+      sp_total = (int64_t)(g.E - e) * (g.Np / kTile) * (g.Kdim / kTile);
     } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]
       T.sp_base = g.sP + (int64_t)e * (g.Kdim / kTile) * (g.Np / kTile);
       T.sp_kb = (int)(g.Np / kTile);
+      sp_total = (int64_t)(g.E - e) * (g.Kdim / kTile) * (g.Np / kTile);
     } else {  // xT_s [Np][M_cap/128]
       T.sp_base = g.sP + k0 / kTile;
       T.sp_kb = 1;
+      sp_total = g.Np * (g.M_cap / kTile);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = (wave * 4 + i) * 16 + (lane >> 2);
+    sp_total -= (MODE == kWgrad) ? k0 / kTile : 0;
+    const int r = 64 * wave + lane;  // tile row of this lane's Q (and wgrad P) scales
+    int64_t q = q0 + r;
+    q = q < q_rows ? q : q_rows - 1;
+    T.sq_off = (uint32_t)(q * q_sld * 4);
+    if (MODE == kWgrad) {
       int64_t p = p0 + r;
       p = p < g.Np ? p : g.Np - 1;
-      int64_t q = q0 + r;
-      q = q < q_rows ? q : q_rows - 1;
-      if (MODE == kFprop) T.sp_off[i] = (uint32_t)((p / kTile) * (g.Kdim / kTile) * 4);
-      else if (MODE == kDgrad) T.sp_off[i] = (uint32_t)((p / kTile) * 4);
-      else T.sp_off[i] = (uint32_t)(p * (g.M_cap / kTile) * 4);
-      T.sq_off[i] = (uint32_t)(q * q_sld * 4);
+      T.sp_off = (uint32_t)(p * (g.M_cap / kTile) * 4);
+    } else {
+      int64_t pb = p0 / kTile + ((lane >> 2) & 1);  // the tile's two weight block rows
+      pb = pb < g.Np / kTile ? pb : g.Np / kTile - 1;
+      const int j = lane & 3;
+      T.sp_off = (uint32_t)(((MODE == kFprop) ? pb * (g.Kdim / kTile) + j : j * (g.Np / kTile) + pb) * 4);
     }
+    T.sp_rsrc = make_rsrc(T.sp_base, (uint32_t)(sp_total * 4));
+    T.sq_rsrc = make_rsrc(T.sq_base, (uint32_t)((sq_total - ((MODE == kWgrad) ? k0 / kTile : 0)) * 4));
   }
+  T.p_rsrc = make_rsrc(T.p_base);
+  T.q_rsrc = make_rsrc(T.q_base);
 
 #pragma unroll
   for (int a = 0; a < 4; ++a)
@@ -473,9 +521,8 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     T.template dma_tile<1, 9>(s1); T.template dma_tile<1, 10>(s1); T.template dma_tile<1, 11>(s1);
     T.template dma_tile<1, 12>(s1); T.template dma_tile<1, 13>(s1); T.template dma_tile<1, 14>(s1);
     T.template dma_tile<1, 15>(s1);
-    T.template dma_scale<0>(0); T.template dma_scale<1>(0); T.template dma_scale<2>(0);
-    T.template dma_scale<3>(0); T.template dma_scale<4>(0); T.template dma_scale<5>(0);
-    T.template dma_scale<6>(0); T.template dma_scale<7>(0);
+    T.dma_scale_p(0);
+    T.dma_scale_q(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     T.template read_all_from<0, 0, true, 0>();
