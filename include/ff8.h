@@ -37,8 +37,9 @@
  *    launched.  FF8_ERR_HIP means a launch failed; ff8_last_error() then holds
  *    the HIP message (thread-local, valid until the next call on the thread).
  *  - Dimensions H, N, K, I, cols must be multiples of 128; M_cap and rows must
- *    be multiples of 128.  The grouped GEMMs also need M_cap * max(N, K) < 2^32 and
- *    N * K < 2^32 (each operand tensor, and each expert's weight, under 4 GiB).
+ *    be multiples of 128.  The grouped GEMMs also need M_cap * max(N, K) < 2^32 and,
+ *    for fprop and dgrad, E * N * K < 2^32 (each operand tensor, including all
+ *    experts' weights together, under 4 GiB); larger shapes return FF8_ERR_SHAPE.
  */
 #ifndef FF8_H
 #define FF8_H

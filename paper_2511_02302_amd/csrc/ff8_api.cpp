@@ -137,23 +137,24 @@ int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows,
 }
 
 static int gemm_common(const char* fn, const void* a, const void* as, const void* b, const void* bs,
-                       const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, const void* out) {
+                       const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, const void* out,
+                       bool expert_weights) {
   if (!a || !as || !b || !bs || !offsets || !out) return fail(FF8_ERR_NULL, "%s: a required pointer is NULL", fn);
   if (E < 1) return fail(FF8_ERR_ARG, "%s: E must be >= 1", fn);
   if (!mult128(M_cap) || !mult128(N) || !mult128(K))
     return fail(FF8_ERR_SHAPE, "%s: M_cap, N and K must be positive multiples of 128", fn);
-  // the kernels address each operand tensor (one expert's weight, the token-major
-  // activations) with 32-bit byte offsets
+  // the kernels address each operand tensor (the token-major activations, all experts'
+  // weights) with 32-bit byte offsets
   const int64_t lim = (int64_t)1 << 32;
-  if (M_cap * (N > K ? N : K) >= lim || N * K >= lim)
-    return fail(FF8_ERR_SHAPE, "%s: an operand exceeds 4 GiB (M_cap*max(N,K) and N*K must be < 2^32)", fn);
+  if (M_cap * (N > K ? N : K) >= lim || (expert_weights ? (int64_t)E * N * K : N * K) >= lim)
+    return fail(FF8_ERR_SHAPE, "%s: an operand exceeds 4 GiB (M_cap*max(N,K) and E*N*K must be < 2^32)", fn);
   return FF8_OK;
 }
 
 int ff8_grouped_gemm_fprop(const ff8_e4m3* a, const float* a_s, const ff8_e4m3* w, const float* w_s,
                            const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
                            void* stream) {
-  const int rc = gemm_common(__func__, a, a_s, w, w_s, offsets, E, M_cap, N, K, out);
+  const int rc = gemm_common(__func__, a, a_s, w, w_s, offsets, E, M_cap, N, K, out, true);
   if (rc != FF8_OK) return rc;
   return hip_status(ff8::launch_grouped_gemm(ff8::kFprop, a, a_s, w, w_s, offsets, E, M_cap, N, K, out, 0,
                                              as_stream(stream)),
@@ -163,7 +164,7 @@ int ff8_grouped_gemm_fprop(const ff8_e4m3* a, const float* a_s, const ff8_e4m3* 
 int ff8_grouped_gemm_dgrad(const ff8_e4m3* g, const float* g_s, const ff8_e4m3* w, const float* w_s,
                            const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
                            void* stream) {
-  const int rc = gemm_common(__func__, g, g_s, w, w_s, offsets, E, M_cap, N, K, out);
+  const int rc = gemm_common(__func__, g, g_s, w, w_s, offsets, E, M_cap, N, K, out, true);
   if (rc != FF8_OK) return rc;
   return hip_status(ff8::launch_grouped_gemm(ff8::kDgrad, g, g_s, w, w_s, offsets, E, M_cap, N, K, out, 0,
                                              as_stream(stream)),
@@ -173,7 +174,7 @@ int ff8_grouped_gemm_dgrad(const ff8_e4m3* g, const float* g_s, const ff8_e4m3* 
 int ff8_grouped_gemm_wgrad(const ff8_e4m3* gT, const float* gT_s, const ff8_e4m3* xT, const float* xT_s,
                            const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, float* dw,
                            int accumulate, void* stream) {
-  const int rc = gemm_common(__func__, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw);
+  const int rc = gemm_common(__func__, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw, false);
   if (rc != FF8_OK) return rc;
   REQUIRE_ARG(accumulate == 0 || accumulate == 1);
   return hip_status(ff8::launch_grouped_gemm(ff8::kWgrad, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw,

@@ -54,14 +54,14 @@ constexpr int kTileBytes = kTP * kBK;  // 32 KB per operand per stage
 constexpr int kScaleBatch = 4;         // K blocks per scale batch
 constexpr int kDmaPerSlot = 1;         // tile DMA instructions issued per MFMA slot
 constexpr int kReadSlots = 8;          // MFMA slots of a half-step that carry fragment reads
-constexpr bool kBufferDma = true;      // MUBUF LDS DMA (false: global_load_lds)
 // Rotate each XCD block's K order (memory-channel spread).  Measured: +5.6% for fprop,
 // whose two operands are row-major over K; -1% / -3% for dgrad / wgrad, which keep it off.
 template <int MODE> constexpr bool kStaggerK = (MODE == kFprop);
 
 __shared__ __attribute__((aligned(1024))) uint8_t g_st0[2 * kTileBytes], g_st1[2 * kTileBytes];  // [P | Q]
 __shared__ __attribute__((aligned(1024))) float g_sc[2][2 * kTP * kScaleBatch];  // [P rows x 4 | Q rows x 4]
-__shared__ int g_cum[1025];
+__shared__ int g_cum[1025];  // fprop/dgrad: cumulative 256-row tile counts per expert
+__shared__ int g_off[1025];  // fprop/dgrad: expert row offsets
 
 template <int B> __device__ __forceinline__ uint8_t* stage_buf() {
   if constexpr (B == 0) return g_st0; else return g_st1;
@@ -81,10 +81,10 @@ struct GemmArgs {
   const int32_t* offsets;
   void* out;
   int E;
-  int64_t M_cap;
-  int64_t Np;         // extent of p (output columns)
-  int64_t Nq;         // wgrad: extent of q (N); fprop/dgrad: unused
-  int64_t Kdim;       // fprop/dgrad: contraction length; wgrad: unused (per group)
+  int M_cap;          // dimensions are below 2^31 (byte offsets below 2^32 are checked on the host)
+  int Np;             // extent of p (output columns)
+  int Nq;             // wgrad: extent of q (N); fprop/dgrad: unused
+  int Kdim;           // fprop/dgrad: contraction length; wgrad: unused (per group)
   int n_pt, n_qt;     // p tiles; q tiles (wgrad only)
   int accumulate;
 };
@@ -94,12 +94,13 @@ __device__ __forceinline__ int kswz(int r) { return (r ^ (r >> 3)) & 7; }
 // dgrad weight stage tile: 128 rows (n) x 256 bytes, chunk c of row n at c ^ wswz(n % 8).
 __device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
 
-// LDS DMA: each lane loads 16 (or 4) bytes from base + soff + voff into LDS at M0 + 16 *
-// lane (or 4 * lane).  Issued through inline asm so that the compiler does not serialize
-// the pipeline with conservative waits; the kernel waits for its own DMA (vmcnt) before
-// the barrier that publishes a stage.  Two encodings: MUBUF (buffer_load ... lds, a
-// 128-bit resource per operand; base in the resource, stage offset in soffset) and
-// global (global_load_lds_*, 64-bit scalar base).
+// LDS DMA (buffer_load ... lds): each lane loads 16 (or 4) bytes at resource base +
+// soff + voff into LDS at M0 + 16 * lane (or 4 * lane).  The resources cover exactly
+// their tensor, and every operand offset is in voffset, which the hardware range-checks:
+// rows past a tensor's end read zeros, so tiles at the edges need no clamping.  Issued
+// through inline asm so that the compiler does not serialize the pipeline with
+// conservative waits; the kernel waits for its own DMA (vmcnt) before the barrier that
+// publishes a stage.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 // Raw (stride 0) buffer resource: loads at offsets >= `bytes` return zeros.
 __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0xFFFFFFFFu) {
@@ -111,14 +112,9 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0x
   r[3] = 0x00020000;   // raw 32-bit data format
   return r;
 }
-__device__ __forceinline__ void dma16(const void* sbase, const i32x4& rsrc, uint32_t soff, uint32_t voff,
-                                      uint32_t lds_off) {
-  if constexpr (kBufferDma)
-    asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc),
-                 "s"(soff) : "memory");
-  else
-    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" : : "{m0}"(lds_off), "v"(voff),
-                 "s"((const uint8_t*)sbase + soff) : "memory");
+__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+               : "memory");
 }
 // Range-checked scale DMA (always MUBUF: tail lanes may point past the scale tensor).
 __device__ __forceinline__ void dma4r(const i32x4& rsrc, uint32_t soff, uint32_t voff, uint32_t lds_off) {
@@ -150,35 +146,52 @@ struct Tile {
   // the next batch, assembled during the last stage of the current one.
   uint32_t cp[4], cq[4], np[4], nq[4];
   u32x4 rsp[4], rsq[4];  // raw fp32 scale rows of the next batch, between read and pack
-  // DMA sources: wave-uniform bases, per-lane 32-bit byte offsets
-  const uint8_t* p_base;
-  const uint8_t* q_base;
-  const float* sp_base;
-  const float* sq_base;
-  i32x4 p_rsrc, q_rsrc, sp_rsrc, sq_rsrc;  // MUBUF resources of the four bases
-  uint32_t p_off[8], q_off[8];   // tile DMA instruction i, stage 0
+  // DMA sources: one resource per tensor; per-lane byte offsets of this tile's stage 0
+  // for the two row-group patterns of the tile DMA (instruction i uses pattern i / 4,
+  // dgrad P: i % 2), and wave-uniform steps between instructions and stages.
+  i32x4 p_rsrc, q_rsrc, sp_rsrc, sq_rsrc;
+  uint32_t p_voff[2], q_voff[2];
   uint32_t sp_off, sq_off;       // scale DMA: this lane's source offset at K block 0
-  int64_t p_kstep;               // bytes per stage of the P source
+  int p_kstep, q_kstep;          // bytes per stage of the P / Q source
+  int p_istep, q_istep;          // bytes between instructions of one pattern
   int sp_kb;                     // floats per K block of the P scale source (q scales: 1)
   // fprop / dgrad: a wave's 128 P rows are one 128x128 weight block, so its P scale is one
   // value per K block (stored compactly as [tile half][4 K blocks]); wgrad: one per row.
   static constexpr bool kBlockP = (MODE != kWgrad);
   int wave, lane, wp, wq;
-  int64_t nk;
-  int64_t k_rot;  // K stages this tile's loop is rotated by (a multiple of the scale batch)
+  int nk;
+  int k_rot;  // K stages this tile's loop is rotated by (a multiple of the scale batch)
   // Stage ks of the loop reads K block (ks + k_rot) mod nk.
-  __device__ __forceinline__ int64_t kphys(int64_t ks) const {
-    const int64_t k = ks + k_rot;
+  __device__ __forceinline__ int kphys(int ks) const {
+    const int k = ks + k_rot;
     return k < nk ? k : k - nk;
   }
 
   // Tile DMA instruction I (0..15) of stage ks into stage buffer B: 0-7 P, 8-15 Q.
+  // K-major tiles (fprop / wgrad operands, dgrad Q): instruction i of wave w carries row
+  // group w + 8i (i < 4) or w + 4 + 8(i - 4) (i >= 4) -- 8 rows x 128 bytes, LDS 1 KB at
+  // group * 1 KB -- so that within each pattern the swizzle (row group % 8) is constant
+  // and consecutive instructions are one uniform step apart.  dgrad P (W_e rows n, 256
+  // bytes): instruction i carries rows 32w + 4i .., patterns by i % 2.
   template <int B, int I>
-  __device__ __forceinline__ void dma_tile(int64_t ks) {
-    const uint32_t base = stage_lds<B>() + (uint32_t)wave * 8192u;  // the wave's 8 KB slice of each tile
-    const int64_t kp = __builtin_amdgcn_readfirstlane((int)kphys(ks));  // uniform: keep the base scalar
-    if constexpr (I < 8) dma16(p_base, p_rsrc, (uint32_t)(kp * p_kstep), p_off[I], base + I * 1024);
-    else dma16(q_base, q_rsrc, (uint32_t)(kp * kBK), q_off[I - 8], base + kTileBytes + (I - 8) * 1024);
+  __device__ __forceinline__ void dma_tile(int ks) {
+    const uint32_t stage = stage_lds<B>();
+    const uint32_t kp = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(ks));  // uniform
+    if constexpr (I < 8) {
+      if constexpr (MODE == kDgrad) {
+        const uint32_t step = kp * (uint32_t)p_kstep + (uint32_t)(I >> 1) * (uint32_t)p_istep;
+        dma16(p_rsrc, p_voff[I & 1] + step, stage + (uint32_t)wave * 8192u + I * 1024);
+      } else {
+        const uint32_t step = kp * (uint32_t)p_kstep + (uint32_t)(I & 3) * (uint32_t)p_istep;
+        const uint32_t grp = (uint32_t)wave + (I < 4 ? 8 * I : 4 + 8 * (I - 4));
+        dma16(p_rsrc, p_voff[I >> 2] + step, stage + grp * 1024u);
+      }
+    } else {
+      constexpr int J = I - 8;
+      const uint32_t step = kp * (uint32_t)q_kstep + (uint32_t)(J & 3) * (uint32_t)q_istep;
+      const uint32_t grp = (uint32_t)wave + (J < 4 ? 8 * J : 4 + 8 * (J - 4));
+      dma16(q_rsrc, q_voff[J >> 2] + step, stage + kTileBytes + grp * 1024u);
+    }
   }
   // Scale DMA of batch b (K blocks 4b..4b+3) into batch buffer b % 2, rows of four floats:
   // the P instruction (kBlockP: 8 lanes carry the two weight blocks' 4 floats, the rest
@@ -186,15 +199,15 @@ struct Tile {
   // l carries tile row 64 wave + l).  Batches are rotated with the K order (k_rot is a
   // multiple of the batch); blocks past the last K block read neighbouring rows or zeros
   // (range-checked resources) and are never multiplied.
-  __device__ __forceinline__ void dma_scale_p(int64_t b) {
+  __device__ __forceinline__ void dma_scale_p(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1));
-    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)kphys(b * kScaleBatch));
+    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
     if constexpr (kBlockP) dma4r(sp_rsrc, kb0 * (uint32_t)sp_kb * 4u, sp_off, lbase);
     else dma16r(sp_rsrc, kb0 * 4u, sp_off, lbase + (uint32_t)wave * 1024u);
   }
-  __device__ __forceinline__ void dma_scale_q(int64_t b) {
+  __device__ __forceinline__ void dma_scale_q(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1)) + kTP * kScaleBatch * 4;
-    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)kphys(b * kScaleBatch));
+    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
     dma16r(sq_rsrc, kb0 * 4u, sq_off, lbase + (uint32_t)wave * 1024u);
   }
 
@@ -237,23 +250,33 @@ struct Tile {
       read_all_from<B, H, kSetA, J + 1>();
     }
   }
-  // Scales of batch b (LDS buffer b % 2, rows of four K-block floats): read the four
-  // rows of one operand this lane multiplies (kQ: Q rows) into raw[R][j] ...
+  // Scales of batch b (LDS buffer b % 2, rows of four K-block floats): read the rows of
+  // one operand this lane multiplies into raw (kQ, or wgrad P: rows 128 w + 32 R + l for
+  // R = 0..3; fprop / dgrad P: the wave's one weight-block row, raw[0] only) ...
   template <bool kQ>
-  __device__ __forceinline__ void read_scale_rows(int64_t b, u32x4 (&raw)[4]) {
+  __device__ __forceinline__ void read_scale_rows(int b, u32x4 (&raw)[4]) {
     const u32x4* S = reinterpret_cast<const u32x4*>(&g_sc[b & 1][0]);
     const int l31 = lane & 31;
+    if constexpr (!kQ && kBlockP) {
+      raw[0] = S[wp];
+    } else {
 #pragma unroll
-    for (int R = 0; R < 4; ++R)
-      raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : (kBlockP ? S[wp] : S[128 * wp + 32 * R + l31]);
+      for (int R = 0; R < 4; ++R) raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : S[128 * wp + 32 * R + l31];
+    }
   }
   // ... and pack them: word j holds the E8M0 byte (the fp32 exponent field of a
   // positive power of two) of row R in byte R.
+  template <bool kQ>
   __device__ __forceinline__ static void pack_scales(const u32x4 (&raw)[4], uint32_t (&dst)[4]) {
+    if constexpr (!kQ && kBlockP) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      dst[j] = (raw[0][j] >> 23) | ((raw[1][j] >> 15) & 0xff00u) | ((raw[2][j] >> 7) & 0xff0000u) |
-               ((raw[3][j] << 1) & 0xff000000u);
+      for (int j = 0; j < 4; ++j) dst[j] = (raw[0][j] >> 23) * 0x01010101u;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        dst[j] = (raw[0][j] >> 23) | ((raw[1][j] >> 15) & 0xff00u) | ((raw[2][j] >> 7) & 0xff0000u) |
+                 ((raw[3][j] << 1) & 0xff000000u);
+    }
   }
 
   template <bool kSetA, int S4, int I>
@@ -267,7 +290,7 @@ struct Tile {
   // Tile DMA instructions of second-half slot I (kDmaPerSlot per slot from slot 0), and
   // the scale batch's eight spread over the same slots.
   template <int B, int S4, int I, int D>
-  __device__ __forceinline__ void dma_slot(int64_t ks_dma, int64_t ks_next) {
+  __device__ __forceinline__ void dma_slot(int ks_dma, int ks_next) {
     if constexpr (D < kDmaPerSlot && kDmaPerSlot * I + D < 16) {
       dma_tile<B, kDmaPerSlot * I + D>(ks_dma);
       if constexpr (S4 == 0 && kDmaPerSlot * I + D == 1) dma_scale_p((ks_next >> 2) + 1);
@@ -308,15 +331,15 @@ struct Tile {
   // reads of stage ks+1's first half (other buffer) into set A follow over the first
   // eight; in the last stage of a batch the next batch's scales are read and packed.
   template <int B, int S4, int I>
-  __device__ __forceinline__ void half1_from(int64_t ks_dma, int64_t ks_next) {
+  __device__ __forceinline__ void half1_from(int ks_dma, int ks_next) {
     if constexpr (I < 16) {
       mfma_op<false, S4, I>();
       dma_slot<B, S4, I, 0>(ks_dma, ks_next);
       reads_of_slot<1 - B, 0, true, I>();
       if constexpr (S4 == 3 && I == 8) read_scale_rows<false>(ks_next >> 2, rsp);
       if constexpr (S4 == 3 && I == 9) read_scale_rows<true>(ks_next >> 2, rsq);
-      if constexpr (S4 == 3 && I == 12) pack_scales(rsp, np);
-      if constexpr (S4 == 3 && I == 14) pack_scales(rsq, nq);
+      if constexpr (S4 == 3 && I == 12) pack_scales<false>(rsp, np);
+      if constexpr (S4 == 3 && I == 14) pack_scales<true>(rsq, nq);
       __builtin_amdgcn_sched_barrier(0);
       half1_from<B, S4, I + 1>(ks_dma, ks_next);
     }
@@ -327,7 +350,7 @@ struct Tile {
   // ks+1 is visible to all and buffer ks % 2 is free for stage ks+2.  Stages past the
   // end are reloads of the last one (in bounds, never multiplied).
   template <int S4>
-  __device__ __forceinline__ void stage(int64_t ks) {
+  __device__ __forceinline__ void stage(int ks) {
     constexpr int B = S4 % 2;
     half0_from<B, S4, 0>();
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
@@ -344,222 +367,155 @@ struct Tile {
   }
 };
 
-template <int MODE>
-__global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
-  const int tid = threadIdx.x;
-  Tile<MODE> T;
-  T.lane = tid & 63;
-  T.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  T.wp = T.wave & 1;
-  T.wq = T.wave >> 1;
+// One tile of the grouped product: expert e, q rows [q0, q_end) of a 256-row tile, p
+// columns from p0, contraction from k0 over nk stages.
+struct TileInfo {
+  int e, blk;
+  int q0, q_end, k0, p0, nk;  // rows, columns and stages all stay below 2^31
+};
 
-  // ---- tile order ----
-  // Workgroups are dispatched round-robin over the 8 XCDs (32 CUs each).  Each XCD
-  // works on blocks of kBQ x kBP = 32 tiles (q-tiles x p-tiles), so its 32 resident
-  // workgroups share 8 q panels and 4 p panels per K step in its L2; consecutive blocks
-  // go to consecutive XCDs with the p-block fastest, so the 8 XCDs together sweep one
-  // 16 x 16-tile window (about one expert) at a time and its operands stay in the MALL.
-  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int blk = (slot >> 5) * 8 + xcd, w_in = slot & 31;
+// Tile w_in of XCD block blk (kBQ x kBP tiles, p fastest).  False for tiles past the
+// edges.  fprop/dgrad: q tiles are 256-row tiles of the expert groups (g_cum / g_off:
+// cumulative tile counts and row offsets per expert, in LDS).
+template <int MODE>
+__device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in, TileInfo& t) {
   const int n_pb = (g.n_pt + kBP - 1) / kBP;
   const int qb = blk / n_pb, pb = blk - qb * n_pb;
   const int qg = qb * kBQ + w_in / kBP;  // global q-tile index
   const int pt = pb * kBP + w_in % kBP;
-  if (pt >= g.n_pt) return;
-
-  // ---- tile decode (uniform) ----
-  int e;
-  int64_t q0, q_end, k0;
+  if (pt >= g.n_pt) return false;
+  t.blk = blk;
+  t.p0 = (int64_t)pt * kTP;
   if (MODE != kWgrad) {
-    // cumulative 256-row tile counts per expert: one wave, 64 experts per pass
-    if (tid < 64) {
-      int carry = 0;
-      for (int base = 0; base < g.E; base += 64) {
-        const int i = base + tid;
-        int v = i < g.E ? (g.offsets[i + 1] - g.offsets[i] + kTQ - 1) / kTQ : 0;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-          const int u = __shfl_up(v, d);
-          if (tid >= d) v += u;
-        }
-        if (i < g.E) g_cum[i + 1] = carry + v;
-        carry += __shfl(v, 63);
-      }
-      if (tid == 0) g_cum[0] = 0;
-    }
-    __syncthreads();
-    if (qg >= g_cum[g.E]) return;
+    if (qg >= g_cum[g.E]) return false;
     int lo = 0, hi = g.E - 1;  // largest e with cum[e] <= qg
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
       if (g_cum[mid] <= qg) lo = mid; else hi = mid - 1;
     }
-    e = __builtin_amdgcn_readfirstlane(lo);
-    const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
-    const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
-    const int c0 = __builtin_amdgcn_readfirstlane(g_cum[e]);
-    q0 = o0 + (int64_t)(qg - c0) * kTQ;
-    q_end = o1;
-    k0 = 0;
-    T.nk = g.Kdim / kBK;
+    const int e = __builtin_amdgcn_readfirstlane(lo);
+    t.e = e;
+    t.q0 = g_off[e] + (int64_t)(qg - g_cum[e]) * kTQ;
+    t.q_end = g_off[e + 1];
+    t.k0 = 0;
+    t.nk = g.Kdim / kBK;
   } else {
-    if (qg >= g.E * g.n_qt) return;
-    e = qg / g.n_qt;
-    const int qt = qg - e * g.n_qt;
-    q0 = (int64_t)qt * kTQ;
-    q_end = g.Nq;
+    if (qg >= g.E * g.n_qt) return false;
+    const int e = qg / g.n_qt;
+    t.e = e;
+    t.q0 = (int64_t)(qg - e * g.n_qt) * kTQ;
+    t.q_end = g.Nq;
     const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
     const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
-    k0 = o0;
-    T.nk = (o1 - o0) / kBK;
+    t.k0 = o0;
+    t.nk = (o1 - o0) / kBK;
   }
-  const int64_t p0 = (int64_t)pt * kTP;
-  const int lane = T.lane, wave = T.wave;
+  return true;
+}
 
-  // ---- DMA sources (lane l of tile DMA instruction i writes LDS bytes 16 l .. of 1 KB) ----
+// DMA sources of tile t: wave-uniform bases and resources, per-lane offsets (lane l of
+// tile DMA instruction i writes LDS bytes 16 l .. of that instruction's 1 KB).
+template <int MODE>
+__device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, const TileInfo& t) {
+  const int lane = T.lane, wave = T.wave, e = t.e;
+  const int64_t q0 = t.q0, k0 = t.k0, p0 = t.p0;
+  T.nk = t.nk;
   const int64_t q_ld = (MODE == kWgrad) ? g.M_cap : g.Kdim;
   const int64_t q_rows = (MODE == kWgrad) ? g.Nq : g.M_cap;
-  T.q_base = g.Q + k0;
+  // K-major row of pattern h (h = 0, 1) for this lane: group w + 4h, row 8 group + l / 8,
+  // 16-byte chunk (l % 8) ^ kswz(row) (kswz depends on row % 8 and group % 8 only).
+  T.q_rsrc = make_rsrc(g.Q, (uint32_t)(q_rows * q_ld));
+  T.q_kstep = kBK;
+  T.q_istep = (int)(64 * q_ld);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = (wave * 8 + i) * 8 + (lane >> 3);
+  for (int hh = 0; hh < 2; ++hh) {
+    const int r = 8 * (wave + 4 * hh) + (lane >> 3);
     const int c = (lane & 7) ^ kswz(r);
-    int64_t row = q0 + r;
-    row = row < q_rows ? row : q_rows - 1;
-    T.q_off[i] = (uint32_t)(row * q_ld + c * 16);
+    T.q_voff[hh] = (uint32_t)((q0 + r) * q_ld + k0 + c * 16);
   }
-  if (MODE == kDgrad) {
-    T.p_base = g.P + (int64_t)e * g.Kdim * g.Np;  // W_e [N = Kdim][K = Np]
+  if (MODE == kDgrad) {  // W_e [N = Kdim][K = Np], rows n = 32w + 4i + l / 16
+    T.p_rsrc = make_rsrc(g.P, (uint32_t)((int64_t)g.E * g.Kdim * g.Np));
+    T.p_kstep = kBK * g.Np;
+    T.p_istep = 8 * g.Np;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int n = (wave * 8 + i) * 4 + (lane >> 4);
+    for (int hh = 0; hh < 2; ++hh) {
+      const int n = 32 * wave + 4 * hh + (lane >> 4);
       const int c = (lane & 15) ^ wswz(n & 7);
-      int64_t col = p0 + c * 16;
-      col = col < g.Np ? col : g.Np - 16;
-      T.p_off[i] = (uint32_t)((int64_t)n * g.Np + col);
+      T.p_voff[hh] = (uint32_t)(((int64_t)e * g.Kdim + n) * g.Np + p0 + c * 16);
     }
-    T.p_kstep = (int64_t)kBK * g.Np;
   } else {
     const int64_t p_ld = (MODE == kWgrad) ? g.M_cap : g.Kdim;
-    T.p_base = ((MODE == kFprop) ? g.P + (int64_t)e * g.Np * g.Kdim : g.P) + k0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = (wave * 8 + i) * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ kswz(r);
-      int64_t row = p0 + r;
-      row = row < g.Np ? row : g.Np - 1;
-      T.p_off[i] = (uint32_t)(row * p_ld + c * 16);
-    }
+    const int64_t p_rows = (MODE == kWgrad) ? g.Np : (int64_t)g.E * g.Np;  // fprop: all experts' rows
+    const int64_t p_row0 = (MODE == kFprop) ? (int64_t)e * g.Np + p0 : p0;
+    T.p_rsrc = make_rsrc(g.P, (uint32_t)(p_rows * p_ld));
     T.p_kstep = kBK;
-  }
-  // Scale DMA sources (resources range-checked to the end of each scale tensor).
-  {
-    const int64_t q_sld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;  // floats per Q scale row
-    T.sq_base = g.sQ + k0 / kTile;
-    const int64_t sq_total = q_rows * q_sld;
-    int64_t sp_total;
-    if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
-      T.sp_base = g.sP + (int64_t)e * (g.Np / kTile) * (g.Kdim / kTile);
-      T.sp_kb = 1;
-      sp_total = (int64_t)(g.E - e) * (g.Np / kTile) * (g.Kdim / kTile);
-    } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]
-      T.sp_base = g.sP + (int64_t)e * (g.Kdim / kTile) * (g.Np / kTile);
-      T.sp_kb = (int)(g.Np / kTile);
-      sp_total = (int64_t)(g.E - e) * (g.Kdim / kTile) * (g.Np / kTile);
-    } else {  // xT_s [Np][M_cap/128]
-      T.sp_base = g.sP + k0 / kTile;
-      T.sp_kb = 1;
-      sp_total = g.Np * (g.M_cap / kTile);
+    T.p_istep = (int)(64 * p_ld);
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int r = 8 * (wave + 4 * hh) + (lane >> 3);
+      const int c = (lane & 7) ^ kswz(r);
+      T.p_voff[hh] = (uint32_t)((p_row0 + r) * p_ld + k0 + c * 16);
     }
-    sp_total -= (MODE == kWgrad) ? k0 / kTile : 0;
-    const int r = 64 * wave + lane;  // tile row of this lane's Q (and wgrad P) scales
-    int64_t q = q0 + r;
-    q = q < q_rows ? q : q_rows - 1;
-    T.sq_off = (uint32_t)(q * q_sld * 4);
-    if (MODE == kWgrad) {
-      int64_t p = p0 + r;
-      p = p < g.Np ? p : g.Np - 1;
-      T.sp_off = (uint32_t)(p * (g.M_cap / kTile) * 4);
-    } else {
-      int64_t pb = p0 / kTile + ((lane >> 2) & 1);  // the tile's two weight block rows
-      pb = pb < g.Np / kTile ? pb : g.Np / kTile - 1;
-      const int j = lane & 3;
-      T.sp_off = (uint32_t)(((MODE == kFprop) ? pb * (g.Kdim / kTile) + j : j * (g.Np / kTile) + pb) * 4);
-    }
-    T.sp_rsrc = make_rsrc(T.sp_base, (uint32_t)(sp_total * 4));
-    T.sq_rsrc = make_rsrc(T.sq_base, (uint32_t)((sq_total - ((MODE == kWgrad) ? k0 / kTile : 0)) * 4));
   }
-  T.p_rsrc = make_rsrc(T.p_base);
-  T.q_rsrc = make_rsrc(T.q_base);
-
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) T.acc[a][b][v] = 0.0f;
-
+  // scale DMA sources (resources range-checked to the end of each scale tensor)
+  const int64_t q_sld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;  // floats per Q scale row
+  const float* sq_base = g.sQ + k0 / kTile;
+  const float* sp_base;
+  const int64_t sq_total = q_rows * q_sld - ((MODE == kWgrad) ? k0 / kTile : 0);
+  int64_t sp_total;
+  if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
+    sp_base = g.sP + (int64_t)e * (g.Np / kTile) * (g.Kdim / kTile);
+    T.sp_kb = 1;
+    sp_total = (int64_t)(g.E - e) * (g.Np / kTile) * (g.Kdim / kTile);
+  } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]
+    sp_base = g.sP + (int64_t)e * (g.Kdim / kTile) * (g.Np / kTile);
+    T.sp_kb = (int)(g.Np / kTile);
+    sp_total = (int64_t)(g.E - e) * (g.Kdim / kTile) * (g.Np / kTile);
+  } else {  // xT_s [Np][M_cap/128]
+    sp_base = g.sP + k0 / kTile;
+    T.sp_kb = 1;
+    sp_total = g.Np * (g.M_cap / kTile) - k0 / kTile;
+  }
+  const int r = 64 * wave + lane;  // tile row of this lane's Q (and wgrad P) scales
+  int64_t q = q0 + r;
+  q = q < q_rows ? q : q_rows - 1;
+  T.sq_off = (uint32_t)(q * q_sld * 4);
+  if (MODE == kWgrad) {
+    int64_t p = p0 + r;
+    p = p < g.Np ? p : g.Np - 1;
+    T.sp_off = (uint32_t)(p * (g.M_cap / kTile) * 4);
+  } else {
+    int64_t pb = p0 / kTile + ((lane >> 2) & 1);  // the tile's two weight block rows
+    pb = pb < g.Np / kTile ? pb : g.Np / kTile - 1;
+    const int j = lane & 3;
+    T.sp_off = (uint32_t)(((MODE == kFprop) ? pb * (g.Kdim / kTile) + j : j * (g.Np / kTile) + pb) * 4);
+  }
+  T.sp_rsrc = make_rsrc(sp_base, (uint32_t)(sp_total * 4));
+  T.sq_rsrc = make_rsrc(sq_base, (uint32_t)(sq_total * 4));
   // Blocks start their K loops at different scale-batch-aligned stages, so that the XCDs
   // running together stream different K bands of the operand rows (spread over memory
   // channels) while the 32 tiles of one block still share every stage through their L2.
   T.k_rot = (kStaggerK<MODE> && (T.nk & (kScaleBatch - 1)) == 0 && T.nk >= 2 * kScaleBatch)
-                ? (int64_t)((blk * 5) % (int)(T.nk / kScaleBatch)) * kScaleBatch
+                ? ((t.blk * 5) % (T.nk / kScaleBatch)) * kScaleBatch
                 : 0;
-  const int64_t nk = T.nk;
-  if (nk > 0) {
-    // prologue: stages 0 and 1, scale batch 0; then stage 0's first-half fragments
-    T.template dma_tile<0, 0>(0); T.template dma_tile<0, 1>(0); T.template dma_tile<0, 2>(0);
-    T.template dma_tile<0, 3>(0); T.template dma_tile<0, 4>(0); T.template dma_tile<0, 5>(0);
-    T.template dma_tile<0, 6>(0); T.template dma_tile<0, 7>(0); T.template dma_tile<0, 8>(0);
-    T.template dma_tile<0, 9>(0); T.template dma_tile<0, 10>(0); T.template dma_tile<0, 11>(0);
-    T.template dma_tile<0, 12>(0); T.template dma_tile<0, 13>(0); T.template dma_tile<0, 14>(0);
-    T.template dma_tile<0, 15>(0);
-    const int64_t s1 = nk > 1 ? 1 : 0;
-    T.template dma_tile<1, 0>(s1); T.template dma_tile<1, 1>(s1); T.template dma_tile<1, 2>(s1);
-    T.template dma_tile<1, 3>(s1); T.template dma_tile<1, 4>(s1); T.template dma_tile<1, 5>(s1);
-    T.template dma_tile<1, 6>(s1); T.template dma_tile<1, 7>(s1); T.template dma_tile<1, 8>(s1);
-    T.template dma_tile<1, 9>(s1); T.template dma_tile<1, 10>(s1); T.template dma_tile<1, 11>(s1);
-    T.template dma_tile<1, 12>(s1); T.template dma_tile<1, 13>(s1); T.template dma_tile<1, 14>(s1);
-    T.template dma_tile<1, 15>(s1);
-    T.dma_scale_p(0);
-    T.dma_scale_q(0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    T.template read_all_from<0, 0, true, 0>();
-    {
-      u32x4 raw[4];
-      T.template read_scale_rows<false>(0, raw);
-      T.pack_scales(raw, T.cp);
-      T.template read_scale_rows<true>(0, raw);
-      T.pack_scales(raw, T.cq);
-    }
-    for (int64_t ks = 0; ks < nk; ks += 4) {
-      T.template stage<0>(ks);
-      if (ks + 1 < nk) T.template stage<1>(ks + 1);
-      if (ks + 2 < nk) T.template stage<2>(ks + 2);
-      if (ks + 3 < nk) T.template stage<3>(ks + 3);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs land before the workgroup retires
-  }
+}
 
-  // ---- epilogue ----
-  // The accumulators go out through LDS so that every global store instruction writes
-  // whole 128-byte lines (16 lanes per 256-byte bf16 row, 32 lanes per 512-byte fp32
-  // row) instead of 16-byte pieces of 32 rows.  Each wave stages its own 128 x 128
-  // sub-tile ([q][p], p contiguous) in 32 KB of the stage buffers, 16-byte chunks of row
-  // q XOR-swizzled by q, which keeps both the fragment-order writes and the row-order
-  // reads free of bank conflicts.  The barrier first retires every wave's last reads of
-  // the stage buffers (and, through each wave's own final vmcnt wait, their DMA).  The
-  // stores are non-temporal: the output is not re-read here, and streaming it keeps the
-  // operand panels that the XCD's other workgroups are still reading in L2.
-  const int wp = T.wp, wq = T.wq;
-  if (MODE == kWgrad && nk == 0 && g.accumulate) return;
-  __syncthreads();
+// Output of one tile through the LDS stage buffers (32 KB per wave).  Every global store instruction
+// writes whole 128-byte lines (16 lanes per 256-byte bf16 row, 32 lanes per 512-byte fp32
+// row) instead of 16-byte pieces of 32 rows: each wave stages 128 (bf16) or 64 (fp32) rows
+// of its 128 x 128 sub-tile at a time ([q][p], p contiguous), 16-byte chunks of row q
+// XOR-swizzled by q, conflict-free for the fragment-order writes and the row-order reads.
+// The stores are non-temporal: the output is not re-read here, and streaming it keeps the
+// operand panels that the XCD's other workgroups are still reading in L2.  A wave only
+// rewrites its own region, after its own reads (LDS order), so rounds need no barrier.
+template <int MODE>
+__device__ __forceinline__ void epilogue(Tile<MODE>& T, const GemmArgs& g, const TileInfo& t) {
+  const int lane = T.lane, wave = T.wave, wp = T.wp, wq = T.wq;
   lds_u8* const region = (lds_u8*)((wave < 2) ? g_st0 : g_st1) + (wave & 1) * 32768;
   const int l31 = lane & 31, h = lane >> 5;
-  const bool p_ok = p0 + 128 * wp < g.Np;  // Np is a multiple of 128: whole-wave predicate
+  const bool p_ok = t.p0 + 128 * wp < g.Np;  // Np is a multiple of 128: whole-wave predicate
   if (MODE == kWgrad) {
-    float* dw = static_cast<float*>(g.out) + (int64_t)e * g.Nq * g.Np + p0 + 128 * wp;
+    float* dw = static_cast<float*>(g.out) + (int64_t)t.e * g.Nq * g.Np + t.p0 + 128 * wp;
 #pragma unroll
     for (int bh = 0; bh < 2; ++bh) {
       // rows ql = 32 (b - 2 bh) + l31 of 512 bytes; chunk c = p / 4 = 8a + 2gr + h
@@ -579,8 +535,8 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
       for (int it = 0; it < 32; ++it) {
         const int ql = 2 * it + h, c = l31;
         const u32x4 v = *(__attribute__((address_space(3))) u32x4*)(region + ql * 512 + ((c ^ (ql & 31)) << 4));
-        const int64_t q = q0 + 128 * wq + 64 * bh + ql;
-        if (!p_ok || q >= q_end) continue;
+        const int64_t q = t.q0 + 128 * wq + 64 * bh + ql;
+        if (!p_ok || q >= t.q_end) continue;
         float* dst = dw + q * g.Np + 4 * c;
         if (g.accumulate) {
           const u32x4 old = ld16(dst);
@@ -594,7 +550,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
       }
     }
   } else {
-    uint16_t* out = static_cast<uint16_t*>(g.out) + p0 + 128 * wp;
+    uint16_t* out = static_cast<uint16_t*>(g.out) + t.p0 + 128 * wp;
     // rows q = 32b + l31 of 256 bytes; 8-byte piece (p = 32a + 8gr + 4h) in chunk 4a + gr, half h
 #pragma unroll
     for (int b = 0; b < 4; ++b)
@@ -612,11 +568,119 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     for (int it = 0; it < 32; ++it) {
       const int ql = 4 * it + (lane >> 4), c = lane & 15;
       const u32x4 v = *(__attribute__((address_space(3))) u32x4*)(region + ql * 256 + ((c ^ (ql & 15)) << 4));
-      const int64_t q = q0 + 128 * wq + ql;
-      if (!p_ok || q >= q_end) continue;
+      const int64_t q = t.q0 + 128 * wq + ql;
+      if (!p_ok || q >= t.q_end) continue;
       stnt16(out + q * g.Np + 8 * c, v);
     }
   }
+}
+
+// First-stage DMA of a tile: stage 0 into buffer 0, then the scale batch 0 (buffer 0).
+template <int MODE>
+__device__ __forceinline__ void dma_first_stage(Tile<MODE>& T) {
+  T.template dma_tile<0, 0>(0); T.template dma_tile<0, 1>(0); T.template dma_tile<0, 2>(0);
+  T.template dma_tile<0, 3>(0); T.template dma_tile<0, 4>(0); T.template dma_tile<0, 5>(0);
+  T.template dma_tile<0, 6>(0); T.template dma_tile<0, 7>(0); T.template dma_tile<0, 8>(0);
+  T.template dma_tile<0, 9>(0); T.template dma_tile<0, 10>(0); T.template dma_tile<0, 11>(0);
+  T.template dma_tile<0, 12>(0); T.template dma_tile<0, 13>(0); T.template dma_tile<0, 14>(0);
+  T.template dma_tile<0, 15>(0);
+  T.dma_scale_p(0);
+  T.dma_scale_q(0);
+}
+// Second-stage DMA (stage 1, or a reload of stage 0 when nk == 1) into buffer 1: exactly
+// kStage1Dma instructions per wave, the newest in flight when stage 0 is awaited.
+constexpr int kStage1Dma = 16;
+template <int MODE>
+__device__ __forceinline__ void dma_second_stage(Tile<MODE>& T) {
+  const int s1 = T.nk > 1 ? 1 : 0;
+  T.template dma_tile<1, 0>(s1); T.template dma_tile<1, 1>(s1); T.template dma_tile<1, 2>(s1);
+  T.template dma_tile<1, 3>(s1); T.template dma_tile<1, 4>(s1); T.template dma_tile<1, 5>(s1);
+  T.template dma_tile<1, 6>(s1); T.template dma_tile<1, 7>(s1); T.template dma_tile<1, 8>(s1);
+  T.template dma_tile<1, 9>(s1); T.template dma_tile<1, 10>(s1); T.template dma_tile<1, 11>(s1);
+  T.template dma_tile<1, 12>(s1); T.template dma_tile<1, 13>(s1); T.template dma_tile<1, 14>(s1);
+  T.template dma_tile<1, 15>(s1);
+}
+
+// One 256 x 256 tile per workgroup.  Workgroups are dispatched round-robin over the 8
+// XCDs (32 CUs each); the 32 consecutive workgroups of XCD x (slots s..s+31) take the
+// tiles of one XCD block (kBQ x kBP = 32 tiles: q-tiles x p-tiles, p fastest), so they
+// share 8 q panels and 4 p panels per K step in their L2, and the 8 XCDs together sweep
+// one 16 x 16-tile window (about one expert) at a time.  Surplus workgroups of the
+// host-sized grid exit at once.  All control flow is workgroup-uniform (tile decode from
+// uniform values), so every barrier is reached by all four waves.
+template <int MODE>
+__global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
+  const int tid = threadIdx.x;
+  Tile<MODE> T;
+  T.lane = tid & 63;
+  T.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  T.wp = T.wave & 1;
+  T.wq = T.wave >> 1;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int blk = (slot >> 5) * 8 + xcd, w_in = slot & 31;
+
+  if (MODE != kWgrad) {
+    // cumulative 256-row tile counts and row offsets per expert: one wave, 64 per pass
+    if (tid < 64) {
+      int carry = 0;
+      for (int base = 0; base < g.E; base += 64) {
+        const int i = base + tid;
+        const int o0 = i < g.E ? g.offsets[i] : 0, o1 = i < g.E ? g.offsets[i + 1] : 0;
+        int v = i < g.E ? (o1 - o0 + kTQ - 1) / kTQ : 0;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const int u = __shfl_up(v, d);
+          if (tid >= d) v += u;
+        }
+        if (i < g.E) {
+          g_cum[i + 1] = carry + v;
+          g_off[i + 1] = o1;
+        }
+        carry += __shfl(v, 63);
+      }
+      if (tid == 0) {
+        g_cum[0] = 0;
+        g_off[0] = g.offsets[0];
+      }
+    }
+    __syncthreads();
+  }
+  TileInfo t;
+  if (!decode_tile<MODE>(g, blk, w_in, t)) return;
+  setup_tile<MODE>(T, g, t);
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) T.acc[a][b][v] = 0.0f;
+  const int nk = T.nk;
+  if (nk > 0) {
+    dma_first_stage<MODE>(T);
+    dma_second_stage<MODE>(T);
+    // stage 0 and scale batch 0 have landed when at most the stage-1 DMAs are in flight
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    static_assert(kStage1Dma == 16, "the wait count above is the stage-1 DMA count");
+    __builtin_amdgcn_s_barrier();
+    T.template read_all_from<0, 0, true, 0>();
+    {
+      u32x4 raw[4];
+      T.template read_scale_rows<false>(0, raw);
+      T.template pack_scales<false>(raw, T.cp);
+      T.template read_scale_rows<true>(0, raw);
+      T.template pack_scales<true>(raw, T.cq);
+    }
+    for (int ks = 0; ks < nk; ks += 4) {
+      T.template stage<0>(ks);
+      if (ks + 1 < nk) T.template stage<1>(ks + 1);
+      if (ks + 2 < nk) T.template stage<2>(ks + 2);
+      if (ks + 3 < nk) T.template stage<3>(ks + 3);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs have landed
+  }
+  if (MODE == kWgrad && nk == 0 && g.accumulate) return;
+  __syncthreads();  // every wave is done with the stage buffers (and, per wave, its DMA)
+  epilogue<MODE>(T, g, t);
 }
 
 // Workgroups for n_qg q-tiles x n_pt p-tiles in XCD blocks of kBQ x kBP (whole rounds of
