@@ -1,0 +1,210 @@
+"""Parity at full size: the DeepSeek-V3 expert-parallel share (T16384 H7168 E32 k8 I2048)
+and the Zipf-skewed layer (T8192, same widths), in the launch configuration bench.py
+times.  One whole forward+backward step runs on the GPU; sampled outputs of every stage
+are then checked against the oracle, element by element, each computed from the GPU's
+own upstream tensors (so no error compounds across stages) (GPU)."""
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import codec, quant, sat, moe
+from paper_2511_02302_amd.layer import ExpertLayerFP8
+
+from test_gpu_kernels import f64, host, rel_frob
+from test_gpu_moe import GEMM_TOL, _swiglu_bounds, _swiglu_check
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = {"dsv3": workloads.DSV3, "skew": workloads.SKEW}
+N_GEMM = 256  # sampled elements per GEMM output
+
+
+def _cuda_idx(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int64)).cuda()
+
+
+def _rows(t, idx):
+    """Rows idx of a device tensor, on the host."""
+    return host(t.index_select(0, _cuda_idx(idx)))
+
+
+@pytest.fixture(scope="module", params=list(SHAPES))
+def run(request):
+    shape = SHAPES[request.param]
+    print(f"\nfull-size layer step: {shape.name}", flush=True)
+    d = workloads.layer_inputs(shape, seed=0, device="cuda")
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
+    L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
+    torch.cuda.synchronize()
+    _, off, row_map, src_row = moe.route(host(d["topk_idx"]), shape.E)
+    yield {"shape": shape, "d": d, "b": L.buf, "off": off.astype(np.int64), "row_map": row_map,
+           "src_row": src_row, "rng": np.random.default_rng(zlib.crc32(request.param.encode()))}
+    del L, d
+    torch.cuda.empty_cache()
+
+
+def _sample_rows(r, n):
+    """n distinct routed rows (padding excluded), sorted, and the expert of each."""
+    real = np.nonzero(r["src_row"] >= 0)[0]
+    m = np.sort(r["rng"].choice(real, size=min(n, real.size), replace=False))
+    return m, np.searchsorted(r["off"], m, side="right") - 1
+
+
+def test_routing_full(run):
+    b = run["b"]
+    m_pad = int(run["off"][-1])
+    assert np.array_equal(host(b["offsets"]).astype(np.int64), run["off"])
+    assert np.array_equal(host(b["row_map"]), run["row_map"])
+    assert np.array_equal(host(b["src_row"])[:m_pad], run["src_row"])
+
+
+def test_weight_quant_sampled_blocks(run):
+    d, b, rng = run["d"], run["b"], run["rng"]
+    for wn in ("w1", "w2"):
+        E, R, C = d[wn].shape
+        for _ in range(8):
+            e, rb, cb = int(rng.integers(E)), int(rng.integers(R // 128)), int(rng.integers(C // 128))
+            sl = (e, slice(rb * 128, (rb + 1) * 128), slice(cb * 128, (cb + 1) * 128))
+            wq, ws = quant.quant_block128(f64(d[wn][sl]))
+            assert np.array_equal(host(b[wn + "q"][sl]), wq), (wn, e, rb, cb)
+            assert host(b[wn + "s"][e, rb, cb]) == ws[0, 0], (wn, e, rb, cb)
+
+
+def test_permute_quant_sampled_rows(run):
+    """F1 (plain) and B1 (routing-weighted) rows: bytes and scales bit-exact."""
+    shape, d, b = run["shape"], run["d"], run["b"]
+    m, _ = _sample_rows(run, 128)
+    src = run["src_row"][m]
+    t, j = src // shape.k, src % shape.k
+    local = np.arange(m.size) * shape.k + j  # sampled row i reads local token i
+    probs = _rows(d["probs"], t)
+    for src_t, qn, sn, w in (("x", "xq", "xs", None), ("dy", "dyq", "dys", probs)):
+        wq, ws = moe.permute_quant_rows(f64(d[src_t].index_select(0, _cuda_idx(t))), local, shape.k, row_w=w)
+        assert np.array_equal(_rows(b[qn], m), wq), qn
+        assert np.array_equal(_rows(b[sn], m), ws), sn
+
+
+def _check_gemm_samples(got, want, terms_abs, bf16_out):
+    """Per-element bound: the float32 accumulation of exact e4m3 products (scales are
+    powers of two) errs by at most about K/64 + 6 roundings of the sum of |terms|, with
+    K/64 <= 112 here, so 2^-14 of that sum leaves an 8x margin; a bf16 output adds half
+    an ulp, at most 2^-8 relative.  (A relative Frobenius check of a few hundred bf16
+    samples is not used: bf16 rounding alone puts it near 1.6e-3, at times above 2e-3.)"""
+    got, want = np.asarray(got, dtype=np.float64), np.asarray(want, dtype=np.float64)
+    bound = terms_abs * 2.0 ** -14 + (np.abs(want) * 2.0 ** -8 if bf16_out else 0.0) + 1e-30
+    bad = np.abs(got - want) > bound
+    assert not bad.any(), (np.nonzero(bad)[0][:4], got[bad][:4], want[bad][:4], bound[bad][:4])
+    if not bf16_out:
+        assert rel_frob(got, want) < GEMM_TOL
+
+
+def _dequant_weight(q, s):
+    """Dequantize block-scaled weight rows or columns: q [..., n], s [..., n / 128] (float64)."""
+    return codec.e4m3_decode(q) * np.repeat(s.astype(np.float64), 128, axis=-1)
+
+
+def _fprop_samples(run, qa, sa, wn, out):
+    """out[m, n] = sum_k A[m, k] W_e[n, k] at sampled (m, n)."""
+    b, rng = run["b"], run["rng"]
+    m, e = _sample_rows(run, N_GEMM)
+    n = rng.integers(b[out].shape[1], size=m.size)
+    a = quant.dequant_rowwise(_rows(b[qa], m), _rows(b[sa], m))
+    got = host(b[out][_cuda_idx(m), _cuda_idx(n)].float())
+    wq = host(b[wn + "q"][_cuda_idx(e), _cuda_idx(n)])           # [samples, K]
+    ws = host(b[wn + "s"][_cuda_idx(e), _cuda_idx(n // 128)])    # [samples, K / 128]
+    w = _dequant_weight(wq, ws)
+    _check_gemm_samples(got, np.sum(a * w, axis=1), np.sum(np.abs(a * w), axis=1), bf16_out=True)
+
+
+def test_fc1_fc2_fprop_sampled(run):
+    _fprop_samples(run, "xq", "xs", "w1", "a")
+    _fprop_samples(run, "hq", "hs", "w2", "y_perm")
+
+
+def _dgrad_samples(run, qg, sg, wn, out):
+    """out[m, c] = sum_n G[m, n] W_e[n, c] at sampled (m, c): column c of the weight."""
+    b, rng = run["b"], run["rng"]
+    m, e = _sample_rows(run, N_GEMM)
+    c = rng.integers(b[out].shape[1], size=m.size)
+    g = quant.dequant_rowwise(_rows(b[qg], m), _rows(b[sg], m))
+    got = host(b[out][_cuda_idx(m), _cuda_idx(c)].float())
+    wq = host(b[wn + "q"][_cuda_idx(e), :, _cuda_idx(c)])          # [samples, N]
+    ws = host(b[wn + "s"][_cuda_idx(e), :, _cuda_idx(c // 128)])   # [samples, N / 128]
+    w = _dequant_weight(wq, ws)
+    _check_gemm_samples(got, np.sum(g * w, axis=1), np.sum(np.abs(g * w), axis=1), bf16_out=True)
+
+
+def test_fc2_fc1_dgrad_sampled(run):
+    _dgrad_samples(run, "dyq", "dys", "w2", "dh")
+    _dgrad_samples(run, "daq", "das", "w1", "dx_perm")
+
+
+def _wgrad_samples(run, gT, xT, out):
+    """dW[e, n, c] = sum over expert e's rows m of GT[n, m] XT[c, m] (column-wise operands
+    from the scaling-aware transpose) on a few busy experts; zeros for experts without rows."""
+    b, off, rng = run["b"], run["off"], run["rng"]
+    E, N, K = b[out].shape
+    busy = np.nonzero(off[1:] > off[:-1])[0]
+    for e in sorted(rng.choice(busy, size=min(4, busy.size), replace=False)):
+        lo, hi = int(off[e]), int(off[e + 1])
+        n = rng.integers(N, size=N_GEMM // 4)
+        c = rng.integers(K, size=N_GEMM // 4)
+        got = host(b[out][int(e)][_cuda_idx(n), _cuda_idx(c)])
+        g = quant.dequant_rowwise(host(b[gT + "q"][_cuda_idx(n), lo:hi]),
+                                  host(b[gT + "s"][_cuda_idx(n), lo // 128:hi // 128]))
+        x = quant.dequant_rowwise(host(b[xT + "q"][_cuda_idx(c), lo:hi]),
+                                  host(b[xT + "s"][_cuda_idx(c), lo // 128:hi // 128]))
+        _check_gemm_samples(got, np.sum(g * x, axis=1), np.sum(np.abs(g * x), axis=1), bf16_out=False)
+    for e in np.nonzero(off[1:] == off[:-1])[0]:
+        assert not bool(b[out][int(e)].any()), f"expert {e} has no rows but a nonzero gradient"
+
+
+def test_fc2_fc1_wgrad_sampled(run):
+    _wgrad_samples(run, "dyT", "hT", "dw2")
+    _wgrad_samples(run, "daT", "xT", "dw1")
+
+
+def test_swiglu_fwd_bwd_sampled_rows(run):
+    b = run["b"]
+    m, _ = _sample_rows(run, 48)
+    a64, dh64 = f64(b["a"].index_select(0, _cuda_idx(m))), f64(b["dh"].index_select(0, _cuda_idx(m)))
+    b_fwd, b_bwd = _swiglu_bounds(a64, dh64)
+    h = moe.swiglu(a64)
+    wq, ws = quant.quant_rowwise(h)
+    _swiglu_check(_rows(b["hq"], m), _rows(b["hs"], m), wq, ws, h, b_fwd)
+    da = moe.swiglu_bwd(a64, dh64)
+    wq, ws = quant.quant_rowwise(da)
+    _swiglu_check(_rows(b["daq"], m), _rows(b["das"], m), wq, ws, da, b_bwd)
+
+
+def test_unpermute_sampled_tokens(run):
+    """F5 (routing-weighted) and B5 (plain) at sampled tokens: within one bf16 ulp of the
+    float64 weighted sum of the GPU's own expert outputs."""
+    shape, d, b, rng = run["shape"], run["d"], run["b"], run["rng"]
+    t = np.sort(rng.choice(shape.T, size=64, replace=False))
+    rows = run["row_map"][t]                                 # [64, k], -1 for dropped slots
+    local = np.where(rows >= 0, np.arange(rows.size).reshape(rows.shape), -1)
+    for src, out, w in (("y_perm", "y", _rows(d["probs"], t)), ("dx_perm", "dx", None)):
+        yp = f64(b[src].index_select(0, _cuda_idx(np.maximum(rows, 0).reshape(-1))))
+        want = moe.unpermute(yp, local, w)
+        got = f64(b[out].index_select(0, _cuda_idx(t)))
+        ulp = np.ldexp(1.0, np.frexp(np.maximum(np.abs(want), 1e-30))[1] - 8)
+        assert np.all(np.abs(got - want) <= ulp + 1e-6), (out, np.max(np.abs(got - want) / ulp))
+
+
+def test_sat_sampled_blocks(run):
+    """B6: sampled 128x128 blocks of all four transposed tensors bit-exact, scales included."""
+    b, rng = run["b"], run["rng"]
+    m_pad = int(run["off"][-1])
+    for name in ("x", "h", "dy", "da"):
+        q, s, qT, sT = b[name + "q"], b[name + "s"], b[name + "Tq"], b[name + "Ts"]
+        for _ in range(6):
+            rb, cb = int(rng.integers(m_pad // 128)), int(rng.integers(q.shape[1] // 128))
+            rs, cs = slice(rb * 128, (rb + 1) * 128), slice(cb * 128, (cb + 1) * 128)
+            wqT, wsT = sat.scaling_aware_transpose(host(q[rs, cs]), host(s[rs, cb:cb + 1]))
+            assert np.array_equal(host(qT[cs, rs]), wqT), (name, rb, cb)
+            assert np.array_equal(host(sT[cs, rb:rb + 1]), wsT), (name, rb, cb)
