@@ -18,19 +18,21 @@
 // block), in two half-steps of 64 (16 MFMAs each).
 // Data movement is sized for the L2, whose request rate is the binding limit: every
 // operand row segment of a stage is one whole 128-byte line, loaded by
-// global_load_lds_dwordx4 straight into LDS (8 lanes per line, no register staging);
+// buffer_load_dwordx4 ... lds straight into LDS (8 lanes per line, no register staging);
 // the scales of four K blocks arrive in one batch (four lanes per row line).  Two
 // stage buffers: the DMA of stage s+2 is issued, spread over the MFMAs, during the
 // second half of stage s, once a barrier has shown every wave done with stage s's
 // buffer and stage s+1 landed.  Fragments are double buffered in VGPRs (one set per
 // half-step), and LDS reads are threaded one or two per MFMA.
-// K-major tiles (128-byte rows) use the 16-byte XOR swizzle chunk ^ ((r ^ r>>3) & 7),
+// K-major tiles (128-byte rows) use the 16-byte XOR swizzle chunk ^ ((r >> 1) & 7),
 // conflict-free for the fragment reads.  dgrad reads W_e in its stored [n][k]
 // orientation (256-byte rows) with ds_read_b64_tr_b8, which transposes 8x8 byte
 // blocks across lanes; its rows use the swizzle chunk ^ ((2j ^ j>>2) & 15), j = n%8.
 //
-// Grouped scheduling is on the device: tiles are counted per expert from offsets
-// (no host sync); surplus workgroups of the host-sized grid exit at once.
+// Grouped scheduling is on the device: tiles are counted per expert from offsets (no
+// host sync).  The kernel is persistent, one workgroup per CU walking its XCD's tiles, so
+// that a tile's epilogue (output staged through one stage buffer, streaming stores)
+// overlaps the next tile's first-stage DMA into the other.
 
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
@@ -89,8 +91,11 @@ struct GemmArgs {
   int accumulate;
 };
 
-// K-major stage tile: 256 rows x 128 bytes, 16-byte chunk c of row r at c ^ kswz(r).
-__device__ __forceinline__ int kswz(int r) { return (r ^ (r >> 3)) & 7; }
+// K-major stage tile: 256 rows x 128 bytes, 16-byte chunk c of row r at c ^ kswz(r).  Any
+// 16 consecutive rows take the 16 distinct (r % 2, chunk) slots of a 256-byte bank window,
+// and the swizzle repeats every 16 rows, so fragment rows 32 apart share one address
+// register (plus an immediate offset).
+__device__ __forceinline__ int kswz(int r) { return (r >> 1) & 7; }
 // dgrad weight stage tile: 128 rows (n) x 256 bytes, chunk c of row n at c ^ wswz(n % 8).
 __device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
 
@@ -134,6 +139,15 @@ __device__ __forceinline__ i32x8 with_half(i32x8 f, const u32x4& x, int half) {
   f[4 * half + 2] = (int)x[2];
   f[4 * half + 3] = (int)x[3];
   return f;
+}
+
+// Lane index as an opaque value: lane-dependent tile setup and epilogue arithmetic built
+// on it is recomputed per tile instead of being hoisted out of the tile loop, where it
+// would stay live (in registers) through the main loop.
+__device__ __forceinline__ int opaque_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
 }
 
 // Per-thread state of one workgroup tile.
@@ -253,29 +267,35 @@ struct Tile {
   // Scales of batch b (LDS buffer b % 2, rows of four K-block floats): read the rows of
   // one operand this lane multiplies into raw (kQ, or wgrad P: rows 128 w + 32 R + l for
   // R = 0..3; fprop / dgrad P: the wave's one weight-block row, raw[0] only) ...
-  template <bool kQ>
+  // Rows R0..R1-1 only (read and packed a few at a time, to keep few raw rows live).
+  template <bool kQ, int R0, int R1>
   __device__ __forceinline__ void read_scale_rows(int b, u32x4 (&raw)[4]) {
     const u32x4* S = reinterpret_cast<const u32x4*>(&g_sc[b & 1][0]);
-    const int l31 = lane & 31;
+    const int l31 = opaque_lane() & 31;  // recomputed here rather than held through the tile
     if constexpr (!kQ && kBlockP) {
-      raw[0] = S[wp];
+      if constexpr (R0 == 0) raw[0] = S[wp];
     } else {
 #pragma unroll
-      for (int R = 0; R < 4; ++R) raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : S[128 * wp + 32 * R + l31];
+      for (int R = R0; R < R1; ++R) raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : S[128 * wp + 32 * R + l31];
     }
   }
   // ... and pack them: word j holds the E8M0 byte (the fp32 exponent field of a
-  // positive power of two) of row R in byte R.
-  template <bool kQ>
+  // positive power of two) of row R in byte R (rows R0..R1-1 added to the word).
+  template <bool kQ, int R0, int R1>
   __device__ __forceinline__ static void pack_scales(const u32x4 (&raw)[4], uint32_t (&dst)[4]) {
     if constexpr (!kQ && kBlockP) {
+      if constexpr (R0 == 0) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) dst[j] = (raw[0][j] >> 23) * 0x01010101u;
+        for (int j = 0; j < 4; ++j) dst[j] = (raw[0][j] >> 23) * 0x01010101u;
+      }
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        dst[j] = (raw[0][j] >> 23) | ((raw[1][j] >> 15) & 0xff00u) | ((raw[2][j] >> 7) & 0xff0000u) |
-                 ((raw[3][j] << 1) & 0xff000000u);
+      for (int j = 0; j < 4; ++j) {
+        uint32_t v = (R0 == 0) ? 0u : dst[j];
+#pragma unroll
+        for (int R = R0; R < R1; ++R) v |= ((raw[R][j] >> 23) & 0xffu) << (8 * R);
+        dst[j] = v;
+      }
     }
   }
 
@@ -336,10 +356,14 @@ struct Tile {
       mfma_op<false, S4, I>();
       dma_slot<B, S4, I, 0>(ks_dma, ks_next);
       reads_of_slot<1 - B, 0, true, I>();
-      if constexpr (S4 == 3 && I == 8) read_scale_rows<false>(ks_next >> 2, rsp);
-      if constexpr (S4 == 3 && I == 9) read_scale_rows<true>(ks_next >> 2, rsq);
-      if constexpr (S4 == 3 && I == 12) pack_scales<false>(rsp, np);
-      if constexpr (S4 == 3 && I == 14) pack_scales<true>(rsq, nq);
+      if constexpr (S4 == 3 && I == 8) read_scale_rows<false, 0, 2>(ks_next >> 2, rsp);
+      if constexpr (S4 == 3 && I == 9) read_scale_rows<true, 0, 2>(ks_next >> 2, rsq);
+      if constexpr (S4 == 3 && I == 10) pack_scales<false, 0, 2>(rsp, np);
+      if constexpr (S4 == 3 && I == 11) read_scale_rows<false, 2, 4>(ks_next >> 2, rsp);
+      if constexpr (S4 == 3 && I == 11) pack_scales<true, 0, 2>(rsq, nq);
+      if constexpr (S4 == 3 && I == 12) read_scale_rows<true, 2, 4>(ks_next >> 2, rsq);
+      if constexpr (S4 == 3 && I == 13) pack_scales<false, 2, 4>(rsp, np);
+      if constexpr (S4 == 3 && I == 14) pack_scales<true, 2, 4>(rsq, nq);
       __builtin_amdgcn_sched_barrier(0);
       half1_from<B, S4, I + 1>(ks_dma, ks_next);
     }
@@ -395,8 +419,8 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in
     }
     const int e = __builtin_amdgcn_readfirstlane(lo);
     t.e = e;
-    t.q0 = g_off[e] + (int64_t)(qg - g_cum[e]) * kTQ;
-    t.q_end = g_off[e + 1];
+    t.q0 = __builtin_amdgcn_readfirstlane(g_off[e] + (qg - g_cum[e]) * kTQ);  // uniform (LDS values)
+    t.q_end = __builtin_amdgcn_readfirstlane(g_off[e + 1]);
     t.k0 = 0;
     t.nk = g.Kdim / kBK;
   } else {
@@ -414,84 +438,84 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in
 }
 
 // DMA sources of tile t: wave-uniform bases and resources, per-lane offsets (lane l of
-// tile DMA instruction i writes LDS bytes 16 l .. of that instruction's 1 KB).
+// tile DMA instruction i writes LDS bytes 16 l .. of that instruction's 1 KB).  Offsets are
+// 32-bit (the host keeps every operand under 4 GiB); past an operand's end they may wrap,
+// which only feeds rows or columns that are never stored.
 template <int MODE>
 __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, const TileInfo& t) {
-  const int lane = T.lane, wave = T.wave, e = t.e;
-  const int64_t q0 = t.q0, k0 = t.k0, p0 = t.p0;
+  const uint32_t lane = (uint32_t)opaque_lane(), wave = (uint32_t)T.wave, e = (uint32_t)t.e;
+  const uint32_t q0 = (uint32_t)t.q0, k0 = (uint32_t)t.k0, p0 = (uint32_t)t.p0;
+  const uint32_t Np = (uint32_t)g.Np, Kdim = (uint32_t)g.Kdim, M_cap = (uint32_t)g.M_cap;
   T.nk = t.nk;
-  const int64_t q_ld = (MODE == kWgrad) ? g.M_cap : g.Kdim;
-  const int64_t q_rows = (MODE == kWgrad) ? g.Nq : g.M_cap;
+  const uint32_t q_ld = (MODE == kWgrad) ? M_cap : Kdim;
+  const uint32_t q_rows = (MODE == kWgrad) ? (uint32_t)g.Nq : M_cap;
   // K-major row of pattern h (h = 0, 1) for this lane: group w + 4h, row 8 group + l / 8,
-  // 16-byte chunk (l % 8) ^ kswz(row) (kswz depends on row % 8 and group % 8 only).
-  T.q_rsrc = make_rsrc(g.Q, (uint32_t)(q_rows * q_ld));
+  // 16-byte chunk (l % 8) ^ kswz(row) (kswz depends on the group's parity and l / 16 only).
+  T.q_rsrc = make_rsrc(g.Q, q_rows * q_ld);
   T.q_kstep = kBK;
   T.q_istep = (int)(64 * q_ld);
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int r = 8 * (wave + 4 * hh) + (lane >> 3);
-    const int c = (lane & 7) ^ kswz(r);
-    T.q_voff[hh] = (uint32_t)((q0 + r) * q_ld + k0 + c * 16);
+  for (uint32_t hh = 0; hh < 2; ++hh) {
+    const uint32_t r = 8 * (wave + 4 * hh) + (lane >> 3);
+    const uint32_t c = (lane & 7) ^ (uint32_t)kswz((int)r);
+    T.q_voff[hh] = (q0 + r) * q_ld + k0 + c * 16;
   }
   if (MODE == kDgrad) {  // W_e [N = Kdim][K = Np], rows n = 32w + 4i + l / 16
-    T.p_rsrc = make_rsrc(g.P, (uint32_t)((int64_t)g.E * g.Kdim * g.Np));
-    T.p_kstep = kBK * g.Np;
-    T.p_istep = 8 * g.Np;
+    T.p_rsrc = make_rsrc(g.P, (uint32_t)g.E * Kdim * Np);
+    T.p_kstep = kBK * Np;
+    T.p_istep = 8 * Np;
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int n = 32 * wave + 4 * hh + (lane >> 4);
-      const int c = (lane & 15) ^ wswz(n & 7);
-      T.p_voff[hh] = (uint32_t)(((int64_t)e * g.Kdim + n) * g.Np + p0 + c * 16);
+    for (uint32_t hh = 0; hh < 2; ++hh) {
+      const uint32_t n = 32 * wave + 4 * hh + (lane >> 4);
+      const uint32_t c = (lane & 15) ^ (uint32_t)wswz((int)(n & 7));
+      T.p_voff[hh] = (e * Kdim + n) * Np + p0 + c * 16;
     }
   } else {
-    const int64_t p_ld = (MODE == kWgrad) ? g.M_cap : g.Kdim;
-    const int64_t p_rows = (MODE == kWgrad) ? g.Np : (int64_t)g.E * g.Np;  // fprop: all experts' rows
-    const int64_t p_row0 = (MODE == kFprop) ? (int64_t)e * g.Np + p0 : p0;
-    T.p_rsrc = make_rsrc(g.P, (uint32_t)(p_rows * p_ld));
+    const uint32_t p_ld = (MODE == kWgrad) ? M_cap : Kdim;
+    const uint32_t p_rows = (MODE == kWgrad) ? Np : (uint32_t)g.E * Np;  // fprop: all experts' rows
+    const uint32_t p_row0 = (MODE == kFprop) ? e * Np + p0 : p0;
+    T.p_rsrc = make_rsrc(g.P, p_rows * p_ld);
     T.p_kstep = kBK;
     T.p_istep = (int)(64 * p_ld);
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int r = 8 * (wave + 4 * hh) + (lane >> 3);
-      const int c = (lane & 7) ^ kswz(r);
-      T.p_voff[hh] = (uint32_t)((p_row0 + r) * p_ld + k0 + c * 16);
+    for (uint32_t hh = 0; hh < 2; ++hh) {
+      const uint32_t r = 8 * (wave + 4 * hh) + (lane >> 3);
+      const uint32_t c = (lane & 7) ^ (uint32_t)kswz((int)r);
+      T.p_voff[hh] = (p_row0 + r) * p_ld + k0 + c * 16;
     }
   }
   // scale DMA sources (resources range-checked to the end of each scale tensor)
-  const int64_t q_sld = (MODE == kWgrad) ? g.M_cap / kTile : g.Kdim / kTile;  // floats per Q scale row
+  const uint32_t q_sld = q_ld / kTile;  // floats per Q scale row
   const float* sq_base = g.sQ + k0 / kTile;
   const float* sp_base;
-  const int64_t sq_total = q_rows * q_sld - ((MODE == kWgrad) ? k0 / kTile : 0);
-  int64_t sp_total;
+  const uint32_t sq_total = q_rows * q_sld - ((MODE == kWgrad) ? k0 / kTile : 0);
+  uint32_t sp_total;
   if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
-    sp_base = g.sP + (int64_t)e * (g.Np / kTile) * (g.Kdim / kTile);
+    sp_base = g.sP + (size_t)e * (Np / kTile) * (Kdim / kTile);
     T.sp_kb = 1;
-    sp_total = (int64_t)(g.E - e) * (g.Np / kTile) * (g.Kdim / kTile);
+    sp_total = ((uint32_t)g.E - e) * (Np / kTile) * (Kdim / kTile);
   } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]
-    sp_base = g.sP + (int64_t)e * (g.Kdim / kTile) * (g.Np / kTile);
-    T.sp_kb = (int)(g.Np / kTile);
-    sp_total = (int64_t)(g.E - e) * (g.Kdim / kTile) * (g.Np / kTile);
+    sp_base = g.sP + (size_t)e * (Kdim / kTile) * (Np / kTile);
+    T.sp_kb = (int)(Np / kTile);
+    sp_total = ((uint32_t)g.E - e) * (Kdim / kTile) * (Np / kTile);
   } else {  // xT_s [Np][M_cap/128]
     sp_base = g.sP + k0 / kTile;
     T.sp_kb = 1;
-    sp_total = g.Np * (g.M_cap / kTile) - k0 / kTile;
+    sp_total = Np * (M_cap / kTile) - k0 / kTile;
   }
-  const int r = 64 * wave + lane;  // tile row of this lane's Q (and wgrad P) scales
-  int64_t q = q0 + r;
-  q = q < q_rows ? q : q_rows - 1;
-  T.sq_off = (uint32_t)(q * q_sld * 4);
+  const uint32_t r = 64 * wave + lane;  // tile row of this lane's Q (and wgrad P) scales
+  const uint32_t q = min(q0 + r, q_rows - 1);
+  T.sq_off = q * q_sld * 4;
   if (MODE == kWgrad) {
-    int64_t p = p0 + r;
-    p = p < g.Np ? p : g.Np - 1;
-    T.sp_off = (uint32_t)(p * (g.M_cap / kTile) * 4);
+    const uint32_t pr = min(p0 + r, Np - 1);
+    T.sp_off = pr * (M_cap / kTile) * 4;
   } else {
-    int64_t pb = p0 / kTile + ((lane >> 2) & 1);  // the tile's two weight block rows
-    pb = pb < g.Np / kTile ? pb : g.Np / kTile - 1;
-    const int j = lane & 3;
-    T.sp_off = (uint32_t)(((MODE == kFprop) ? pb * (g.Kdim / kTile) + j : j * (g.Np / kTile) + pb) * 4);
+    const uint32_t pb = min(p0 / kTile + ((lane >> 2) & 1), Np / kTile - 1);  // the tile's two weight block rows
+    const uint32_t j = lane & 3;
+    T.sp_off = ((MODE == kFprop) ? pb * (Kdim / kTile) + j : j * (Np / kTile) + pb) * 4;
   }
-  T.sp_rsrc = make_rsrc(sp_base, (uint32_t)(sp_total * 4));
-  T.sq_rsrc = make_rsrc(sq_base, (uint32_t)(sq_total * 4));
+  T.sp_rsrc = make_rsrc(sp_base, sp_total * 4);
+  T.sq_rsrc = make_rsrc(sq_base, sq_total * 4);
   // Blocks start their K loops at different scale-batch-aligned stages, so that the XCDs
   // running together stream different K bands of the operand rows (spread over memory
   // channels) while the 32 tiles of one block still share every stage through their L2.
@@ -500,77 +524,97 @@ __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, con
                 : 0;
 }
 
-// Output of one tile through the LDS stage buffers (32 KB per wave).  Every global store instruction
+// Output of one tile through stage buffer 1 only (16 KB per wave), so that the next
+// tile's first stage can stream into buffer 0 meanwhile.  Every global store instruction
 // writes whole 128-byte lines (16 lanes per 256-byte bf16 row, 32 lanes per 512-byte fp32
-// row) instead of 16-byte pieces of 32 rows: each wave stages 128 (bf16) or 64 (fp32) rows
+// row) instead of 16-byte pieces of 32 rows: each wave stages 64 (bf16) or 32 (fp32) rows
 // of its 128 x 128 sub-tile at a time ([q][p], p contiguous), 16-byte chunks of row q
 // XOR-swizzled by q, conflict-free for the fragment-order writes and the row-order reads.
 // The stores are non-temporal: the output is not re-read here, and streaming it keeps the
 // operand panels that the XCD's other workgroups are still reading in L2.  A wave only
-// rewrites its own region, after its own reads (LDS order), so rounds need no barrier.
+// rewrites its own region, after its own reads (LDS order), so passes need no barrier.
 template <int MODE>
 __device__ __forceinline__ void epilogue(Tile<MODE>& T, const GemmArgs& g, const TileInfo& t) {
-  const int lane = T.lane, wave = T.wave, wp = T.wp, wq = T.wq;
-  lds_u8* const region = (lds_u8*)((wave < 2) ? g_st0 : g_st1) + (wave & 1) * 32768;
+  const int lane = opaque_lane(), wave = T.wave, wp = T.wp, wq = T.wq;
+  lds_u8* const region = (lds_u8*)g_st1 + wave * 16384;
   const int l31 = lane & 31, h = lane >> 5;
   const bool p_ok = t.p0 + 128 * wp < g.Np;  // Np is a multiple of 128: whole-wave predicate
   if (MODE == kWgrad) {
-    float* dw = static_cast<float*>(g.out) + (int64_t)t.e * g.Nq * g.Np + t.p0 + 128 * wp;
+    // uniform base of this wave's 128 x 128 sub-tile, 32-bit lane offsets from it
+    uint8_t* const dw = reinterpret_cast<uint8_t*>(
+        static_cast<float*>(g.out) + ((size_t)t.e * g.Nq + t.q0 + 128 * wq) * g.Np + t.p0 + 128 * wp);
 #pragma unroll
-    for (int bh = 0; bh < 2; ++bh) {
-      // rows ql = 32 (b - 2 bh) + l31 of 512 bytes; chunk c = p / 4 = 8a + 2gr + h
+    for (int b = 0; b < 4; ++b) {
+      // rows ql = l31 of 512 bytes (q = 32 b + ql); chunk c = p / 4 = 8a + 2gr + h
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+          const int c = 8 * a + 2 * gr + h;
+          u32x4 o;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(T.acc[a][b][4 * gr + j]);
+          *(__attribute__((address_space(3))) u32x4*)(region + l31 * 512 + ((c ^ l31) << 4)) = o;
+          __builtin_amdgcn_sched_barrier(0);  // few accumulators in VGPRs at a time
+        }
+      // all of the pass's row reads first, then the stores (one LDS wait, not one per store)
+      u32x4 v[16];
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int ql = 2 * it + h;
+        v[it] = *(__attribute__((address_space(3))) u32x4*)(region + ql * 512 + ((l31 ^ ql) << 4));
+      }
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int qr = 32 * b + 2 * it + h;  // row within the wave's sub-tile
+        if (!p_ok || t.q0 + 128 * wq + qr >= t.q_end) continue;
+        uint8_t* dst = dw + (uint32_t)(qr * g.Np + 4 * l31) * 4u;
+        if (g.accumulate) {
+          const u32x4 old = ld16(dst);
+          u32x4 o;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(__uint_as_float(old[j]) + __uint_as_float(v[it][j]));
+          stnt16(dst, o);
+        } else {
+          stnt16(dst, v[it]);
+        }
+      }
+    }
+  } else {
+    // uniform base of this wave's 128 x 128 sub-tile, 32-bit lane offsets from it
+    uint8_t* const out = reinterpret_cast<uint8_t*>(static_cast<uint16_t*>(g.out) + (size_t)(t.q0 + 128 * wq) * g.Np +
+                                                    t.p0 + 128 * wp);
+#pragma unroll
+    for (int ph = 0; ph < 2; ++ph) {
+      // rows ql = 32bb + l31 of 256 bytes (q = 64 ph + ql); 8-byte piece (p = 32a + 8gr + 4h)
+      // in chunk 4a + gr, half h
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
           for (int gr = 0; gr < 4; ++gr) {
-            const int ql = 32 * bb + l31, c = 8 * a + 2 * gr + h;
-            u32x4 o;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(T.acc[a][2 * bh + bb][4 * gr + j]);
-            *(__attribute__((address_space(3))) u32x4*)(region + ql * 512 + ((c ^ (ql & 31)) << 4)) = o;
+            const int ql = 32 * bb + l31, m = 4 * a + gr;
+            u32x2 o;
+            o[0] = pack_bf16x2(T.acc[a][2 * ph + bb][4 * gr + 0], T.acc[a][2 * ph + bb][4 * gr + 1]);
+            o[1] = pack_bf16x2(T.acc[a][2 * ph + bb][4 * gr + 2], T.acc[a][2 * ph + bb][4 * gr + 3]);
+            *(__attribute__((address_space(3))) u32x2*)(region + ql * 256 + ((m ^ (ql & 15)) << 4) + 8 * h) = o;
+            __builtin_amdgcn_sched_barrier(0);  // few accumulators in VGPRs at a time
           }
-#pragma unroll 4
-      for (int it = 0; it < 32; ++it) {
-        const int ql = 2 * it + h, c = l31;
-        const u32x4 v = *(__attribute__((address_space(3))) u32x4*)(region + ql * 512 + ((c ^ (ql & 31)) << 4));
-        const int64_t q = t.q0 + 128 * wq + 64 * bh + ql;
-        if (!p_ok || q >= t.q_end) continue;
-        float* dst = dw + q * g.Np + 4 * c;
-        if (g.accumulate) {
-          const u32x4 old = ld16(dst);
-          u32x4 o;
+      // all of the pass's row reads first, then the stores (one LDS wait, not one per store)
+      const int c = lane & 15;
+      u32x4 v[16];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) o[j] = __float_as_uint(__uint_as_float(old[j]) + __uint_as_float(v[j]));
-          stnt16(dst, o);
-        } else {
-          stnt16(dst, v);
-        }
+      for (int it = 0; it < 16; ++it) {
+        const int ql = 4 * it + (lane >> 4);
+        v[it] = *(__attribute__((address_space(3))) u32x4*)(region + ql * 256 + ((c ^ (ql & 15)) << 4));
       }
-    }
-  } else {
-    uint16_t* out = static_cast<uint16_t*>(g.out) + t.p0 + 128 * wp;
-    // rows q = 32b + l31 of 256 bytes; 8-byte piece (p = 32a + 8gr + 4h) in chunk 4a + gr, half h
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int gr = 0; gr < 4; ++gr) {
-          const int ql = 32 * b + l31, m = 4 * a + gr;
-          u32x2 o;
-          o[0] = pack_bf16x2(T.acc[a][b][4 * gr + 0], T.acc[a][b][4 * gr + 1]);
-          o[1] = pack_bf16x2(T.acc[a][b][4 * gr + 2], T.acc[a][b][4 * gr + 3]);
-          *(__attribute__((address_space(3))) u32x2*)(region + ql * 256 + ((m ^ (ql & 15)) << 4) + 8 * h) = o;
-        }
-#pragma unroll 4
-    for (int it = 0; it < 32; ++it) {
-      const int ql = 4 * it + (lane >> 4), c = lane & 15;
-      const u32x4 v = *(__attribute__((address_space(3))) u32x4*)(region + ql * 256 + ((c ^ (ql & 15)) << 4));
-      const int64_t q = t.q0 + 128 * wq + ql;
-      if (!p_ok || q >= t.q_end) continue;
-      stnt16(out + q * g.Np + 8 * c, v);
+      for (int it = 0; it < 16; ++it) {
+        const int qr = 64 * ph + 4 * it + (lane >> 4);  // row within the wave's sub-tile
+        if (!p_ok || t.q0 + 128 * wq + qr >= t.q_end) continue;
+        stnt16(out + (uint32_t)(qr * g.Np + 8 * c) * 2u, v[it]);
+      }
     }
   }
 }
@@ -601,13 +645,37 @@ __device__ __forceinline__ void dma_second_stage(Tile<MODE>& T) {
   T.template dma_tile<1, 15>(s1);
 }
 
-// One 256 x 256 tile per workgroup.  Workgroups are dispatched round-robin over the 8
-// XCDs (32 CUs each); the 32 consecutive workgroups of XCD x (slots s..s+31) take the
-// tiles of one XCD block (kBQ x kBP = 32 tiles: q-tiles x p-tiles, p fastest), so they
-// share 8 q panels and 4 p panels per K step in their L2, and the 8 XCDs together sweep
-// one 16 x 16-tile window (about one expert) at a time.  Surplus workgroups of the
-// host-sized grid exit at once.  All control flow is workgroup-uniform (tile decode from
-// uniform values), so every barrier is reached by all four waves.
+// Persistent: one workgroup per CU, up to kPersistSlots per XCD.  Workgroups are
+// dispatched round-robin over the 8 XCDs.  XCD x owns XCD blocks x, x + 8, x + 16, ...
+// (kBQ x kBP tiles each, p fastest); its work list is their tiles in that order, and its
+// S workgroups take items s, s + S, s + 2S, ...  With S = 32 (256 CUs), slot s takes tile
+// s of every block, so the 32 workgroups of an XCD work on one block at a time and share
+// its 8 q panels and 4 p panels per K step in their L2, while the 8 XCDs together sweep
+// one 16 x 16-tile window (about one expert).
+// Between tiles, the next tile's first stage (and scale batch) streams into stage buffer 0
+// while the finished tile's output is staged through buffer 1 and stored; its second
+// stage follows once the epilogue has left buffer 1.  All control flow is
+// workgroup-uniform (tile decode from uniform values), so every barrier is reached by all
+// four waves, and every wave leaves the tile loop with the same tile count.
+constexpr int kPersistSlots = kBQ * kBP;  // workgroups per XCD
+
+// Workgroup barrier that waits for this wave's LDS accesses only: global stores may stay in
+// flight across it (a __syncthreads fence would drain them).  One asm statement, so that
+// no memory access moves across the barrier.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Next tile of this workgroup from work item k on (k advances past empty edge tiles).
+template <int MODE>
+__device__ __forceinline__ bool next_tile(const GemmArgs& g, int xcd, int slot, int n_slots, int n_blocks, int& k,
+                                          TileInfo& t) {
+  for (;; ++k) {
+    const int i = k * n_slots + slot;
+    const int blk = (i / kPersistSlots) * 8 + xcd;
+    if (blk >= n_blocks) return false;
+    if (decode_tile<MODE>(g, blk, i % kPersistSlots, t)) return true;
+  }
+}
+
 template <int MODE>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   const int tid = threadIdx.x;
@@ -616,9 +684,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   T.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   T.wp = T.wave & 1;
   T.wq = T.wave >> 1;
-  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int blk = (slot >> 5) * 8 + xcd, w_in = slot & 31;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, n_slots = gridDim.x >> 3;
 
+  int n_qg;  // q tiles
   if (MODE != kWgrad) {
     // cumulative 256-row tile counts and row offsets per expert: one wave, 64 per pass
     if (tid < 64) {
@@ -644,51 +712,70 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
       }
     }
     __syncthreads();
+    n_qg = __builtin_amdgcn_readfirstlane(g_cum[g.E]);
+  } else {
+    n_qg = g.E * g.n_qt;
   }
+  const int n_blocks = ((g.n_pt + kBP - 1) / kBP) * ((n_qg + kBQ - 1) / kBQ);
+  int k = 0;
   TileInfo t;
-  if (!decode_tile<MODE>(g, blk, w_in, t)) return;
+  if (!next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k, t)) return;
   setup_tile<MODE>(T, g, t);
+  if (T.nk > 0) dma_first_stage<MODE>(T);
+  // Loop invariant: tile t is set up, its stage 0 and scale batch 0 are in flight (if it
+  // has any K), and stage buffer 1 is free.
+  for (;;) {
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+      for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) T.acc[a][b][v] = 0.0f;
-  const int nk = T.nk;
-  if (nk > 0) {
-    dma_first_stage<MODE>(T);
-    dma_second_stage<MODE>(T);
-    // stage 0 and scale batch 0 have landed when at most the stage-1 DMAs are in flight
-    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    static_assert(kStage1Dma == 16, "the wait count above is the stage-1 DMA count");
-    __builtin_amdgcn_s_barrier();
-    T.template read_all_from<0, 0, true, 0>();
-    {
-      u32x4 raw[4];
-      T.template read_scale_rows<false>(0, raw);
-      T.template pack_scales<false>(raw, T.cp);
-      T.template read_scale_rows<true>(0, raw);
-      T.template pack_scales<true>(raw, T.cq);
+        for (int v = 0; v < 16; ++v) T.acc[a][b][v] = 0.0f;
+    const int nk = T.nk;
+    if (nk > 0) {
+      dma_second_stage<MODE>(T);
+      // stage 0 and scale batch 0 have landed when at most the stage-1 DMAs are in flight
+      // (loads retire in order; older epilogue stores still in flight only make this wait longer)
+      asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
+      static_assert(kStage1Dma == 16, "the wait count above is the stage-1 DMA count");
+      T.template read_all_from<0, 0, true, 0>();
+      {
+        u32x4 raw[4];
+        T.template read_scale_rows<false, 0, 4>(0, raw);
+        T.template pack_scales<false, 0, 4>(raw, T.cp);
+        T.template read_scale_rows<true, 0, 4>(0, raw);
+        T.template pack_scales<true, 0, 4>(raw, T.cq);
+      }
+      for (int ks = 0; ks < nk; ks += 4) {
+        T.template stage<0>(ks);
+        if (ks + 1 < nk) T.template stage<1>(ks + 1);
+        if (ks + 2 < nk) T.template stage<2>(ks + 2);
+        if (ks + 3 < nk) T.template stage<3>(ks + 3);
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs have landed
     }
-    for (int ks = 0; ks < nk; ks += 4) {
-      T.template stage<0>(ks);
-      if (ks + 1 < nk) T.template stage<1>(ks + 1);
-      if (ks + 2 < nk) T.template stage<2>(ks + 2);
-      if (ks + 3 < nk) T.template stage<3>(ks + 3);
+    lds_barrier();  // every wave is done with the stage buffers and the scale batches
+    TileInfo tn;
+    ++k;
+    const bool more = next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k, tn);
+    if (more) {
+      setup_tile<MODE>(T, g, tn);
+      if (T.nk > 0) dma_first_stage<MODE>(T);  // buffer 0 and scale batch 0, under the epilogue
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs have landed
+    if (!(MODE == kWgrad && t.nk == 0 && g.accumulate)) epilogue<MODE>(T, g, t);
+    if (!more) break;
+    t = tn;
+    lds_barrier();  // buffer 1 is free for the next tile's second stage
   }
-  if (MODE == kWgrad && nk == 0 && g.accumulate) return;
-  __syncthreads();  // every wave is done with the stage buffers (and, per wave, its DMA)
-  epilogue<MODE>(T, g, t);
 }
 
-// Workgroups for n_qg q-tiles x n_pt p-tiles in XCD blocks of kBQ x kBP (whole rounds of
-// 8 blocks, one per XCD); tiles past the edges exit at once.
-unsigned grid_blocks(int n_pt, int n_qg) {
-  const int64_t n_pb = (n_pt + kBP - 1) / kBP, n_qb = (n_qg + kBQ - 1) / kBQ;
-  const int64_t rounds = (n_pb * n_qb + 7) / 8;
-  return (unsigned)(rounds * 8 * kBQ * kBP);
+// Persistent grid: one workgroup per CU, the same number on each of the 8 XCDs, at most
+// kPersistSlots per XCD.
+unsigned grid_blocks() {
+  int cus = (device_cu_count() / 8) * 8;
+  if (cus > 8 * kPersistSlots) cus = 8 * kPersistSlots;
+  if (cus < 8) cus = 8;
+  return (unsigned)cus;
 }
 
 }  // namespace
@@ -707,18 +794,18 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
   if (mode == kFprop) {  // out[m, n] = a[m, :] . w[e, n, :]
     g.Np = N; g.Kdim = K;
     g.n_pt = (int)((N + kTP - 1) / kTP);
-    grid = grid_blocks(g.n_pt, (int)((M_cap + kTQ - 1) / kTQ + (E + 1) / 2));
+    grid = grid_blocks();
     grouped_gemm_kernel<kFprop><<<grid, kThreads, 0, st>>>(g);
   } else if (mode == kDgrad) {  // out[m, k] = g[m, :] . w[e, :, k]
     g.Np = K; g.Kdim = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
-    grid = grid_blocks(g.n_pt, (int)((M_cap + kTQ - 1) / kTQ + (E + 1) / 2));
+    grid = grid_blocks();
     grouped_gemm_kernel<kDgrad><<<grid, kThreads, 0, st>>>(g);
   } else {  // dw[e, n, k] = sum_m gT[n, m] xT[k, m]
     g.Np = K; g.Nq = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
     g.n_qt = (int)((N + kTQ - 1) / kTQ);
-    grid = grid_blocks(g.n_pt, E * g.n_qt);
+    grid = grid_blocks();
     grouped_gemm_kernel<kWgrad><<<grid, kThreads, 0, st>>>(g);
   }
   return hipGetLastError();
