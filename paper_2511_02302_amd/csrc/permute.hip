@@ -6,9 +6,9 @@
 // each expert group):
 //   route_count  : one workgroup per chunk of 256 tokens counts its (token, slot)
 //                  pairs per expert in LDS -> counts[chunk][e];
-//   route_scan   : one workgroup turns the counts into per-chunk bases, pads every
-//                  expert to a multiple of 128 rows, writes offsets[E+1] and marks the
-//                  padding rows' src_row = -1;
+//   route_scan   : one workgroup (E x parts threads) turns the counts into per-chunk
+//                  bases, pads every expert to a multiple of 128 rows, writes
+//                  offsets[E+1] and marks the padding rows' src_row = -1;
 //   route_assign : one wave per chunk walks its tokens 64 at a time; a 64-bit LDS
 //                  ballot mask per expert gives each pair its rank among earlier lanes.
 // Then permute_quant reads each token row ONCE (one workgroup per token, 16 elements per
@@ -46,37 +46,55 @@ __global__ __launch_bounds__(kThreads) void route_count_kernel(const int32_t* __
   for (int e = threadIdx.x; e < E; e += kThreads) counts[(int64_t)blockIdx.x * E + e] = cnt[e];
 }
 
+// Thread (e, part) of P = 1024 / E parts owns a contiguous range of chunks of expert e:
+// it sums them, the parts' sums are scanned per expert in LDS, and each thread then
+// rewrites its range as exclusive bases.  All chunk loads of a pass are independent.
 __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ counts, int64_t n_chunks, int E,
                                                           int32_t* __restrict__ offsets, int32_t* __restrict__ src_row) {
-  __shared__ int padded[1024];
+  __shared__ int part_sum[1024];  // [e][part], then exclusive prefix within e
+  __shared__ int totals[1024];
   __shared__ int offs[1025];
-  const int e = threadIdx.x;
-  int total = 0;
-  if (e < E) {
-    for (int64_t c = 0; c < n_chunks; ++c) {  // counts -> exclusive per-chunk prefix (in place)
-      const int v = counts[c * E + e];
-      counts[c * E + e] = total;
-      total += v;
+  const int P = 1024 / E;  // parts per expert (E <= 1024)
+  const int e = threadIdx.x / P, part = threadIdx.x - e * P;
+  const int64_t per = (n_chunks + P - 1) / P;
+  const int64_t c0 = (int64_t)part * per;
+  const int64_t c1 = c0 + per < n_chunks ? c0 + per : n_chunks;
+  int sum = 0;
+  if (e < E)
+    for (int64_t c = c0; c < c1; ++c) sum += counts[c * E + e];
+  part_sum[threadIdx.x] = sum;
+  __syncthreads();
+  if (threadIdx.x < E) {  // per expert: exclusive scan over its parts, total, padded size
+    int acc = 0;
+    for (int i = 0; i < P; ++i) {
+      const int v = part_sum[threadIdx.x * P + i];
+      part_sum[threadIdx.x * P + i] = acc;
+      acc += v;
     }
-    padded[e] = (total + kTile - 1) / kTile * kTile;
+    totals[threadIdx.x] = acc;
   }
   __syncthreads();
-  if (e == 0) {
+  if (threadIdx.x == 0) {
     int acc = 0;
     for (int i = 0; i < E; ++i) {
       offs[i] = acc;
-      acc += padded[i];
+      acc += (totals[i] + kTile - 1) / kTile * kTile;
     }
     offs[E] = acc;
   }
   __syncthreads();
   if (e < E) {
-    const int base = offs[e];
-    for (int64_t c = 0; c < n_chunks; ++c) counts[c * E + e] += base;
-    offsets[e] = base;
-    for (int r = base + total; r < offs[e + 1]; ++r) src_row[r] = -1;
+    int run = offs[e] + part_sum[threadIdx.x];
+    for (int64_t c = c0; c < c1; ++c) {
+      const int v = counts[c * E + e];
+      counts[c * E + e] = run;
+      run += v;
+    }
+    if (part == 0) offsets[e] = offs[e];
+    // padding rows of the group: src_row = -1, spread over the expert's parts
+    for (int r = offs[e] + totals[e] + part; r < offs[e + 1]; r += P) src_row[r] = -1;
   }
-  if (e == 0) offsets[E] = offs[E];
+  if (threadIdx.x == 0) offsets[E] = offs[E];
 }
 
 __global__ __launch_bounds__(64) void route_assign_kernel(const int32_t* __restrict__ idx, int64_t T, int k, int E,
@@ -181,28 +199,25 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uin
 }
 
 // Padding rows (src_row == -1 below offsets[E]): bytes 0x00, scales 2^-126.  Padding
-// only occurs in the last 128-row block of a group; other blocks exit after one read.
+// only occurs in the last 128-row block of a group; other blocks exit after their reads.
+// kPadSplit workgroups share a block: wave w of part p takes rows p * 4 + w + 32 j, a
+// fixed partition, so every padding row is written exactly once.
+constexpr int kPadSplit = 8;
 __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __restrict__ offsets, int E,
-                                                            const int32_t* __restrict__ src_row, int64_t H,
+                                                            const int32_t* __restrict__ src_row, int H,
                                                             uint8_t* __restrict__ q, float* __restrict__ s) {
-  __shared__ int pad_rows[kTile];
-  __shared__ int n_pad;
-  const int64_t r0 = (int64_t)blockIdx.x * kTile;
+  const int blk = blockIdx.x / kPadSplit, part = blockIdx.x - blk * kPadSplit;
+  const int64_t r0 = (int64_t)blk * kTile;
   if (r0 >= offsets[E]) return;
-  if (threadIdx.x == 0) n_pad = 0;
-  __syncthreads();
-  if (threadIdx.x < kTile && src_row[r0 + threadIdx.x] < 0) pad_rows[atomicAdd(&n_pad, 1)] = threadIdx.x;
-  __syncthreads();
-  const int np = n_pad;
-  const int64_t c16 = H / 16, sh = H / kTile;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int c16 = H / 16, sh = H / kTile;
   const u32x4 z = {0u, 0u, 0u, 0u};
-  for (int64_t i = threadIdx.x; i < (int64_t)np * c16; i += kThreads) {
-    const int64_t r = r0 + pad_rows[i / c16];
-    stnt16(q + r * H + (i % c16) * 16, z);
-  }
-  for (int64_t i = threadIdx.x; i < (int64_t)np * sh; i += kThreads) {
-    const int64_t r = r0 + pad_rows[i / sh];
-    s[r * sh + i % sh] = exp2i(kTMin);
+  for (int i = part * (kThreads / 64) + wave; i < kTile; i += kPadSplit * (kThreads / 64)) {
+    const int64_t r = r0 + i;
+    if (src_row[r] >= 0) continue;  // wave-uniform
+    uint8_t* row = q + r * H;
+    for (int c = lane; c < c16; c += 64) stnt16(row + c * 16, z);
+    for (int c = lane; c < sh; c += 64) s[r * sh + c] = exp2i(kTMin);
   }
 }
 
@@ -293,7 +308,7 @@ hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T
     else
       permute_quant_kernel<false><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
   }
-  pad_fill_kernel<<<(unsigned)(M_cap / kTile), kThreads, 0, st>>>(offsets, E, src_row, H, q, s);
+  pad_fill_kernel<<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
   return hipGetLastError();
 }
 

@@ -62,6 +62,16 @@ def test_routing_full(run):
     assert np.array_equal(host(b["src_row"])[:m_pad], run["src_row"])
 
 
+def test_padding_rows_full(run):
+    """Every padding row of the four row-wise FP8 tensors (F1, B1, F3, B3): bytes 0x00 and
+    scale 2^-126 (padding rows enter the weight-gradient sums, so none may hold stale data)."""
+    b = run["b"]
+    pad = _cuda_idx(np.nonzero(run["src_row"] < 0)[0])
+    for qn, sn in (("xq", "xs"), ("dyq", "dys"), ("hq", "hs"), ("daq", "das")):
+        assert not bool(b[qn].index_select(0, pad).any()), qn
+        assert bool((b[sn].index_select(0, pad) == 2.0 ** -126).all()), sn
+
+
 def test_weight_quant_sampled_blocks(run):
     d, b, rng = run["d"], run["b"], run["rng"]
     for wn in ("w1", "w2"):

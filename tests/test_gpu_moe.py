@@ -82,6 +82,28 @@ def test_permute_quant_build_and_reuse(case):
     assert untouched(dq[m_pad:])
 
 
+def test_permute_padding_spans_block():
+    """Groups whose padding covers most of a 128-row block (rows in both 64-row halves),
+    written into poisoned buffers: every padding row must come out zero with scale 2^-126."""
+    shape = workloads.LayerShape("pad", 200, 256, 3, 1, 256, "iid")
+    inp = workloads.layer_inputs(shape, seed=5)
+    idx = torch.full((200, 1), 1, dtype=torch.int32)
+    idx[:5, 0] = 0      # 5 rows -> 123 padding rows
+    idx[5:70, 0] = 2    # 65 rows -> 63 padding rows
+    M_cap, row_map, offsets, src_row, ws = _routing_device(shape, inp)
+    for dst_rows in range(2):  # twice into the same poisoned buffers: the second pass overwrites the first
+        q = poisoned((M_cap, shape.H), torch.uint8) if dst_rows == 0 else q
+        s = poisoned((M_cap, shape.H // 128), torch.float32) if dst_rows == 0 else s
+        ff8.ff8_permute_quant(dev(inp["x"]), None, shape.k, shape.E, dev(idx), False, row_map, offsets, src_row,
+                              q, s, ws)
+        torch.cuda.synchronize()
+        _, w_off, _, w_src = moe.route(host(idx), shape.E)
+        m_pad = int(w_off[-1])
+        wq, wsc = moe.permute_quant_rows(f64(inp["x"]), w_src, shape.k)
+        assert np.array_equal(host(q[:m_pad]), wq) and np.array_equal(host(s[:m_pad]), wsc)
+        assert untouched(q[m_pad:]) and untouched(s[m_pad:])
+
+
 def test_permute_deterministic_and_dropped_slots():
     shape = workloads.LayerShape("drop", 700, 256, 5, 3, 256, "iid")
     inp = workloads.layer_inputs(shape, seed=3)
