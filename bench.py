@@ -141,7 +141,7 @@ def cast_ops(torch, reps=20):
     qs = [torch.empty((R, C), dtype=torch.uint8, device="cuda") for _ in range(n_sets)]
     ss = [torch.empty((R, C // 128), dtype=torch.float32, device="cuda") for _ in range(n_sets)]
     qTs = [torch.empty((C, R), dtype=torch.uint8, device="cuda") for _ in range(n_sets)]
-    sTs = [torch.empty((C, R // 128), dtype=torch.float32, device="cuda") for _ in range(n_sets)]
+    sTs = [torch.empty((R // 128, C), dtype=torch.float32, device="cuda") for _ in range(n_sets)]
     for i in range(n_sets):
         ff8.ff8_quant_rowwise(xs[i], qs[i], ss[i])
     d = torch.empty((R, C), dtype=torch.bfloat16, device="cuda")

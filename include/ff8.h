@@ -18,8 +18,10 @@
  *    Inputs to the quantizers must be finite.  The GEMMs read only the exponent
  *    field of each scale, so scales passed to them must be such powers of two.
  *  - Row-wise (1x128) scaled tensor: q [rows, cols] row-major, s [rows, cols/128].
- *    Column-wise scaled tensors are stored transposed: qT [cols, rows], sT
- *    [cols, rows/128].  Block (128x128) scaled weights: q [E, N, K], s [E, N/128, K/128].
+ *    Column-wise scaled tensors are stored transposed, qT [cols, rows], with
+ *    block-major scales sT [rows/128, cols]: row b holds the scale of every column
+ *    over rows 128b..128b+127.  Block (128x128) scaled weights: q [E, N, K],
+ *    s [E, N/128, K/128].
  *  - Grouped (expert-contiguous) tensors have M_cap rows; expert e owns rows
  *    [offsets[e], offsets[e+1]), every group is padded to a multiple of 128 rows,
  *    and offsets ([E+1] int32) live in DEVICE memory.  Kernels read offsets[E]
@@ -135,8 +137,9 @@ int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t 
  *   dec(b) * 2^-k is rounded to nearest even on the subnormal grid.  No
  *   dequantize / requantize round trip happens, so there is no double
  *   quantization error.
- *   qT [cols, rows] e4m3 (physically transposed), sT [cols, rows/128] float32
- *   (every row of a 128-column tile gets that block's S_max).
+ *   qT [cols, rows] e4m3 (physically transposed), sT [rows/128, cols] float32
+ *   (block-major: sT[b, c] is the S_max of the 128x128 block holding row 128b and
+ *   column c, the same for all 128 columns of a tile).
  *   offsets: [E+1] device int32 (only offsets[E] is read: rows at and beyond it
  *   are skipped and the matching qT columns / sT entries untouched) or NULL
  *   (all rows).  E is ignored when offsets is NULL.
@@ -171,7 +174,8 @@ int ff8_grouped_gemm_dgrad(const ff8_e4m3* g, const float* g_s, const ff8_e4m3* 
  * ff8_grouped_gemm_wgrad -- FP8 grouped GEMM, weight gradient ("Wgrad" of paper
  * section 3.1, fed by column-wise operands from the scaling-aware transpose).
  *   dw[e, n, k] (+)= sum_{m in expert e's rows} D(gT)[n, m] * D(xT)[k, m].
- *   gT [N, M_cap] e4m3 + gT_s [N, M_cap/128]; xT [K, M_cap] e4m3 + xT_s [K, M_cap/128];
+ *   gT [N, M_cap] e4m3 + gT_s [M_cap/128, N]; xT [K, M_cap] e4m3 + xT_s [M_cap/128, K]
+ *   (block-major scales, as written by ff8_scaling_aware_transpose);
  *   dw [E, N, K] float32.  accumulate = 0 overwrites (experts without rows get
  *   zeros); accumulate = 1 adds to dw (experts without rows are left untouched).
  */

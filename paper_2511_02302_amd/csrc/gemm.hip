@@ -89,6 +89,7 @@ struct GemmArgs {
   int Kdim;           // fprop/dgrad: contraction length; wgrad: unused (per group)
   int n_pt, n_qt;     // p tiles; q tiles (wgrad only)
   int accumulate;
+  int n_slots;        // workgroups per XCD in one group of the grid
 };
 
 // K-major stage tile: 256 rows x 128 bytes, 16-byte chunk c of row r at c ^ kswz(r).  Any
@@ -121,14 +122,11 @@ __device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t
   asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
                : "memory");
 }
-// Range-checked scale DMA (always MUBUF: tail lanes may point past the scale tensor).
-__device__ __forceinline__ void dma4r(const i32x4& rsrc, uint32_t soff, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc),
-               "s"(soff) : "memory");
-}
-__device__ __forceinline__ void dma16r(const i32x4& rsrc, uint32_t soff, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc),
-               "s"(soff) : "memory");
+// 4-byte form (scales).  The scale DMAs, like the operand DMAs, keep their whole offset in
+// the range-checked voffset, so a lane past a scale tensor's end reads zeros.
+__device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+               : "memory");
 }
 
 __device__ __forceinline__ uint32_t e8m0(float s) { return __float_as_uint(s) >> 23; }
@@ -168,7 +166,7 @@ struct Tile {
   uint32_t sp_off, sq_off;       // scale DMA: this lane's source offset at K block 0
   int p_kstep, q_kstep;          // bytes per stage of the P / Q source
   int p_istep, q_istep;          // bytes between instructions of one pattern
-  int sp_kb;                     // floats per K block of the P scale source (q scales: 1)
+  int sp_kb, sq_kb;              // floats per K block of the P / Q scale sources
   // fprop / dgrad: a wave's 128 P rows are one 128x128 weight block, so its P scale is one
   // value per K block (stored compactly as [tile half][4 K blocks]); wgrad: one per row.
   static constexpr bool kBlockP = (MODE != kWgrad);
@@ -207,22 +205,28 @@ struct Tile {
       dma16(q_rsrc, q_voff[J >> 2] + step, stage + kTileBytes + grp * 1024u);
     }
   }
-  // Scale DMA of batch b (K blocks 4b..4b+3) into batch buffer b % 2, rows of four floats:
-  // the P instruction (kBlockP: 8 lanes carry the two weight blocks' 4 floats, the rest
-  // duplicate them; else lane l carries tile row 64 wave + l) and the Q instruction (lane
-  // l carries tile row 64 wave + l).  Batches are rotated with the K order (k_rot is a
-  // multiple of the batch); blocks past the last K block read neighbouring rows or zeros
-  // (range-checked resources) and are never multiplied.
+  // Scale DMA of batch b (K blocks kb0..kb0+3 in loop order) into batch buffer b % 2:
+  //   fprop / dgrad P (kBlockP): 8 lanes carry the tile's two weight blocks' 4 floats (the
+  //     rest duplicate them) -> LDS P rows 0 and 1, four floats each;
+  //   fprop / dgrad Q (row-major scales [rows][K/128]): lane l carries the four floats of
+  //     tile row 64 wave + l -> LDS [row][4];
+  //   wgrad P and Q (block-major scales [M_cap/128][rows]): wave w carries K block kb0 + w,
+  //     lane l the tile rows 4l..4l+3, one contiguous 1 KB run -> LDS [K block][256 rows].
+  // Batches are rotated with the K order (k_rot is a multiple of the batch); blocks past
+  // the last K block read neighbouring scales or zeros and are never multiplied.
   __device__ __forceinline__ void dma_scale_p(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1));
     const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-    if constexpr (kBlockP) dma4r(sp_rsrc, kb0 * (uint32_t)sp_kb * 4u, sp_off, lbase);
-    else dma16r(sp_rsrc, kb0 * 4u, sp_off, lbase + (uint32_t)wave * 1024u);
+    if constexpr (kBlockP) dma4(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * 4u, lbase);
+    else dma16(sp_rsrc, sp_off + (kb0 + (uint32_t)wave) * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
   }
   __device__ __forceinline__ void dma_scale_q(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1)) + kTP * kScaleBatch * 4;
     const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-    dma16r(sq_rsrc, kb0 * 4u, sq_off, lbase + (uint32_t)wave * 1024u);
+    if constexpr (MODE == kWgrad)
+      dma16(sq_rsrc, sq_off + (kb0 + (uint32_t)wave) * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
+    else
+      dma16(sq_rsrc, sq_off + kb0 * 4u, lbase + (uint32_t)wave * 1024u);
   }
 
   // Fragment read J of half h of stage buffer B into register set kSetA.
@@ -264,8 +268,8 @@ struct Tile {
       read_all_from<B, H, kSetA, J + 1>();
     }
   }
-  // Scales of batch b (LDS buffer b % 2, rows of four K-block floats): read the rows of
-  // one operand this lane multiplies into raw (kQ, or wgrad P: rows 128 w + 32 R + l for
+  // Scales of batch b (LDS buffer b % 2): read the four K-block scales of each row of one
+  // operand this lane multiplies into raw[R] (kQ, or wgrad P: rows 128 w + 32 R + l for
   // R = 0..3; fprop / dgrad P: the wave's one weight-block row, raw[0] only) ...
   // Rows R0..R1-1 only (read and packed a few at a time, to keep few raw rows live).
   template <bool kQ, int R0, int R1>
@@ -274,9 +278,16 @@ struct Tile {
     const int l31 = opaque_lane() & 31;  // recomputed here rather than held through the tile
     if constexpr (!kQ && kBlockP) {
       if constexpr (R0 == 0) raw[0] = S[wp];
-    } else {
+    } else if constexpr (MODE == kWgrad) {  // [K block][256 rows]
+      const float* F = &g_sc[b & 1][kQ ? kTP * kScaleBatch : 0];
+      const int row = (kQ ? 128 * wq : 128 * wp) + l31;
 #pragma unroll
-      for (int R = R0; R < R1; ++R) raw[R] = kQ ? S[kTP + 128 * wq + 32 * R + l31] : S[128 * wp + 32 * R + l31];
+      for (int R = R0; R < R1; ++R)
+#pragma unroll
+        for (int j = 0; j < kScaleBatch; ++j) raw[R][j] = __float_as_uint(F[j * kTP + row + 32 * R]);
+    } else {  // Q rows of four K-block floats
+#pragma unroll
+      for (int R = R0; R < R1; ++R) raw[R] = S[kTP + 128 * wq + 32 * R + l31];
     }
   }
   // ... and pack them: word j holds the E8M0 byte (the fp32 exponent field of a
@@ -484,36 +495,42 @@ __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, con
       T.p_voff[hh] = (p_row0 + r) * p_ld + k0 + c * 16;
     }
   }
-  // scale DMA sources (resources range-checked to the end of each scale tensor)
-  const uint32_t q_sld = q_ld / kTile;  // floats per Q scale row
-  const float* sq_base = g.sQ + k0 / kTile;
+  // scale DMA sources (resources range-checked to the end of each scale tensor; offsets
+  // are at K block 0 of the tile, the batch adds its K-block offset)
   const float* sp_base;
-  const uint32_t sq_total = q_rows * q_sld - ((MODE == kWgrad) ? k0 / kTile : 0);
-  uint32_t sp_total;
-  if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
-    sp_base = g.sP + (size_t)e * (Np / kTile) * (Kdim / kTile);
-    T.sp_kb = 1;
-    sp_total = ((uint32_t)g.E - e) * (Np / kTile) * (Kdim / kTile);
-  } else if (MODE == kDgrad) {  // w_s [E][Kdim/128][Np/128]
-    sp_base = g.sP + (size_t)e * (Kdim / kTile) * (Np / kTile);
-    T.sp_kb = (int)(Np / kTile);
-    sp_total = ((uint32_t)g.E - e) * (Kdim / kTile) * (Np / kTile);
-  } else {  // xT_s [Np][M_cap/128]
-    sp_base = g.sP + k0 / kTile;
-    T.sp_kb = 1;
-    sp_total = Np * (M_cap / kTile) - k0 / kTile;
-  }
-  const uint32_t r = 64 * wave + lane;  // tile row of this lane's Q (and wgrad P) scales
-  const uint32_t q = min(q0 + r, q_rows - 1);
-  T.sq_off = q * q_sld * 4;
-  if (MODE == kWgrad) {
-    const uint32_t pr = min(p0 + r, Np - 1);
-    T.sp_off = pr * (M_cap / kTile) * 4;
+  uint32_t sp_total, sq_total;
+  if (MODE == kWgrad) {  // block-major: xT_s [M_cap/128][Np], gT_s [M_cap/128][Nq]
+    const uint32_t Nq = (uint32_t)g.Nq, kb_first = k0 / kTile;
+    sp_base = g.sP;
+    T.sp_kb = (int)Np;
+    T.sq_kb = (int)Nq;
+    sp_total = (M_cap / kTile) * Np;
+    sq_total = (M_cap / kTile) * Nq;
+    T.sp_off = (kb_first * Np + p0 + 4 * lane) * 4;
+    T.sq_off = (kb_first * Nq + q0 + 4 * lane) * 4;
   } else {
-    const uint32_t pb = min(p0 / kTile + ((lane >> 2) & 1), Np / kTile - 1);  // the tile's two weight block rows
+    // Q: row-major a_s / g_s [M_cap][Kdim/128], lane l of wave w carries tile row 64 w + l
+    const uint32_t q_sld = Kdim / kTile;
+    const uint32_t q = min(q0 + 64 * wave + lane, q_rows - 1);
+    T.sq_kb = 1;
+    sq_total = q_rows * q_sld;
+    T.sq_off = q * q_sld * 4;
+    // P: the tile's two weight block rows, four K blocks per lane group of four
+    const uint32_t pb = min(p0 / kTile + ((lane >> 2) & 1), Np / kTile - 1);
     const uint32_t j = lane & 3;
-    T.sp_off = ((MODE == kFprop) ? pb * (Kdim / kTile) + j : j * (Np / kTile) + pb) * 4;
+    if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
+      sp_base = g.sP + (size_t)e * (Np / kTile) * (Kdim / kTile);
+      T.sp_kb = 1;
+      sp_total = ((uint32_t)g.E - e) * (Np / kTile) * (Kdim / kTile);
+      T.sp_off = (pb * (Kdim / kTile) + j) * 4;
+    } else {  // w_s [E][Kdim/128][Np/128]
+      sp_base = g.sP + (size_t)e * (Kdim / kTile) * (Np / kTile);
+      T.sp_kb = (int)(Np / kTile);
+      sp_total = ((uint32_t)g.E - e) * (Kdim / kTile) * (Np / kTile);
+      T.sp_off = (j * (Np / kTile) + pb) * 4;
+    }
   }
+  const float* sq_base = g.sQ;
   T.sp_rsrc = make_rsrc(sp_base, sp_total * 4);
   T.sq_rsrc = make_rsrc(sq_base, sq_total * 4);
   // Blocks start their K loops at different scale-batch-aligned stages, so that the XCDs
@@ -645,35 +662,41 @@ __device__ __forceinline__ void dma_second_stage(Tile<MODE>& T) {
   T.template dma_tile<1, 15>(s1);
 }
 
-// Persistent: one workgroup per CU, up to kPersistSlots per XCD.  Workgroups are
-// dispatched round-robin over the 8 XCDs.  XCD x owns XCD blocks x, x + 8, x + 16, ...
-// (kBQ x kBP tiles each, p fastest); its work list is their tiles in that order, and its
-// S workgroups take items s, s + S, s + 2S, ...  With S = 32 (256 CUs), slot s takes tile
-// s of every block, so the 32 workgroups of an XCD work on one block at a time and share
-// its 8 q panels and 4 p panels per K step in their L2, while the 8 XCDs together sweep
-// one 16 x 16-tile window (about one expert).
+// Semi-persistent: the grid is a sequence of groups of S workgroups per XCD (S = 32 on
+// 256 CUs, one workgroup per CU), and each workgroup runs kRoundsPerWg tiles.  Workgroups
+// are dispatched round-robin over the 8 XCDs, and in order within an XCD.  XCD x owns XCD
+// blocks x, x + 8, x + 16, ... (kBQ x kBP tiles each, p fastest); its work list is their
+// tiles in that order, item i = k S + s going to slot s of the group that owns round k.
+// With S = 32, slot s takes tile s of every block, so the 32 workgroups of an XCD work on
+// one block at a time and share its 8 q panels and 4 p panels per K step in their L2, while
+// the 8 XCDs together sweep one 16 x 16-tile window (about one expert).  Bounding a
+// workgroup to a few rounds keeps an XCD's workgroups from drifting apart (which costs L2
+// sharing) and lets faster CUs take more groups.
 // Between tiles, the next tile's first stage (and scale batch) streams into stage buffer 0
 // while the finished tile's output is staged through buffer 1 and stored; its second
 // stage follows once the epilogue has left buffer 1.  All control flow is
 // workgroup-uniform (tile decode from uniform values), so every barrier is reached by all
 // four waves, and every wave leaves the tile loop with the same tile count.
-constexpr int kPersistSlots = kBQ * kBP;  // workgroups per XCD
+constexpr int kPersistSlots = kBQ * kBP;  // workgroups per XCD and group
+constexpr int kRoundsPerWg = 4;           // work rounds (tiles) per workgroup
 
 // Workgroup barrier that waits for this wave's LDS accesses only: global stores may stay in
 // flight across it (a __syncthreads fence would drain them).  One asm statement, so that
 // no memory access moves across the barrier.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Next tile of this workgroup from work item k on (k advances past empty edge tiles).
+// Next tile of this workgroup from round k on, below round k_end (k advances past empty
+// edge tiles).
 template <int MODE>
-__device__ __forceinline__ bool next_tile(const GemmArgs& g, int xcd, int slot, int n_slots, int n_blocks, int& k,
-                                          TileInfo& t) {
-  for (;; ++k) {
+__device__ __forceinline__ bool next_tile(const GemmArgs& g, int xcd, int slot, int n_slots, int n_blocks, int k_end,
+                                          int& k, TileInfo& t) {
+  for (; k < k_end; ++k) {
     const int i = k * n_slots + slot;
     const int blk = (i / kPersistSlots) * 8 + xcd;
     if (blk >= n_blocks) return false;
     if (decode_tile<MODE>(g, blk, i % kPersistSlots, t)) return true;
   }
+  return false;
 }
 
 template <int MODE>
@@ -684,7 +707,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   T.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   T.wp = T.wave & 1;
   T.wq = T.wave >> 1;
-  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, n_slots = gridDim.x >> 3;
+  const int n_slots = g.n_slots, group_size = 8 * n_slots;
+  const int group = blockIdx.x / group_size, in_group = blockIdx.x - group * group_size;
+  const int xcd = in_group & 7, slot = in_group >> 3;
+  const int k_end = (group + 1) * kRoundsPerWg;
 
   int n_qg;  // q tiles
   if (MODE != kWgrad) {
@@ -717,9 +743,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     n_qg = g.E * g.n_qt;
   }
   const int n_blocks = ((g.n_pt + kBP - 1) / kBP) * ((n_qg + kBQ - 1) / kBQ);
-  int k = 0;
+  int k = group * kRoundsPerWg;
   TileInfo t;
-  if (!next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k, t)) return;
+  if (!next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, k, t)) return;
   setup_tile<MODE>(T, g, t);
   if (T.nk > 0) dma_first_stage<MODE>(T);
   // Loop invariant: tile t is set up, its stage 0 and scale batch 0 are in flight (if it
@@ -757,7 +783,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     lds_barrier();  // every wave is done with the stage buffers and the scale batches
     TileInfo tn;
     ++k;
-    const bool more = next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k, tn);
+    const bool more = next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, k, tn);
     if (more) {
       setup_tile<MODE>(T, g, tn);
       if (T.nk > 0) dma_first_stage<MODE>(T);  // buffer 0 and scale batch 0, under the epilogue
@@ -769,14 +795,20 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   }
 }
 
-// Persistent grid: one workgroup per CU, the same number on each of the 8 XCDs, at most
-// kPersistSlots per XCD.
-unsigned grid_blocks() {
+// Grid: groups of n_slots workgroups per XCD (one per CU, the same number on each of the
+// 8 XCDs, at most kPersistSlots), enough groups of kRoundsPerWg rounds for n_blocks_max XCD
+// blocks (workgroups past the work actually present exit at once).
+unsigned grid_blocks(int64_t n_blocks_max, int& n_slots) {
   int cus = (device_cu_count() / 8) * 8;
   if (cus > 8 * kPersistSlots) cus = 8 * kPersistSlots;
   if (cus < 8) cus = 8;
-  return (unsigned)cus;
+  n_slots = cus / 8;
+  const int64_t items = (n_blocks_max + 7) / 8 * kPersistSlots;  // work items per XCD
+  const int64_t rounds = (items + n_slots - 1) / n_slots;
+  const int64_t groups = (rounds + kRoundsPerWg - 1) / kRoundsPerWg;
+  return (unsigned)((groups > 0 ? groups : 1) * 8 * n_slots);
 }
+int64_t blocks_of(int n_pt, int64_t n_qg) { return (int64_t)((n_pt + kBP - 1) / kBP) * ((n_qg + kBQ - 1) / kBQ); }
 
 }  // namespace
 
@@ -794,18 +826,18 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
   if (mode == kFprop) {  // out[m, n] = a[m, :] . w[e, n, :]
     g.Np = N; g.Kdim = K;
     g.n_pt = (int)((N + kTP - 1) / kTP);
-    grid = grid_blocks();
+    grid = grid_blocks(blocks_of(g.n_pt, (M_cap + kTQ - 1) / kTQ + (E + 1) / 2), g.n_slots);
     grouped_gemm_kernel<kFprop><<<grid, kThreads, 0, st>>>(g);
   } else if (mode == kDgrad) {  // out[m, k] = g[m, :] . w[e, :, k]
     g.Np = K; g.Kdim = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
-    grid = grid_blocks();
+    grid = grid_blocks(blocks_of(g.n_pt, (M_cap + kTQ - 1) / kTQ + (E + 1) / 2), g.n_slots);
     grouped_gemm_kernel<kDgrad><<<grid, kThreads, 0, st>>>(g);
   } else {  // dw[e, n, k] = sum_m gT[n, m] xT[k, m]
     g.Np = K; g.Nq = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
     g.n_qt = (int)((N + kTQ - 1) / kTQ);
-    grid = grid_blocks();
+    grid = grid_blocks(blocks_of(g.n_pt, (int64_t)E * g.n_qt), g.n_slots);
     grouped_gemm_kernel<kWgrad><<<grid, kThreads, 0, st>>>(g);
   }
   return hipGetLastError();

@@ -15,8 +15,9 @@
 //      output order (XOR-swizzled 8-byte chunks, conflict-free);
 //   5. the 128x128 output block is streamed out with 16-byte non-temporal stores, 8
 //      lanes per 128-byte output row segment.
-// The block's S_max is written to sT once per output row: kRB consecutive blocks give
-// kRB contiguous floats per row, so scale stores are 4*kRB bytes wide.
+// The column-wise scales are block-major, sT [rows/128][cols]: block rb's S_max goes to the
+// 128 consecutive floats of its column tile (one coalesced 512-byte store per block), and
+// a consumer reads one contiguous run per 128-row block for any range of columns.
 
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
@@ -73,7 +74,6 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
   (void)n_rb_groups;
   const int64_t m_rows = active_rows(offsets, E, rows);
   const int64_t n_rb = rows / kTile;
-  const int n_sb = (int)(rows / kTile);  // sT row stride (floats)
   const int64_t rb0 = (int64_t)rg * kRB;
   int n_valid = 0;  // blocks of this group that hold data (uniform)
 #pragma unroll
@@ -164,17 +164,10 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
     __syncthreads();  // the tile is rewritten by the next block
   }
 
-  // 5. column-wise scales: every output row of the tile gets S_max of each block.
+  // 5. column-wise scales: S_max of each block for the tile's 128 columns.
   if (tid < 128) {
-    float* dst = sT + ((int64_t)cb * kTile + tid) * n_sb + rb0;
-    if (kRB == 4 && n_valid == kRB && (((uintptr_t)dst) & 15) == 0) {  // one 16-byte store
-      u32x4 o;
-#pragma unroll
-      for (int bi = 0; bi < kRB; ++bi) o[bi] = __float_as_uint(exp2i((int)max(wmax[bi][0], wmax[bi][1]) - 256));
-      st16(dst, o);
-    } else {
-      for (int bi = 0; bi < n_valid; ++bi) dst[bi] = exp2i((int)max(wmax[bi][0], wmax[bi][1]) - 256);
-    }
+    for (int bi = 0; bi < n_valid; ++bi)
+      sT[(rb0 + bi) * cols + (int64_t)cb * kTile + tid] = exp2i((int)max(wmax[bi][0], wmax[bi][1]) - 256);
   }
 }
 

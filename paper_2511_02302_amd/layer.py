@@ -73,7 +73,7 @@ class ExpertLayerFP8:
         b["dx"] = _empty((T, H), bf16, dev)
         for name, cols in (("x", H), ("h", I), ("dy", H), ("da", 2 * I)):
             b[name + "Tq"] = _empty((cols, M), u8, dev)
-            b[name + "Ts"] = _empty((cols, M // 128), f32, dev)
+            b[name + "Ts"] = _empty((M // 128, cols), f32, dev)  # block-major column scales
         b["dw1"] = _empty((E, 2 * I, H), f32, dev)
         b["dw2"] = _empty((E, H, I), f32, dev)
 

@@ -165,9 +165,9 @@ def _wgrad_samples(run, gT, xT, out):
         c = rng.integers(K, size=N_GEMM // 4)
         got = host(b[out][int(e)][_cuda_idx(n), _cuda_idx(c)])
         g = quant.dequant_rowwise(host(b[gT + "q"][_cuda_idx(n), lo:hi]),
-                                  host(b[gT + "s"][_cuda_idx(n), lo // 128:hi // 128]))
+                                  host(b[gT + "s"][lo // 128:hi // 128][:, _cuda_idx(n)]).T)
         x = quant.dequant_rowwise(host(b[xT + "q"][_cuda_idx(c), lo:hi]),
-                                  host(b[xT + "s"][_cuda_idx(c), lo // 128:hi // 128]))
+                                  host(b[xT + "s"][lo // 128:hi // 128][:, _cuda_idx(c)]).T)
         _check_gemm_samples(got, np.sum(g * x, axis=1), np.sum(np.abs(g * x), axis=1), bf16_out=False)
     for e in np.nonzero(off[1:] == off[:-1])[0]:
         assert not bool(b[out][int(e)].any()), f"expert {e} has no rows but a nonzero gradient"
@@ -217,4 +217,4 @@ def test_sat_sampled_blocks(run):
             rs, cs = slice(rb * 128, (rb + 1) * 128), slice(cb * 128, (cb + 1) * 128)
             wqT, wsT = sat.scaling_aware_transpose(host(q[rs, cs]), host(s[rs, cb:cb + 1]))
             assert np.array_equal(host(qT[cs, rs]), wqT), (name, rb, cb)
-            assert np.array_equal(host(sT[cs, rb:rb + 1]), wsT), (name, rb, cb)
+            assert np.array_equal(host(sT[rb:rb + 1, cs]).T, wsT), (name, rb, cb)

@@ -147,7 +147,7 @@ def _row_scaled_fp8(rows, cols, seed, kmax=12):
 def test_sat_bit_exact(rows, cols, n_rows):
     q, s = _row_scaled_fp8(rows, cols, seed=rows + cols)
     qT = poisoned((cols, rows), torch.uint8)
-    sT = poisoned((cols, rows // 128), torch.float32)
+    sT = poisoned((rows // 128, cols), torch.float32)
     offsets = None
     if n_rows != rows:
         offsets = dev(torch.tensor([0, n_rows // 2, n_rows], dtype=torch.int32))
@@ -156,8 +156,8 @@ def test_sat_bit_exact(rows, cols, n_rows):
     torch.cuda.synchronize()
     wqT, wsT = sat.scaling_aware_transpose(q, s, n_rows)
     assert np.array_equal(host(qT[:, :n_rows]), wqT)
-    assert np.array_equal(host(sT[:, : n_rows // 128]), wsT)
-    assert untouched(qT[:, n_rows:]) and untouched(sT[:, n_rows // 128:])
+    assert np.array_equal(host(sT[: n_rows // 128]).T, wsT)  # block-major on the device
+    assert untouched(qT[:, n_rows:]) and untouched(sT[n_rows // 128:])
 
 
 def test_sat_extreme_row_range():
@@ -173,12 +173,12 @@ def test_sat_extreme_row_range():
     x = x.to(torch.bfloat16)
     q, s = quant.quant_rowwise(f64(x))
     qT = poisoned((256, 256), torch.uint8)
-    sT = poisoned((256, 2), torch.float32)
+    sT = poisoned((2, 256), torch.float32)
     ff8.ff8_scaling_aware_transpose(dev(torch.from_numpy(q)), dev(torch.from_numpy(s)), qT, sT)
     torch.cuda.synchronize()
     wqT, wsT = sat.scaling_aware_transpose(q, s)
     assert np.array_equal(host(qT), wqT)
-    assert np.array_equal(host(sT), wsT)
+    assert np.array_equal(host(sT).T, wsT)
 
 
 def test_sat_full_size_sampled_blocks():
@@ -188,7 +188,7 @@ def test_sat_full_size_sampled_blocks():
     s = torch.empty((rows, cols // 128), dtype=torch.float32, device="cuda")
     ff8.ff8_quant_rowwise(x, q, s)
     qT = torch.empty((cols, rows), dtype=torch.uint8, device="cuda")
-    sT = torch.empty((cols, rows // 128), dtype=torch.float32, device="cuda")
+    sT = torch.empty((rows // 128, cols), dtype=torch.float32, device="cuda")
     ff8.ff8_scaling_aware_transpose(q, s, qT, sT)
     torch.cuda.synchronize()
     rng = np.random.default_rng(1)
@@ -198,7 +198,7 @@ def test_sat_full_size_sampled_blocks():
         sb = host(s[rb * 128:(rb + 1) * 128, cb:cb + 1])
         wqT, wsT = sat.scaling_aware_transpose(qb, sb)
         assert np.array_equal(host(qT[cb * 128:(cb + 1) * 128, rb * 128:(rb + 1) * 128]), wqT)
-        assert np.array_equal(host(sT[cb * 128:(cb + 1) * 128, rb:rb + 1]), wsT)
+        assert np.array_equal(host(sT[rb:rb + 1, cb * 128:(cb + 1) * 128]).T, wsT)
 
 
 def test_naive_baseline_chain_matches_oracle():

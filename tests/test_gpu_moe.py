@@ -175,15 +175,15 @@ def test_grouped_gemms(case):
     assert rel_frob(f64(dh[:m_pad]), want) < GEMM_TOL
     # wgrad: dW1[e] = G_e^T X_e from column-wise operands (scaling-aware transposes)
     gT = torch.empty((2 * I, M_cap), dtype=torch.uint8, device="cuda")
-    gTs = torch.empty((2 * I, M_cap // 128), dtype=torch.float32, device="cuda")
+    gTs = torch.empty((M_cap // 128, 2 * I), dtype=torch.float32, device="cuda")  # block-major
     xT = torch.empty((H, M_cap), dtype=torch.uint8, device="cuda")
-    xTs = torch.empty((H, M_cap // 128), dtype=torch.float32, device="cuda")
+    xTs = torch.empty((M_cap // 128, H), dtype=torch.float32, device="cuda")
     ff8.ff8_scaling_aware_transpose(gq, gs, gT, gTs, offsets, E)
     ff8.ff8_scaling_aware_transpose(xq, xs, xT, xTs, offsets, E)
     dw = torch.full((E, 2 * I, H), 7.0, dtype=torch.float32, device="cuda")
     ff8.ff8_grouped_gemm_wgrad(gT, gTs, xT, xTs, offsets, dw, accumulate=False)
     torch.cuda.synchronize()
-    want = moe.grouped_gemm_wgrad(host(gT), host(gTs), host(xT), host(xTs), off)
+    want = moe.grouped_gemm_wgrad(host(gT), host(gTs).T, host(xT), host(xTs).T, off)
     assert rel_frob(host(dw), want) < GEMM_TOL
     for e in range(E):
         if off[e + 1] == off[e]:
@@ -340,8 +340,8 @@ def test_layer_stagewise(case):
     for name in ("x", "h", "dy", "da"):
         qT, sT = sat.scaling_aware_transpose(host(b[name + "q"][:m_pad]), host(b[name + "s"][:m_pad]))
         assert np.array_equal(host(b[name + "Tq"][:, :m_pad]), qT), name
-        assert np.array_equal(host(b[name + "Ts"][:, : m_pad // 128]), sT), name
-    dW2 = moe.grouped_gemm_wgrad(host(b["dyTq"]), host(b["dyTs"]), host(b["hTq"]), host(b["hTs"]), off)
+        assert np.array_equal(host(b[name + "Ts"][: m_pad // 128]).T, sT), name
+    dW2 = moe.grouped_gemm_wgrad(host(b["dyTq"]), host(b["dyTs"]).T, host(b["hTq"]), host(b["hTs"]).T, off)
     assert rel_frob(host(b["dw2"]), dW2) < GEMM_TOL
-    dW1 = moe.grouped_gemm_wgrad(host(b["daTq"]), host(b["daTs"]), host(b["xTq"]), host(b["xTs"]), off)
+    dW1 = moe.grouped_gemm_wgrad(host(b["daTq"]), host(b["daTs"]).T, host(b["xTq"]), host(b["xTs"]).T, off)
     assert rel_frob(host(b["dw1"]), dW1) < GEMM_TOL
