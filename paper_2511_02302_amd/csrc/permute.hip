@@ -221,9 +221,11 @@ __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __res
   }
 }
 
-// One workgroup per token: lane c sums 16 elements of the token's k rows in slot order
-// (float32, routing weight applied per slot when given), one bf16 rounding.  Up to
-// kUnrollK slots are loaded before the sum so that their reads are in flight together.
+// One workgroup per token: each lane sums two 8-element chunks (c and c + blockDim, so
+// that every 16-byte load instruction of a wave covers 1 KB contiguous) of the token's k
+// rows in slot order (float32, routing weight applied per slot when given), one bf16
+// rounding.  Up to kUnrollK slots are loaded before the sum so that their reads are in
+// flight together.
 constexpr int kUnrollK = 8;
 template <bool kWeighted>
 __global__ __launch_bounds__(kRowThreadsMax) void unpermute_kernel(const uint16_t* __restrict__ y_perm,
@@ -231,8 +233,10 @@ __global__ __launch_bounds__(kRowThreadsMax) void unpermute_kernel(const uint16_
                                                                    const float* __restrict__ row_w, int k, int64_t H,
                                                                    int64_t M_cap, uint16_t* __restrict__ y) {
   const int64_t t = blockIdx.x;
-  const int64_t n16 = H / 16;
-  for (int64_t c = threadIdx.x; c < n16; c += blockDim.x) {
+  const int64_t n8 = H / 8, stride = blockDim.x;
+  for (int64_t c = threadIdx.x; c < n8; c += 2 * stride) {
+    const bool two = c + stride < n8;
+    const int64_t c1 = two ? c + stride : c;
     float acc[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
@@ -244,8 +248,8 @@ __global__ __launch_bounds__(kRowThreadsMax) void unpermute_kernel(const uint16_
         const int j = j0 + jj;
         rows[jj] = (j < k) ? row_map[t * k + j] : -1;
         if (rows[jj] >= 0 && rows[jj] < M_cap) {
-          a[jj] = ldnt16(y_perm + (int64_t)rows[jj] * H + c * 16);
-          b[jj] = ldnt16(y_perm + (int64_t)rows[jj] * H + c * 16 + 8);
+          a[jj] = ldnt16(y_perm + (int64_t)rows[jj] * H + c * 8);
+          b[jj] = ldnt16(y_perm + (int64_t)rows[jj] * H + c1 * 8);
         }
       }
 #pragma unroll
@@ -270,8 +274,8 @@ __global__ __launch_bounds__(kRowThreadsMax) void unpermute_kernel(const uint16_
       o0[i] = pack_bf16x2(acc[2 * i], acc[2 * i + 1]);
       o1[i] = pack_bf16x2(acc[8 + 2 * i], acc[8 + 2 * i + 1]);
     }
-    stnt16(y + t * H + c * 16, o0);
-    stnt16(y + t * H + c * 16 + 8, o1);
+    stnt16(y + t * H + c * 8, o0);
+    if (two) stnt16(y + t * H + c1 * 8, o1);
   }
 }
 
