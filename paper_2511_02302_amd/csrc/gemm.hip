@@ -106,7 +106,11 @@ __device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
 // rows past a tensor's end read zeros, so tiles at the edges need no clamping.  Issued
 // through inline asm so that the compiler does not serialize the pipeline with
 // conservative waits; the kernel waits for its own DMA (vmcnt) before the barrier that
-// publishes a stage.
+// publishes a stage.  The compiler's hazard checks do not look inside asm, so each asm
+// starts with the 5 wait states that a buffer instruction needs after a VALU write of an
+// SGPR it reads (the resource or M0 may come straight from v_readfirstlane, or from
+// v_readlane when the compiler reloads a spilled SGPR); with fewer, the load can use the
+// register's old value.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 // Raw (stride 0) buffer resource: loads at offsets >= `bytes` return zeros.
 __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0xFFFFFFFFu) {
@@ -119,13 +123,13 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0x
   return r;
 }
 __device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
                : "memory");
 }
 // 4-byte form (scales).  The scale DMAs, like the operand DMAs, keep their whole offset in
 // the range-checked voffset, so a lane past a scale tensor's end reads zeros.
 __device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+  asm volatile("s_nop 4\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
                : "memory");
 }
 
