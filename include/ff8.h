@@ -27,6 +27,11 @@
  *    and offsets ([E+1] int32) live in DEVICE memory.  Kernels read offsets[E]
  *    (= M_pad) on the device; rows in [M_pad, M_cap) are neither read nor
  *    written.  Grids are sized from M_cap, so no call synchronizes with the host.
+ *    Because they are never copied to the host, offsets are not validated: they
+ *    must satisfy 0 = offsets[0] <= offsets[1] <= ... <= offsets[E] <= M_cap with
+ *    every difference a multiple of 128, as ff8_permute_quant writes them.  Other
+ *    values give undefined results and may make kernels access memory outside the
+ *    tensors.  E is at most 1024.
  *  - Every pointer is a device pointer unless stated otherwise.  The caller
  *    owns all memory; the library allocates nothing and keeps no pointer after
  *    a call returns.

@@ -140,7 +140,8 @@ static int gemm_common(const char* fn, const void* a, const void* as, const void
                        const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, const void* out,
                        bool expert_weights) {
   if (!a || !as || !b || !bs || !offsets || !out) return fail(FF8_ERR_NULL, "%s: a required pointer is NULL", fn);
-  if (E < 1) return fail(FF8_ERR_ARG, "%s: E must be >= 1", fn);
+  // fprop and dgrad keep per-expert tile counts and row offsets in LDS tables of 1025 entries
+  if (E < 1 || E > 1024) return fail(FF8_ERR_ARG, "%s: E must be in [1, 1024]", fn);
   if (!mult128(M_cap) || !mult128(N) || !mult128(K))
     return fail(FF8_ERR_SHAPE, "%s: M_cap, N and K must be positive multiples of 128", fn);
   // the kernels address each operand tensor (the token-major activations, all experts'

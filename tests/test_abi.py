@@ -58,6 +58,8 @@ def test_validation_errors_without_gpu(lib):
     assert lib.ff8_grouped_gemm_fprop(fake, fake, fake, fake, fake, 0, 128, 128, 128, fake, None) == 3
     assert lib.ff8_grouped_gemm_wgrad(fake, fake, fake, fake, fake, 2, 128, 128, 128, fake, 2, None) == 3
     assert lib.ff8_grouped_gemm_dgrad(fake, fake, fake, fake, None, 2, 128, 128, 128, fake, None) == 1
+    assert lib.ff8_grouped_gemm_fprop(fake, fake, fake, fake, fake, 1025, 128, 128, 128, fake, None) == 3
+    assert b"1024" in lib.ff8_last_error()
     # permute: k > E, M_cap below the bound, workspace too small
     assert lib.ff8_permute_quant(fake, None, 16, 128, 3, 2, fake, 0, fake, fake, fake, 1024, fake, fake,
                                  fake, 1 << 20, None) == 3
