@@ -187,6 +187,7 @@ int ff8_swiglu_quant(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M
                      float* hs, void* stream) {
   REQUIRE_PTR(a); REQUIRE_PTR(hq); REQUIRE_PTR(hs);
   REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
   if (offsets) REQUIRE_ARG(E >= 1);
   return hip_status(ff8::launch_swiglu_quant(a, offsets, E, M_cap, I, hq, hs, as_stream(stream)), __func__);
 }
@@ -195,6 +196,7 @@ int ff8_swiglu_bwd_quant(const ff8_bf16* a, const ff8_bf16* dh, const int32_t* o
                          int64_t I, ff8_e4m3* daq, float* das, void* stream) {
   REQUIRE_PTR(a); REQUIRE_PTR(dh); REQUIRE_PTR(daq); REQUIRE_PTR(das);
   REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
   if (offsets) REQUIRE_ARG(E >= 1);
   return hip_status(ff8::launch_swiglu_bwd_quant(a, dh, offsets, E, M_cap, I, daq, das, as_stream(stream)),
                     __func__);

@@ -7,7 +7,7 @@
 //   1. up front, the row scales of all kRB blocks give every row's exponent (to LDS)
 //      and each block's S_max (wave DPP max + LDS), behind a single barrier;
 //   2. per block, lane (sr, sc) holds an 8x8 byte sub-block (rows 8 sr.., bytes 8 sc..;
-//      16 lanes read a full 128-byte row segment), loaded one block ahead;
+//      16 lanes read a full 128-byte row segment); all kRB blocks are loaded up front;
 //   3. rows with k_i = log2(S_max) - log2(s_i) > 0 are re-expressed at S_max: decode
 //      (exact), multiply by 2^-k (exact), hardware RNE encode -- equal to lowering the
 //      exponent field by k_i while it stays >= 1, and the nearest-even subnormal below;
@@ -27,7 +27,7 @@ namespace ff8 {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kRB = 4;  // 128-row blocks per workgroup
+constexpr int kRB = 2;  // 128-row blocks per workgroup (all loaded before the first is written)
 
 __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
   return __builtin_amdgcn_perm(hi, lo, sel);
@@ -95,19 +95,23 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
       if ((tid & 63) == 0) wmax[bi][tid >> 6] = m;
     }
   }
-  // first block's data in flight across the barrier
-  u32x2 v[8];
-  {
-    const uint8_t* src = q + (rb0 * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
-    if (n_valid > 0) {
+  // every block's data in flight across the barrier
+  u32x2 vb[kRB][8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = ld8(src + (int64_t)i * cols);
+  for (int bi = 0; bi < kRB; ++bi) {
+    if (bi < n_valid) {
+      const uint8_t* src = q + ((rb0 + bi) * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) vb[bi][i] = ld8(src + (int64_t)i * cols);
     }
   }
   __syncthreads();
 
-  for (int bi = 0; bi < n_valid; ++bi) {
+#pragma unroll
+  for (int bi = 0; bi < kRB; ++bi) {
+    if (bi >= n_valid) break;
     const int64_t rb = rb0 + bi;
+    u32x2* v = vb[bi];
     const int t_max = (int)max(wmax[bi][0], wmax[bi][1]) - 256;
     // 2. rows below S_max are re-expressed at S_max: decode (exact), times 2^-k (exact),
     //    RNE encode -- the exponent-field decrement, and nearest-even below the normals.
@@ -128,12 +132,6 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
     transpose4x4(v[4][0], v[5][0], v[6][0], v[7][0], o_hi[0], o_hi[1], o_hi[2], o_hi[3]);
     transpose4x4(v[0][1], v[1][1], v[2][1], v[3][1], o_lo[4], o_lo[5], o_lo[6], o_lo[7]);
     transpose4x4(v[4][1], v[5][1], v[6][1], v[7][1], o_hi[4], o_hi[5], o_hi[6], o_hi[7]);
-    // next block's data in flight while this one goes through LDS
-    if (bi + 1 < n_valid) {
-      const uint8_t* src = q + ((rb + 1) * kTile + sr * 8) * cols + (int64_t)cb * kTile + sc * 8;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = ld8(src + (int64_t)i * cols);
-    }
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int orow = sc * 8 + c;
