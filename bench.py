@@ -47,6 +47,7 @@ def parse():
     ap.add_argument("--workload", choices=["dsv3", "skew", "tiny"], default="dsv3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cast-ops", action="store_true")
+    ap.add_argument("--no-fp8-checkpoint", action="store_true")
     return ap.parse_args()
 
 
@@ -91,24 +92,31 @@ class StageTimer:
         return {n: sum(v) / len(v) for n, v in out.items()}
 
 
-def run_step(L, d, ev=None):
-    """One full step; `ev` is a list of (start, end) event pairs, one per stage."""
+def run_step(L, d, ev=None, ckpt=None):
+    """One full step; `ev` is a list of (start, end) event pairs, one per stage.  With `ckpt`
+    (buffers "aq", "as"), F3 also writes the FP8 checkpoint of A and B3 reads A from it."""
     from paper_2511_02302_amd import ff8
 
     b, dm = L.buf, L.d
     off = b["offsets"]
+    if ckpt is None:
+        f3 = lambda: ff8.ff8_swiglu_quant(b["a"], b["hq"], b["hs"], off, dm.E)
+        b3 = lambda: ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, dm.E)
+    else:
+        f3 = lambda: ff8.ff8_swiglu_quant_keep_fp8(b["a"], b["hq"], b["hs"], ckpt["aq"], ckpt["as"], off, dm.E)
+        b3 = lambda: ff8.ff8_swiglu_bwd_quant_fp8a(ckpt["aq"], ckpt["as"], b["dh"], b["daq"], b["das"], off, dm.E)
     stages = [
         lambda: L.quantize_weights(d["w1"], d["w2"]),
         lambda: ff8.ff8_permute_quant(d["x"], None, dm.k, dm.E, d["topk_idx"], False, b["row_map"], off,
                                       b["src_row"], b["xq"], b["xs"], b["ws"]),
         lambda: ff8.ff8_grouped_gemm_fprop(b["xq"], b["xs"], b["w1q"], b["w1s"], off, b["a"]),
-        lambda: ff8.ff8_swiglu_quant(b["a"], b["hq"], b["hs"], off, dm.E),
+        f3,
         lambda: ff8.ff8_grouped_gemm_fprop(b["hq"], b["hs"], b["w2q"], b["w2s"], off, b["y_perm"]),
         lambda: ff8.ff8_unpermute(b["y_perm"], b["row_map"], d["probs"], b["y"]),
         lambda: ff8.ff8_permute_quant(d["dy"], d["probs"], dm.k, dm.E, None, True, b["row_map"], off,
                                       b["src_row"], b["dyq"], b["dys"]),
         lambda: ff8.ff8_grouped_gemm_dgrad(b["dyq"], b["dys"], b["w2q"], b["w2s"], off, b["dh"]),
-        lambda: ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, dm.E),
+        b3,
         lambda: ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"]),
         lambda: ff8.ff8_unpermute(b["dx_perm"], b["row_map"], None, b["dx"]),
         lambda: [ff8.ff8_scaling_aware_transpose(b[n + "q"], b[n + "s"], b[n + "Tq"], b[n + "Ts"], off, dm.E)
@@ -122,6 +130,44 @@ def run_step(L, d, ev=None):
         fn()
         if ev is not None:
             ev[i][1].record()
+
+
+def fp8_checkpoint(torch, L, d, shape, M, steps, warmup, ms_bf16_a):
+    """The step with A kept as an FP8 checkpoint (F3 writes it, B3 reads it), and the bytes of
+    activations the forward keeps for the backward under three recipes (M_cap-row buffers):
+    all BF16 (permuted X, A, H), FP8-Flow with BF16 A, FP8-Flow with the FP8 checkpoint."""
+    Mc, H, I = L.M_cap, shape.H, shape.I
+    ck = {"aq": torch.empty((Mc, 2 * I), dtype=torch.uint8, device="cuda"),
+          "as": torch.empty((Mc, 2 * I // 128), dtype=torch.float32, device="cuda")}
+    for _ in range(warmup):
+        run_step(L, d, ckpt=ck)
+    torch.cuda.synchronize()
+    names = list(stage_costs(shape, M))
+    timer = StageTimer(torch, names, steps)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run_step(L, d, timer.ev[i], ckpt=ck)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    st = timer.ms()
+    sc = lambda n: 4 * n // 128
+    f3_bytes = M * 2 * I * 2 + M * I + sc(M * I) + M * 2 * I + sc(M * 2 * I)
+    b3_bytes = M * 2 * I + sc(M * 2 * I) + M * I * 2 + M * 2 * I + sc(M * 2 * I)
+    out = {}
+    for name, stage, by in (("F3_swiglu_quant_keep_fp8", "F3_swiglu_quant", f3_bytes),
+                            ("B3_swiglu_bwd_quant_fp8a", "B3_swiglu_bwd_quant", b3_bytes)):
+        gbs = by / (st[stage] * 1e-3) / 1e9
+        out[name] = {"ms": round(st[stage], 4), "GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 3)}
+    fp8_xh = Mc * H + sc(Mc * H) + Mc * I + sc(Mc * I)
+    saved = {"bf16_recipe": Mc * (H + 2 * I + I) * 2, "fp8_flow_bf16_a": fp8_xh + Mc * 2 * I * 2,
+             "fp8_flow_fp8_checkpoint": fp8_xh + Mc * 2 * I + sc(Mc * 2 * I)}
+    assert saved["fp8_flow_bf16_a"] == L.saved_activation_bytes()  # the layer's own buffers
+    out.update({"ms_per_step": round(ms_step, 4), "ms_per_step_bf16_a": round(ms_bf16_a, 4),
+                "saved_activation_bytes": saved,
+                "saving_vs_bf16_a": round(1 - saved["fp8_flow_fp8_checkpoint"] / saved["fp8_flow_bf16_a"], 4),
+                "saving_vs_bf16_recipe": round(1 - saved["fp8_flow_fp8_checkpoint"] / saved["bf16_recipe"], 4)})
+    del ck
+    return out
 
 
 def cast_ops(torch, reps=20):
@@ -347,6 +393,8 @@ def main():
         "roofline": roof,
         "stages": stages,
     }
+    if not args.no_fp8_checkpoint:
+        rec["fp8_checkpoint"] = fp8_checkpoint(torch, L, d, shape, M, args.steps, args.warmup, ms_step)
     if not args.no_cast_ops:
         del L, d
         torch.cuda.empty_cache()

@@ -208,6 +208,27 @@ int ff8_swiglu_bwd_quant(const ff8_bf16* a, const ff8_bf16* dh, const int32_t* o
                          int64_t I, ff8_e4m3* daq, float* das, void* stream);
 
 /*
+ * ff8_swiglu_quant_keep_fp8 -- ff8_swiglu_quant that also keeps an FP8 checkpoint of
+ *   its input for the backward (paper section 4.2: the activations saved for the
+ *   backward are stored in FP8 instead of BF16, which is where the method's peak
+ *   memory saving comes from).  hq, hs as ff8_swiglu_quant; in addition
+ *   a_q [M_cap, 2I] e4m3 + a_s [M_cap, 2I/128] = a quantized 1x128 (gate tiles, then
+ *   up tiles), bit-identical to ff8_quant_rowwise on the active rows.  Once it has
+ *   run, the BF16 a is no longer needed.  Rows >= offsets[E] untouched.
+ */
+int ff8_swiglu_quant_keep_fp8(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                              ff8_e4m3* hq, float* hs, ff8_e4m3* a_q, float* a_s, void* stream);
+
+/*
+ * ff8_swiglu_bwd_quant_fp8a -- ff8_swiglu_bwd_quant reading A from its FP8 checkpoint:
+ *   g, u = a_q * a_s (exact in float32), then the same dg, du and 1x128 quantization.
+ *   a_q [M_cap, 2I] e4m3 + a_s [M_cap, 2I/128] as written by ff8_swiglu_quant_keep_fp8;
+ *   dh [M_cap, I] bf16; daq [M_cap, 2I] e4m3 + das [M_cap, 2I/128].
+ */
+int ff8_swiglu_bwd_quant_fp8a(const ff8_e4m3* a_q, const float* a_s, const ff8_bf16* dh, const int32_t* offsets,
+                              int E, int64_t M_cap, int64_t I, ff8_e4m3* daq, float* das, void* stream);
+
+/*
  * ff8_unpermute -- fused unpermute + unpadding (paper section 3.3.1):
  *   y[t] = sum_{j < k, row_map[t,j] >= 0} w[t, j] * y_perm[row_map[t, j]],
  *   accumulated in float32 in slot order, rounded once to bf16; w = 1 when

@@ -19,6 +19,10 @@ Steps (names used by the tests and the benchmark):
 
 GEMM outputs that the dataflow keeps in BF16 are rounded to bf16 here as well,
 so that the next stage sees the same kind of operand as on the device.
+
+fp8_checkpoint=True keeps A for the backward as its 1x128 FP8 quantization (the
+activations saved for the backward stored in FP8, section 4.2): F3 also returns
+aq, as, and B3 takes A = D(aq).
 """
 
 import numpy as np
@@ -40,7 +44,7 @@ def quantize_weights(w1, w2):
     return out
 
 
-def forward(x, topk_idx, probs, w1q, w1s, w2q, w2s, E):
+def forward(x, topk_idx, probs, w1q, w1s, w2q, w2s, E, fp8_checkpoint=False):
     """F1..F5.  Returns a dict of every intermediate (numpy arrays)."""
     T, k = topk_idx.shape
     st = {}
@@ -48,7 +52,10 @@ def forward(x, topk_idx, probs, w1q, w1s, w2q, w2s, E):
     st.update(counts=counts, offsets=offsets, row_map=row_map, src_row=src_row)
     st["xq"], st["xs"] = moe.permute_quant_rows(x, src_row, k)
     st["a"] = bf16_round(moe.grouped_gemm_fprop(st["xq"], st["xs"], w1q, w1s, offsets))
-    st["hq"], st["hs"] = moe.swiglu_quant(st["a"])
+    if fp8_checkpoint:
+        st["hq"], st["hs"], st["aq"], st["as"] = moe.swiglu_quant_keep(st["a"])
+    else:
+        st["hq"], st["hs"] = moe.swiglu_quant(st["a"])
     st["y_perm"] = bf16_round(moe.grouped_gemm_fprop(st["hq"], st["hs"], w2q, w2s, offsets))
     st["y"] = moe.unpermute(st["y_perm"], row_map, probs)
     return st
@@ -61,7 +68,10 @@ def backward(st, dy, probs, w1q, w1s, w2q, w2s):
     bw = {}
     bw["dyq"], bw["dys"] = moe.permute_quant_rows(dy, st["src_row"], k, row_w=probs)
     bw["dh"] = bf16_round(moe.grouped_gemm_dgrad(bw["dyq"], bw["dys"], w2q, w2s, offsets))
-    bw["daq"], bw["das"] = moe.swiglu_bwd_quant(st["a"], bw["dh"])
+    if "aq" in st:
+        bw["daq"], bw["das"] = moe.swiglu_bwd_quant_from_checkpoint(st["aq"], st["as"], bw["dh"])
+    else:
+        bw["daq"], bw["das"] = moe.swiglu_bwd_quant(st["a"], bw["dh"])
     bw["dx_perm"] = bf16_round(moe.grouped_gemm_dgrad(bw["daq"], bw["das"], w1q, w1s, offsets))
     bw["dx"] = moe.unpermute(bw["dx_perm"], st["row_map"], None)
     for name, (q, s) in (("x", (st["xq"], st["xs"])), ("h", (st["hq"], st["hs"])),

@@ -157,6 +157,20 @@ def swiglu_bwd_quant(a, dh):
     return quant_rowwise(swiglu_bwd(a, dh))
 
 
+def swiglu_quant_keep(a):
+    """Fused SwiGLU + quantization that also keeps A, the fc1 output, as an FP8 checkpoint for
+    the backward (section 4.2: activations saved for the backward are stored in FP8 rather
+    than BF16).  Returns hq, hs and the 1x128 quantization aq, as of A itself."""
+    hq, hs = swiglu_quant(a)
+    aq, a_s = quant_rowwise(a)
+    return hq, hs, aq, a_s
+
+
+def swiglu_bwd_quant_from_checkpoint(aq, a_s, dh):
+    """SwiGLU backward + quantization with A taken from its FP8 checkpoint: A = D(aq), exact."""
+    return swiglu_bwd_quant(dequant_rowwise(aq, a_s), dh)
+
+
 def unpermute(y_perm, row_map, row_w=None):
     """y[t] = sum_j w[t, j] * y_perm[row_map[t, j]] (float64, dropped slots skipped), then bf16 rounding."""
     y_perm = np.asarray(y_perm, dtype=np.float64)

@@ -202,6 +202,26 @@ int ff8_swiglu_bwd_quant(const ff8_bf16* a, const ff8_bf16* dh, const int32_t* o
                     __func__);
 }
 
+int ff8_swiglu_quant_keep_fp8(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                              ff8_e4m3* hq, float* hs, ff8_e4m3* a_q, float* a_s, void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(hq); REQUIRE_PTR(hs); REQUIRE_PTR(a_q); REQUIRE_PTR(a_s);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_quant_keep_fp8(a, offsets, E, M_cap, I, hq, hs, a_q, a_s, as_stream(stream)),
+                    __func__);
+}
+
+int ff8_swiglu_bwd_quant_fp8a(const ff8_e4m3* a_q, const float* a_s, const ff8_bf16* dh, const int32_t* offsets,
+                              int E, int64_t M_cap, int64_t I, ff8_e4m3* daq, float* das, void* stream) {
+  REQUIRE_PTR(a_q); REQUIRE_PTR(a_s); REQUIRE_PTR(dh); REQUIRE_PTR(daq); REQUIRE_PTR(das);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(
+      ff8::launch_swiglu_bwd_quant_fp8a(a_q, a_s, dh, offsets, E, M_cap, I, daq, das, as_stream(stream)), __func__);
+}
+
 int ff8_unpermute(const ff8_bf16* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k, int64_t H,
                   int64_t M_cap, ff8_bf16* y, void* stream) {
   REQUIRE_ARG(k >= 1);

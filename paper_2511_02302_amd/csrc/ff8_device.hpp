@@ -123,6 +123,29 @@ __device__ __forceinline__ u32x2 quant8_tile16(const float* v, int& t_out) {
   return r;
 }
 
+// Max of non-negative float bit patterns across aligned groups of 8 lanes (DPP).
+__device__ __forceinline__ uint32_t max8_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+  return v;
+}
+// 16 values of one 1x128 tile shared by 8 consecutive lanes -> 16 e4m3 bytes and the
+// tile's scale exponent.
+__device__ __forceinline__ u32x4 quant16_tile8(const float* v, int& t_out) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) m = max(m, abs_bits(v[i]));
+  m = max8_u32(m);
+  const int t = scale_exponent(__uint_as_float(m));
+  const float inv = exp2i(-t);
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = cvt_e4m3x4(v[4 * i] * inv, v[4 * i + 1] * inv, v[4 * i + 2] * inv, v[4 * i + 3] * inv);
+  t_out = t;
+  return r;
+}
+
 // Rows of the grouped tensor that hold data: offsets[E] when offsets are given.
 __device__ __forceinline__ int64_t active_rows(const int32_t* offsets, int E, int64_t rows) {
   if (offsets == nullptr) return rows;

@@ -35,6 +35,10 @@ hipError_t launch_swiglu_quant(const uint16_t* a, const int32_t* offsets, int E,
                                uint8_t* hq, float* hs, hipStream_t st);
 hipError_t launch_swiglu_bwd_quant(const uint16_t* a, const uint16_t* dh, const int32_t* offsets, int E,
                                    int64_t M_cap, int64_t I, uint8_t* daq, float* das, hipStream_t st);
+hipError_t launch_swiglu_quant_keep_fp8(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                                        uint8_t* hq, float* hs, uint8_t* aq, float* as_, hipStream_t st);
+hipError_t launch_swiglu_bwd_quant_fp8a(const uint8_t* aq, const float* as_, const uint16_t* dh, const int32_t* offsets,
+                                        int E, int64_t M_cap, int64_t I, uint8_t* daq, float* das, hipStream_t st);
 hipError_t launch_swiglu_bf16(const uint16_t* a, const int32_t* offsets, int E, int64_t rows, int64_t I,
                               uint16_t* h, hipStream_t st);
 

@@ -136,27 +136,6 @@ __global__ __launch_bounds__(64) void route_assign_kernel(const int32_t* __restr
 // lanes one 128-element tile (8-lane DPP amax).  The token's k destination rows and
 // weights are workgroup-uniform (scalar loads); every copy is one 16-byte store per lane,
 // so a wave writes 1 KB contiguous of one destination row.
-__device__ __forceinline__ uint32_t max8_u32(uint32_t v) {
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
-  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
-  return v;
-}
-// 16 values of one tile shared by 8 consecutive lanes -> 16 e4m3 bytes and the exponent.
-__device__ __forceinline__ u32x4 quant16_tile8(const float* v, int& t_out) {
-  uint32_t m = 0;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) m = max(m, abs_bits(v[i]));
-  m = max8_u32(m);
-  const int t = scale_exponent(__uint_as_float(m));
-  const float inv = exp2i(-t);
-  u32x4 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) r[i] = cvt_e4m3x4(v[4 * i] * inv, v[4 * i + 1] * inv, v[4 * i + 2] * inv, v[4 * i + 3] * inv);
-  t_out = t;
-  return r;
-}
-
 template <bool kWeighted>
 __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uint16_t* __restrict__ x,
                                                                        const float* __restrict__ row_w, int64_t H,

@@ -1,9 +1,14 @@
 // Fused SwiGLU + quantization (paper section 3.3.2) and its backward twin, for gfx950.
 //
-// The fc1 output A [rows, 2I] is [gate | up].  Work item (m, c) covers 8 output
-// columns of row m; 16 consecutive items form one 1x128 output tile, so the tile amax
-// is a 16-lane DPP reduction and the activation goes from float32 registers straight
-// to e4m3 without a bf16 round trip.  Rows at and beyond offsets[E] are skipped.
+// The fc1 output A [rows, 2I] is [gate | up].  Work item (m, c) covers 8 or 16 output
+// columns of row m; the items of one 1x128 output tile are consecutive lanes, so the tile
+// amax is a DPP reduction and the activation goes from float32 registers straight to
+// e4m3 without a bf16 round trip.  Rows at and beyond offsets[E] are skipped.
+//
+// FP8 checkpoint (the paper's experiments keep the activations saved for the backward in
+// FP8 instead of BF16): the forward kernel can also emit A itself quantized 1x128
+// (gate and up tiles, from the same registers), and the backward kernel can read that
+// FP8 copy in place of the BF16 A, dequantizing it exactly in float32.
 
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
@@ -16,28 +21,57 @@ constexpr int kThreads = 256;
 
 __device__ __forceinline__ float sigmoid(float g) { return __frcp_rn(1.0f + __expf(-g)); }
 
-// One item per thread, no grid-stride loop.  Holding several items per thread issues
-// more loads up front but measured slower inside the layer step, where A was just
-// written by the fc1 GEMM.
+// Decode 16 e4m3 bytes times a power-of-two scale (exact in float32).
+__device__ __forceinline__ void dequant16(const u32x4& w, float s, float* v) {
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const f32x2 lo = dec_e4m3x2<false>(w[h]), hi = dec_e4m3x2<true>(w[h]);
+    v[4 * h + 0] = lo[0] * s;
+    v[4 * h + 1] = lo[1] * s;
+    v[4 * h + 2] = hi[0] * s;
+    v[4 * h + 3] = hi[1] * s;
+  }
+}
+
+// Forward: lane c covers 16 output columns (two 16-byte loads each of gate and up), 8
+// lanes one 1x128 tile, one 16-byte store per lane; one item per thread, no grid-stride
+// loop.  (16 columns per lane measured faster than 8 here, and slower in the backward.)
+// kKeepA: also write A as 1x128 FP8 (aq [rows, 2I], as_ [rows, 2I/128]).
+template <bool kKeepA>
 __global__ __launch_bounds__(kThreads) void swiglu_quant_kernel(const uint16_t* __restrict__ a,
                                                                 const int32_t* __restrict__ offsets, int E,
                                                                 int64_t M_cap, int64_t I, uint8_t* __restrict__ hq,
-                                                                float* __restrict__ hs) {
+                                                                float* __restrict__ hs, uint8_t* __restrict__ aq,
+                                                                float* __restrict__ as_) {
   const int64_t rows = active_rows(offsets, E, M_cap);
-  const int64_t cpr = I / 8, n_items = rows * cpr, sh = I / kTile;
+  const int64_t cpr = I / 16, n_items = rows * cpr, sh = I / kTile;
   const int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (it >= n_items) return;  // whole 16-lane tiles (cpr is a multiple of 16)
+  if (it >= n_items) return;  // whole 8-lane tiles (cpr is a multiple of 8)
   const int64_t m = it / cpr, c = it - m * cpr;
-  const uint16_t* row = a + m * 2 * I + c * 8;
-  float g[8], u[8], h[8];
-  unpack_bf16x8(ldnt16(row), g);
-  unpack_bf16x8(ldnt16(row + I), u);
+  const uint16_t* row = a + m * 2 * I + c * 16;
+  const u32x4 g0 = ldnt16(row), g1 = ldnt16(row + 8), u0 = ldnt16(row + I), u1 = ldnt16(row + I + 8);
+  float g[16], u[16], h[16];
+  unpack_bf16x8(g0, g);
+  unpack_bf16x8(g1, g + 8);
+  unpack_bf16x8(u0, u);
+  unpack_bf16x8(u1, u + 8);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) h[i] = g[i] * sigmoid(g[i]) * u[i];
+  for (int i = 0; i < 16; ++i) h[i] = g[i] * sigmoid(g[i]) * u[i];
   int t;
-  const u32x2 r = quant8_tile16(h, t);
-  stnt8(hq + m * I + c * 8, r);
-  if ((threadIdx.x & 15) == 0) hs[m * sh + (c >> 4)] = exp2i(t);
+  const u32x4 r = quant16_tile8(h, t);
+  stnt16(hq + m * I + c * 16, r);
+  if ((threadIdx.x & 7) == 0) hs[m * sh + (c >> 3)] = exp2i(t);
+  if (kKeepA) {
+    int tg, tu;
+    const u32x4 rg = quant16_tile8(g, tg);
+    const u32x4 ru = quant16_tile8(u, tu);
+    stnt16(aq + m * 2 * I + c * 16, rg);
+    stnt16(aq + m * 2 * I + I + c * 16, ru);
+    if ((threadIdx.x & 7) == 0) {
+      as_[m * 2 * sh + (c >> 3)] = exp2i(tg);
+      as_[m * 2 * sh + sh + (c >> 3)] = exp2i(tu);
+    }
+  }
 }
 
 // Backward: the same layout, three 16-byte loads per lane.
@@ -76,6 +110,48 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_kernel(const uint16
   }
 }
 
+// Backward from the FP8 checkpoint of A: lane c covers 16 columns (16-byte loads of the
+// gate and up codes, two of dH), 8 lanes one 1x128 tile of each half of the output.
+__global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_fp8a_kernel(const uint8_t* __restrict__ aq,
+                                                                         const float* __restrict__ as_,
+                                                                         const uint16_t* __restrict__ dh,
+                                                                         const int32_t* __restrict__ offsets, int E,
+                                                                         int64_t M_cap, int64_t I,
+                                                                         uint8_t* __restrict__ daq,
+                                                                         float* __restrict__ das) {
+  const int64_t rows = active_rows(offsets, E, M_cap);
+  const int64_t cpr = I / 16, n_items = rows * cpr, sh = 2 * I / kTile;
+  const int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (it >= n_items) return;  // whole 8-lane tiles (cpr is a multiple of 8)
+  const int64_t m = it / cpr, c = it - m * cpr;
+  const uint8_t* row = aq + m * 2 * I + c * 16;
+  const float* srow = as_ + m * sh;  // gate tiles, then up tiles
+  const u32x4 qg = ldnt16(row), qu = ldnt16(row + I);
+  const u32x4 d0 = ldnt16(dh + m * I + c * 16), d1 = ldnt16(dh + m * I + c * 16 + 8);
+  float g[16], u[16], d[16], dg[16], du[16];
+  dequant16(qg, srow[c >> 3], g);
+  dequant16(qu, srow[I / kTile + (c >> 3)], u);
+  unpack_bf16x8(d0, d);
+  unpack_bf16x8(d1, d + 8);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float sg = sigmoid(g[i]);
+    const float gs = g[i] * sg;  // silu(g)
+    du[i] = d[i] * gs;
+    dg[i] = d[i] * u[i] * sg * (1.0f + g[i] * (1.0f - sg));
+  }
+  int tg, tu;
+  const u32x4 rg = quant16_tile8(dg, tg);
+  const u32x4 ru = quant16_tile8(du, tu);
+  uint8_t* out = daq + m * 2 * I + c * 16;
+  stnt16(out, rg);
+  stnt16(out + I, ru);
+  if ((threadIdx.x & 7) == 0) {
+    das[m * sh + (c >> 3)] = exp2i(tg);
+    das[m * sh + I / kTile + (c >> 3)] = exp2i(tu);
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void swiglu_bf16_kernel(const uint16_t* __restrict__ a,
                                                                const int32_t* __restrict__ offsets, int E,
                                                                int64_t n_rows, int64_t I, uint16_t* __restrict__ h) {
@@ -109,9 +185,17 @@ int grid_for(int64_t items) {
 
 hipError_t launch_swiglu_quant(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
                                uint8_t* hq, float* hs, hipStream_t st) {
-  const int64_t items = M_cap * (I / 8);
-  swiglu_quant_kernel<<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(a, offsets, E, M_cap, I, hq,
-                                                                                        hs);
+  const int64_t items = M_cap * (I / 16);
+  swiglu_quant_kernel<false><<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+      a, offsets, E, M_cap, I, hq, hs, nullptr, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_quant_keep_fp8(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                                        uint8_t* hq, float* hs, uint8_t* aq, float* as_, hipStream_t st) {
+  const int64_t items = M_cap * (I / 16);
+  swiglu_quant_kernel<true><<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+      a, offsets, E, M_cap, I, hq, hs, aq, as_);
   return hipGetLastError();
 }
 
@@ -120,6 +204,14 @@ hipError_t launch_swiglu_bwd_quant(const uint16_t* a, const uint16_t* dh, const 
   const int64_t items = M_cap * (I / 8);
   swiglu_bwd_quant_kernel<<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(a, dh, offsets, E, M_cap,
                                                                                              I, daq, das);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_bwd_quant_fp8a(const uint8_t* aq, const float* as_, const uint16_t* dh, const int32_t* offsets,
+                                        int E, int64_t M_cap, int64_t I, uint8_t* daq, float* das, hipStream_t st) {
+  const int64_t items = M_cap * (I / 16);
+  swiglu_bwd_quant_fp8a_kernel<<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+      aq, as_, dh, offsets, E, M_cap, I, daq, das);
   return hipGetLastError();
 }
 

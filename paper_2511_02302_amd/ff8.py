@@ -39,6 +39,10 @@ _SIGNATURES = {
                                         _c_int, _c_vp]),
     "ff8_swiglu_quant": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
     "ff8_swiglu_bwd_quant": (_c_int, [_c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_swiglu_quant_keep_fp8": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp, _c_vp,
+                                           _c_vp]),
+    "ff8_swiglu_bwd_quant_fp8a": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp,
+                                           _c_vp]),
     "ff8_unpermute": (_c_int, [_c_vp, _c_vp, _c_vp, _c_i64, _c_int, _c_i64, _c_i64, _c_vp, _c_vp]),
     "ff8_cast_f32_to_e4m3": (_c_int, [_c_vp, _c_i64, _c_vp, _c_vp]),
     "ff8_cast_e4m3_to_f32": (_c_int, [_c_vp, _c_i64, _c_vp, _c_vp]),
@@ -189,6 +193,21 @@ def ff8_swiglu_bwd_quant(a, dh, daq, das, offsets=None, E=0, stream=None):
     _check(load().ff8_swiglu_bwd_quant(_ptr(a, _bf16, "a", 2), _ptr(dh, _bf16, "dh", 2),
                                        _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2, _ptr(daq, _u8, "daq", 2),
                                        _ptr(das, _f32, "das", 2), _stream(stream)), "ff8_swiglu_bwd_quant")
+
+
+def ff8_swiglu_quant_keep_fp8(a, hq, hs, a_q, a_s, offsets=None, E=0, stream=None):
+    M_cap, I2 = a.shape
+    _check(load().ff8_swiglu_quant_keep_fp8(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
+                                            _ptr(hq, _u8, "hq", 2), _ptr(hs, _f32, "hs", 2), _ptr(a_q, _u8, "a_q", 2),
+                                            _ptr(a_s, _f32, "a_s", 2), _stream(stream)), "ff8_swiglu_quant_keep_fp8")
+
+
+def ff8_swiglu_bwd_quant_fp8a(a_q, a_s, dh, daq, das, offsets=None, E=0, stream=None):
+    M_cap, I2 = a_q.shape
+    _check(load().ff8_swiglu_bwd_quant_fp8a(_ptr(a_q, _u8, "a_q", 2), _ptr(a_s, _f32, "a_s", 2),
+                                            _ptr(dh, _bf16, "dh", 2), _ptr(offsets, _i32, "offsets"), E, M_cap,
+                                            I2 // 2, _ptr(daq, _u8, "daq", 2), _ptr(das, _f32, "das", 2),
+                                            _stream(stream)), "ff8_swiglu_bwd_quant_fp8a")
 
 
 def ff8_unpermute(y_perm, row_map, row_w, y, stream=None):

@@ -10,6 +10,11 @@ BF16 stays only at the fc1 output (feeding the activation) and at the fc2 output
 Every step is one or more calls into libff8.so through the ctypes binding; torch
 only provides device memory (all buffers are allocated once, in __init__) and the
 stream.
+
+With fp8_checkpoint=True the forward also keeps A, the fc1 output, as a 1x128 FP8
+checkpoint, and the backward reads A from it: the BF16 A is then only needed between
+fc1 and the activation (the paper stores the activations saved for the backward in
+FP8, section 4.2).
 """
 
 from dataclasses import dataclass
@@ -39,8 +44,9 @@ def _empty(shape, dtype, device):
 class ExpertLayerFP8:
     """Buffers and step sequence of one expert layer (E local experts, top-k routing)."""
 
-    def __init__(self, T, H, E, k, I, device="cuda"):
+    def __init__(self, T, H, E, k, I, device="cuda", fp8_checkpoint=False):
         self.d = d = Dims(T, H, E, k, I)
+        self.fp8_checkpoint = fp8_checkpoint
         self.device = dev = torch.device(device)
         M = self.M_cap = d.m_cap
         u8, f32, bf16, i32 = torch.uint8, torch.float32, torch.bfloat16, torch.int32
@@ -61,6 +67,9 @@ class ExpertLayerFP8:
         b["a"] = _empty((M, 2 * I), bf16, dev)
         b["hq"] = _empty((M, I), u8, dev)
         b["hs"] = _empty((M, I // 128), f32, dev)
+        if fp8_checkpoint:
+            b["aq"] = _empty((M, 2 * I), u8, dev)
+            b["as"] = _empty((M, 2 * I // 128), f32, dev)
         b["y_perm"] = _empty((M, H), bf16, dev)
         b["y"] = _empty((T, H), bf16, dev)
         # backward
@@ -89,7 +98,10 @@ class ExpertLayerFP8:
         ff8.ff8_permute_quant(x, None, d.k, d.E, topk_idx, False, b["row_map"], b["offsets"], b["src_row"],
                               b["xq"], b["xs"], b["ws"])
         ff8.ff8_grouped_gemm_fprop(b["xq"], b["xs"], b["w1q"], b["w1s"], b["offsets"], b["a"])
-        ff8.ff8_swiglu_quant(b["a"], b["hq"], b["hs"], b["offsets"], d.E)
+        if self.fp8_checkpoint:
+            ff8.ff8_swiglu_quant_keep_fp8(b["a"], b["hq"], b["hs"], b["aq"], b["as"], b["offsets"], d.E)
+        else:
+            ff8.ff8_swiglu_quant(b["a"], b["hq"], b["hs"], b["offsets"], d.E)
         ff8.ff8_grouped_gemm_fprop(b["hq"], b["hs"], b["w2q"], b["w2s"], b["offsets"], b["y_perm"])
         ff8.ff8_unpermute(b["y_perm"], b["row_map"], probs, b["y"])
         return b["y"]
@@ -100,7 +112,10 @@ class ExpertLayerFP8:
         off = b["offsets"]
         ff8.ff8_permute_quant(dy, probs, d.k, d.E, None, True, b["row_map"], off, b["src_row"], b["dyq"], b["dys"])
         ff8.ff8_grouped_gemm_dgrad(b["dyq"], b["dys"], b["w2q"], b["w2s"], off, b["dh"])
-        ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, d.E)
+        if self.fp8_checkpoint:
+            ff8.ff8_swiglu_bwd_quant_fp8a(b["aq"], b["as"], b["dh"], b["daq"], b["das"], off, d.E)
+        else:
+            ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, d.E)
         ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"])
         ff8.ff8_unpermute(b["dx_perm"], b["row_map"], None, b["dx"])
         for name in ("x", "h", "dy", "da"):
@@ -108,6 +123,14 @@ class ExpertLayerFP8:
         ff8.ff8_grouped_gemm_wgrad(b["dyTq"], b["dyTs"], b["hTq"], b["hTs"], off, b["dw2"])
         ff8.ff8_grouped_gemm_wgrad(b["daTq"], b["daTs"], b["xTq"], b["xTs"], off, b["dw1"])
         return b["dx"], b["dw1"], b["dw2"]
+
+    def saved_activation_bytes(self):
+        """Bytes of the expert-path activations the forward keeps for the backward: the
+        row-wise FP8 X and H (inputs of the weight gradients) and A (the SwiGLU backward's
+        input), as BF16 or as its FP8 checkpoint.  Routing maps are not counted."""
+        b = self.buf
+        names = ["xq", "xs", "hq", "hs"] + (["aq", "as"] if self.fp8_checkpoint else ["a"])
+        return sum(b[n].numel() * b[n].element_size() for n in names)
 
     def step(self, x, topk_idx, probs, dy, w1, w2):
         """One pass of the whole hot path: F0, F1..F5, B1..B8."""

@@ -12,6 +12,7 @@ import torch
 
 import workloads
 from oracle import codec, quant, sat, moe
+from paper_2511_02302_amd import ff8
 from paper_2511_02302_amd.layer import ExpertLayerFP8
 
 from test_gpu_kernels import f64, host, rel_frob
@@ -189,6 +190,34 @@ def test_swiglu_fwd_bwd_sampled_rows(run):
     da = moe.swiglu_bwd(a64, dh64)
     wq, ws = quant.quant_rowwise(da)
     _swiglu_check(_rows(b["daq"], m), _rows(b["das"], m), wq, ws, da, b_bwd)
+
+
+def test_fp8_checkpoint_sampled_rows(run):
+    """F3 with the FP8 checkpoint of A and B3 reading it, on the step's own A and dH: H equal
+    to the step's, the checkpoint bit-exact and dA against the oracle at sampled rows."""
+    shape, b = run["shape"], run["b"]
+    M_cap, I2 = b["a"].shape
+    m_pad = int(run["off"][-1])
+    u8, f32 = torch.uint8, torch.float32
+    hq, hs = torch.empty((M_cap, I2 // 2), dtype=u8, device="cuda"), torch.empty((M_cap, I2 // 256), dtype=f32,
+                                                                                    device="cuda")
+    aq, a_s = torch.empty((M_cap, I2), dtype=u8, device="cuda"), torch.empty((M_cap, I2 // 128), dtype=f32,
+                                                                               device="cuda")
+    daq, das = torch.empty_like(aq), torch.empty_like(a_s)
+    ff8.ff8_swiglu_quant_keep_fp8(b["a"], hq, hs, aq, a_s, b["offsets"], shape.E)
+    ff8.ff8_swiglu_bwd_quant_fp8a(aq, a_s, b["dh"], daq, das, b["offsets"], shape.E)
+    torch.cuda.synchronize()
+    assert torch.equal(hq[:m_pad], b["hq"][:m_pad]) and torch.equal(hs[:m_pad], b["hs"][:m_pad])
+    m, _ = _sample_rows(run, 48)
+    a64, dh64 = f64(b["a"].index_select(0, _cuda_idx(m))), f64(b["dh"].index_select(0, _cuda_idx(m)))
+    want_aq, want_as = quant.quant_rowwise(a64)
+    assert np.array_equal(_rows(aq, m), want_aq) and np.array_equal(_rows(a_s, m), want_as)
+    ad = quant.dequant_rowwise(want_aq, want_as)
+    _, b_bwd = _swiglu_bounds(ad, dh64)
+    da = moe.swiglu_bwd(ad, dh64)
+    wq, ws = quant.quant_rowwise(da)
+    _swiglu_check(_rows(daq, m), _rows(das, m), wq, ws, da, b_bwd)
+    del hq, hs, aq, a_s, daq, das
 
 
 def test_unpermute_sampled_tokens(run):

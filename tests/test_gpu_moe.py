@@ -273,6 +273,41 @@ def test_swiglu_fwd_bwd(case):
     assert untouched(daq[m_pad:])
 
 
+@pytest.mark.parametrize("case", list(CASES))
+def test_swiglu_fp8_checkpoint(case):
+    """F3 keeping A as an FP8 checkpoint, and B3 reading A back from it (section 4.2):
+    the checkpoint bit-exact, H and dA against the oracle on the same operands."""
+    shape, inp = _inputs(case)
+    I, E = shape.I, shape.E
+    M_cap = 1024
+    a = workloads.randn_bf16((M_cap, 2 * I), 2.0, seed=8)
+    dh = workloads.randn_bf16((M_cap, I), 1.0, seed=9)
+    offsets = dev(torch.tensor([0, 256, 256, 640, 896][: min(5, E + 1)] + [896] * max(0, E + 1 - 5),
+                               dtype=torch.int32))
+    m_pad = 896
+    hq = poisoned((M_cap, I), torch.uint8)
+    hs = poisoned((M_cap, I // 128), torch.float32)
+    aq = poisoned((M_cap, 2 * I), torch.uint8)
+    a_s = poisoned((M_cap, 2 * I // 128), torch.float32)
+    ff8.ff8_swiglu_quant_keep_fp8(dev(a), hq, hs, aq, a_s, offsets, E)
+    daq = poisoned((M_cap, 2 * I), torch.uint8)
+    das = poisoned((M_cap, 2 * I // 128), torch.float32)
+    ff8.ff8_swiglu_bwd_quant_fp8a(aq, a_s, dev(dh), daq, das, offsets, E)
+    torch.cuda.synchronize()
+    a64, dh64 = f64(a)[:m_pad], f64(dh)[:m_pad]
+    want_hq, want_hs, want_aq, want_as = moe.swiglu_quant_keep(a64)
+    assert np.array_equal(host(aq[:m_pad]), want_aq) and np.array_equal(host(a_s[:m_pad]), want_as)
+    assert untouched(aq[m_pad:]) and untouched(a_s[m_pad:]) and untouched(hq[m_pad:])
+    b_fwd, _ = _swiglu_bounds(a64, dh64)
+    _swiglu_check(host(hq[:m_pad]), host(hs[:m_pad]), want_hq, want_hs, moe.swiglu(a64), b_fwd)
+    ad = quant.dequant_rowwise(want_aq, want_as)
+    _, b_bwd = _swiglu_bounds(ad, dh64)
+    da = moe.swiglu_bwd(ad, dh64)
+    wq, ws = moe.swiglu_bwd_quant_from_checkpoint(want_aq, want_as, dh64)
+    _swiglu_check(host(daq[:m_pad]), host(das[:m_pad]), wq, ws, da, b_bwd)
+    assert untouched(daq[m_pad:]) and untouched(das[m_pad:])
+
+
 @pytest.mark.parametrize("k", [1, 2, 8])
 def test_unpermute(k):
     T, H, E = 500, 256, 8
@@ -296,12 +331,14 @@ def test_unpermute(k):
         assert np.all(np.abs(got - want) <= ulp + 1e-6), np.max(np.abs(got - want) / ulp)
 
 
+@pytest.mark.parametrize("ckpt", [False, True], ids=["bf16_a", "fp8_checkpoint"])
 @pytest.mark.parametrize("case", list(CASES))
-def test_layer_stagewise(case):
+def test_layer_stagewise(case, ckpt):
     """Whole forward+backward through ExpertLayerFP8; every stage is checked against the
-    oracle applied to the GPU's own upstream outputs (no error compounding)."""
+    oracle applied to the GPU's own upstream outputs (no error compounding).  With the FP8
+    checkpoint, A's checkpoint is bit-exact and the SwiGLU backward reads A from it."""
     shape, inp = _inputs(case)
-    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt)
     d = {k: dev(v) for k, v in inp.items()}
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
@@ -330,9 +367,14 @@ def test_layer_stagewise(case):
     dH = moe.grouped_gemm_dgrad(dyq, dys, w["w2q"], w["w2s"], off)
     assert rel_frob(f64(b["dh"][:m_pad]), dH) < GEMM_TOL
     dh_gpu = f64(b["dh"][:m_pad])
-    da = moe.swiglu_bwd(a_gpu, dh_gpu)
+    a_bwd = a_gpu
+    if ckpt:
+        aq, a_s = quant.quant_rowwise(a_gpu)
+        assert np.array_equal(host(b["aq"][:m_pad]), aq) and np.array_equal(host(b["as"][:m_pad]), a_s)
+        a_bwd = quant.dequant_rowwise(aq, a_s)
+    da = moe.swiglu_bwd(a_bwd, dh_gpu)
     daq, das = quant.quant_rowwise(da)
-    _swiglu_check(host(b["daq"][:m_pad]), host(b["das"][:m_pad]), daq, das, da, _swiglu_bounds(a_gpu, dh_gpu)[1])
+    _swiglu_check(host(b["daq"][:m_pad]), host(b["das"][:m_pad]), daq, das, da, _swiglu_bounds(a_bwd, dh_gpu)[1])
     dXp = moe.grouped_gemm_dgrad(host(b["daq"][:m_pad]), host(b["das"][:m_pad]), w["w1q"], w["w1s"], off)
     assert rel_frob(f64(b["dx_perm"][:m_pad]), dXp) < GEMM_TOL
     dx = moe.unpermute(f64(b["dx_perm"][:m_pad]), w_map, None)

@@ -158,6 +158,36 @@ def test_swiglu_vs_torch_autograd():
     assert np.array_equal(hq, q2) and np.array_equal(hs, s2)
 
 
+def test_fp8_checkpoint_of_a():
+    """The FP8 checkpoint of A is the plain 1x128 quantization of A, gate tiles and up tiles
+    each with their own scale: when A is exactly representable (every tile holds a +-448 code
+    times a power of two) it is lossless, and the backward from it equals the backward from A."""
+    rng = np.random.default_rng(8)
+    rows, I = 24, 256
+    codes = rng.integers(0, 256, size=(rows, 2 * I), dtype=np.uint8)
+    codes[(codes & 0x7F) == 0x7F] = 0x00  # no NaN codes
+    codes[:, ::TILE] = 0x7E  # every tile's amax is 448 (code 0x7E)
+    t = rng.integers(-20, 6, size=(rows, 2 * I // TILE))
+    t[:, : I // TILE] = -3  # gate tiles and up tiles on different scales
+    s = np.power(2.0, t)
+    a = e4m3_decode(codes) * np.repeat(s, TILE, axis=1)
+    hq, hs, aq, a_s = moe.swiglu_quant_keep(a)
+    assert np.array_equal(aq, codes) and np.array_equal(a_s, s.astype(np.float32))
+    hq2, hs2 = moe.swiglu_quant(a)
+    assert np.array_equal(hq, hq2) and np.array_equal(hs, hs2)
+    dh = rng.standard_normal((rows, I))
+    dq, ds = moe.swiglu_bwd_quant_from_checkpoint(aq, a_s, dh)
+    dq2, ds2 = moe.swiglu_bwd_quant(a, dh)
+    assert np.array_equal(dq, dq2) and np.array_equal(ds, ds2)
+    # a general A: the gradient from the checkpoint stays within the e4m3 rounding of g and u
+    a = rng.standard_normal((rows, 2 * I)) * 3.0
+    _, _, aq, a_s = moe.swiglu_quant_keep(a)
+    ad = dequant_rowwise(aq, a_s)
+    assert np.all(np.abs(ad - a) <= np.abs(a) * 2.0 ** -4 + 2.0 ** -9 * np.repeat(a_s, TILE, axis=1))
+    g_ref, g_ck = moe.swiglu_bwd(a, dh), moe.swiglu_bwd(ad, dh)
+    assert np.linalg.norm(g_ck - g_ref) / np.linalg.norm(g_ref) < 0.05
+
+
 def test_unpermute_loop_and_gather():
     T, k, E, H = 30, 3, 5, 128
     idx = _routing(T, k, E, 8, drop=0.1)
