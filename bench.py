@@ -48,6 +48,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cast-ops", action="store_true")
     ap.add_argument("--no-fp8-checkpoint", action="store_true")
+    ap.add_argument("--no-router-grad", action="store_true")
     return ap.parse_args()
 
 
@@ -92,9 +93,10 @@ class StageTimer:
         return {n: sum(v) / len(v) for n, v in out.items()}
 
 
-def run_step(L, d, ev=None, ckpt=None):
+def run_step(L, d, ev=None, ckpt=None, dprobs=None):
     """One full step; `ev` is a list of (start, end) event pairs, one per stage.  With `ckpt`
-    (buffers "aq", "as"), F3 also writes the FP8 checkpoint of A and B3 reads A from it."""
+    (buffers "aq", "as"), F3 also writes the FP8 checkpoint of A and B3 reads A from it; with
+    `dprobs` (a [T, k] float32 buffer), B1 also computes the router gradient."""
     from paper_2511_02302_amd import ff8
 
     b, dm = L.buf, L.d
@@ -105,6 +107,12 @@ def run_step(L, d, ev=None, ckpt=None):
     else:
         f3 = lambda: ff8.ff8_swiglu_quant_keep_fp8(b["a"], b["hq"], b["hs"], ckpt["aq"], ckpt["as"], off, dm.E)
         b3 = lambda: ff8.ff8_swiglu_bwd_quant_fp8a(ckpt["aq"], ckpt["as"], b["dh"], b["daq"], b["das"], off, dm.E)
+    if dprobs is None:
+        b1 = lambda: ff8.ff8_permute_quant(d["dy"], d["probs"], dm.k, dm.E, None, True, b["row_map"], off,
+                                           b["src_row"], b["dyq"], b["dys"])
+    else:
+        b1 = lambda: ff8.ff8_permute_quant_dprobs(d["dy"], d["probs"], dm.k, dm.E, b["row_map"], off, b["src_row"],
+                                                  b["dyq"], b["dys"], b["y_perm"], dprobs)
     stages = [
         lambda: L.quantize_weights(d["w1"], d["w2"]),
         lambda: ff8.ff8_permute_quant(d["x"], None, dm.k, dm.E, d["topk_idx"], False, b["row_map"], off,
@@ -113,8 +121,7 @@ def run_step(L, d, ev=None, ckpt=None):
         f3,
         lambda: ff8.ff8_grouped_gemm_fprop(b["hq"], b["hs"], b["w2q"], b["w2s"], off, b["y_perm"]),
         lambda: ff8.ff8_unpermute(b["y_perm"], b["row_map"], d["probs"], b["y"]),
-        lambda: ff8.ff8_permute_quant(d["dy"], d["probs"], dm.k, dm.E, None, True, b["row_map"], off,
-                                      b["src_row"], b["dyq"], b["dys"]),
+        b1,
         lambda: ff8.ff8_grouped_gemm_dgrad(b["dyq"], b["dys"], b["w2q"], b["w2s"], off, b["dh"]),
         b3,
         lambda: ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"]),
@@ -168,6 +175,32 @@ def fp8_checkpoint(torch, L, d, shape, M, steps, warmup, ms_bf16_a):
                 "saving_vs_bf16_recipe": round(1 - saved["fp8_flow_fp8_checkpoint"] / saved["bf16_recipe"], 4)})
     del ck
     return out
+
+
+def router_grad(torch, L, d, shape, M, steps, warmup, ms_base, b1_base_ms):
+    """The step with B1 fused with the router gradient dprobs[t, j] = <dY[t], Y_perm[row]>: its
+    step time and B1's time and rate.  The fused B1 additionally reads the k rows of Y_perm of
+    every token (the dot products) and writes dprobs."""
+    T, H, k = shape.T, shape.H, shape.k
+    dp = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    for _ in range(warmup):
+        run_step(L, d, dprobs=dp)
+    torch.cuda.synchronize()
+    names = list(stage_costs(shape, M))
+    timer = StageTimer(torch, names, steps)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run_step(L, d, timer.ev[i], dprobs=dp)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    st = timer.ms()
+    by = stage_costs(shape, M)["B1_permute_quant_dy"][1] + M * H * 2 + T * k * 4
+    gbs = by / (st["B1_permute_quant_dy"] * 1e-3) / 1e9
+    del dp
+    return {"B1_permute_quant_dprobs": {"ms": round(st["B1_permute_quant_dy"], 4), "GB/s": round(gbs, 1),
+                                        "frac_hbm": round(gbs / HBM_PEAK_GBS, 3), "bytes": by},
+            "B1_without_dprobs_ms": round(b1_base_ms, 4),
+            "ms_per_step": round(ms_step, 4), "ms_per_step_without": round(ms_base, 4)}
 
 
 def cast_ops(torch, reps=20):
@@ -395,6 +428,9 @@ def main():
     }
     if not args.no_fp8_checkpoint:
         rec["fp8_checkpoint"] = fp8_checkpoint(torch, L, d, shape, M, args.steps, args.warmup, ms_step)
+    if not args.no_router_grad:
+        rec["router_grad"] = router_grad(torch, L, d, shape, M, args.steps, args.warmup, ms_step,
+                                         st_ms["B1_permute_quant_dy"])
     if not args.no_cast_ops:
         del L, d
         torch.cuda.empty_cache()

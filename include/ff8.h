@@ -133,6 +133,23 @@ int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t 
                       size_t ws_bytes, void* stream);
 
 /*
+ * ff8_permute_quant_dprobs -- the backward permute of dY (ff8_permute_quant with reuse_map = 1
+ *   and routing weights) fused with the router gradient, the backward of the
+ *   routing-weighted combine y[t] = sum_j row_w[t, j] * y_perm[row_map[t, j]] (paper section
+ *   3.2: the combine and the dispatch sit at the fc2 output, which stays BF16):
+ *     dprobs[t, j] = sum_h dy[t, h] * y_perm[row_map[t, j], h],
+ *   accumulated in float32 (each bf16 x bf16 product is exact), 0 for a dropped slot.
+ *   q, s, padding rows: exactly as ff8_permute_quant (reuse_map = 1) writes them from dy and
+ *   row_w.  row_map, offsets, src_row as written by the forward's ff8_permute_quant.
+ *   y_perm [M_cap, H] bf16 (the fc2 output of the forward); dprobs [T, k] float32.
+ *   Limits: k <= 64 and H <= 8192 (one workgroup holds a token's dy row in registers);
+ *   larger values return FF8_ERR_ARG / FF8_ERR_SHAPE.
+ */
+int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                             const int32_t* row_map, const int32_t* offsets, const int32_t* src_row, int64_t M_cap,
+                             ff8_e4m3* q, float* s, const ff8_bf16* y_perm, float* dprobs, void* stream);
+
+/*
  * ff8_scaling_aware_transpose -- Algorithm 1 of paper section 3.1 (scaling-aware
  * FP8 transpose) with its exponent-shift identity.
  *   q [rows, cols] e4m3 with row-wise scales s [rows, cols/128].

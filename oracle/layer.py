@@ -22,7 +22,8 @@ so that the next stage sees the same kind of operand as on the device.
 
 fp8_checkpoint=True keeps A for the backward as its 1x128 FP8 quantization (the
 activations saved for the backward stored in FP8, section 4.2): F3 also returns
-aq, as, and B3 takes A = D(aq).
+aq, as, and B3 takes A = D(aq).  router_grad=True adds the routing weights' gradient
+dprobs (the backward of the weighted combine) to the backward's outputs.
 """
 
 import numpy as np
@@ -61,12 +62,14 @@ def forward(x, topk_idx, probs, w1q, w1s, w2q, w2s, E, fp8_checkpoint=False):
     return st
 
 
-def backward(st, dy, probs, w1q, w1s, w2q, w2s):
+def backward(st, dy, probs, w1q, w1s, w2q, w2s, router_grad=False):
     """B1..B8 given the forward state.  Returns a dict of every intermediate."""
     k = st["row_map"].shape[1]
     offsets = st["offsets"]
     bw = {}
     bw["dyq"], bw["dys"] = moe.permute_quant_rows(dy, st["src_row"], k, row_w=probs)
+    if router_grad:
+        bw["dprobs"] = moe.router_grad(dy, st["y_perm"], st["row_map"])
     bw["dh"] = bf16_round(moe.grouped_gemm_dgrad(bw["dyq"], bw["dys"], w2q, w2s, offsets))
     if "aq" in st:
         bw["daq"], bw["das"] = moe.swiglu_bwd_quant_from_checkpoint(st["aq"], st["as"], bw["dh"])

@@ -171,6 +171,22 @@ def swiglu_bwd_quant_from_checkpoint(aq, a_s, dh):
     return swiglu_bwd_quant(dequant_rowwise(aq, a_s), dh)
 
 
+def router_grad(dy, y_perm, row_map):
+    """Gradient of the routing weights through the weighted combine y[t] = sum_j w[t, j] *
+    y_perm[row_map[t, j]]: dprobs[t, j] = <dy[t], y_perm[row_map[t, j]]> (float64), 0 for a
+    dropped slot.  The combine's final bf16 rounding is taken as the identity."""
+    dy = np.asarray(dy, dtype=np.float64)
+    y_perm = np.asarray(y_perm, dtype=np.float64)
+    row_map = np.asarray(row_map, dtype=np.int64)
+    T, k = row_map.shape
+    out = np.zeros((T, k), dtype=np.float64)
+    for j in range(k):
+        r = row_map[:, j]
+        ok = r >= 0
+        out[ok, j] = np.einsum("th,th->t", dy[ok], y_perm[r[ok]])
+    return out
+
+
 def unpermute(y_perm, row_map, row_w=None):
     """y[t] = sum_j w[t, j] * y_perm[row_map[t, j]] (float64, dropped slots skipped), then bf16 rounding."""
     y_perm = np.asarray(y_perm, dtype=np.float64)

@@ -128,6 +128,22 @@ int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t 
                     __func__);
 }
 
+int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                             const int32_t* row_map, const int32_t* offsets, const int32_t* src_row, int64_t M_cap,
+                             ff8_e4m3* q, float* s, const ff8_bf16* y_perm, float* dprobs, void* stream) {
+  REQUIRE_ARG(k >= 1 && E >= 1 && k <= E && E <= 1024 && k <= ff8::max_k_dprobs());
+  REQUIRE_SHAPE(T >= 0 && mult128(H) && H <= ff8::max_h_dprobs() && M_cap % 128 == 0);
+  REQUIRE_SHAPE(M_cap >= ff8_rows_bound(T, k, E));
+  REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
+  if (T > 0) {
+    REQUIRE_PTR(dy); REQUIRE_PTR(row_w); REQUIRE_PTR(y_perm); REQUIRE_PTR(dprobs);
+  }
+  REQUIRE_PTR(row_map); REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  return hip_status(ff8::launch_permute_quant_dprobs(dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s,
+                                                     y_perm, dprobs, as_stream(stream)),
+                    __func__);
+}
+
 int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows, int64_t cols,
                                 const int32_t* offsets, int E, ff8_e4m3* qT, float* sT, void* stream) {
   REQUIRE_PTR(q); REQUIRE_PTR(s); REQUIRE_PTR(qT); REQUIRE_PTR(sT);

@@ -28,6 +28,12 @@ hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int32_
 hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                                 const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                 int64_t M_cap, uint8_t* q, float* s, hipStream_t st);
+hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                       const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                       int64_t M_cap, uint8_t* q, float* s, const uint16_t* y_perm, float* dprobs,
+                                       hipStream_t st);
+int max_k_dprobs();
+int64_t max_h_dprobs();
 hipError_t launch_unpermute(const uint16_t* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k,
                             int64_t H, int64_t M_cap, uint16_t* y, hipStream_t st);
 

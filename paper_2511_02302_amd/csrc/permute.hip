@@ -177,6 +177,65 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uin
   }
 }
 
+// B1 with the router gradient (the backward of the routing-weighted combine): besides the
+// weighted, quantized copies of dY[t], dprobs[t, j] = sum_h dY[t, h] * Y_perm[row_map[t, j], h]
+// in float32 (bf16 x bf16 products are exact).  One chunk of 16 columns per lane (H <= 16 *
+// kRowThreadsMax), so dY[t] stays in registers for all k dot products.  Sum order, fixed: the
+// lane's 16 products in column order, a butterfly over the wave, then the waves in order.
+// (Loading 2, 4 or 8 slots' Y_perm rows ahead of their dot products measured no faster: the
+// registers it takes cost occupancy.)
+constexpr int kMaxKDprobs = 64;
+__global__ __launch_bounds__(kRowThreadsMax) void permute_quant_dprobs_kernel(
+    const uint16_t* __restrict__ dy, const float* __restrict__ row_w, int64_t H, int k,
+    const int32_t* __restrict__ row_map, int64_t M_cap, uint8_t* __restrict__ q, float* __restrict__ s,
+    const uint16_t* __restrict__ y_perm, float* __restrict__ dprobs) {
+  __shared__ float part[kMaxKDprobs * (kRowThreadsMax / 64)];
+  const int64_t t = blockIdx.x;
+  const int64_t n16 = H / 16, sh = H / kTile;
+  const int c = threadIdx.x, wave = c >> 6, n_waves = blockDim.x >> 6;
+  const bool act = c < n16;  // uniform per 8-lane tile
+  const bool leader = (c & 7) == 0;
+  float v[16];
+  if (act) {
+    unpack_bf16x8(ldnt16(dy + t * H + c * 16), v);
+    unpack_bf16x8(ldnt16(dy + t * H + c * 16 + 8), v + 8);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = 0.0f;
+  }
+  for (int j = 0; j < k; ++j) {
+    const int row = row_map[t * k + j];
+    const bool ok = row >= 0 && row < M_cap;  // uniform
+    float acc = 0.0f;
+    if (ok && act) {
+      const uint16_t* yp = y_perm + (int64_t)row * H + c * 16;
+      float y[16];
+      unpack_bf16x8(ldnt16(yp), y);
+      unpack_bf16x8(ldnt16(yp + 8), y + 8);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc = fmaf(v[i], y[i], acc);
+      const float w = row_w[t * k + j];
+      float vw[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) vw[i] = w * v[i];
+      int tq;
+      const u32x4 r = quant16_tile8(vw, tq);
+      stnt16(q + (int64_t)row * H + c * 16, r);
+      if (leader) s[(int64_t)row * sh + (c >> 3)] = exp2i(tq);
+    }
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) acc += __shfl_xor(acc, d);
+    if ((c & 63) == 0) part[j * (kRowThreadsMax / 64) + wave] = acc;
+  }
+  __syncthreads();
+  for (int j = c; j < k; j += blockDim.x) {
+    const int row = row_map[t * k + j];
+    float sum = 0.0f;
+    for (int w = 0; w < n_waves; ++w) sum += part[j * (kRowThreadsMax / 64) + w];
+    dprobs[t * k + j] = (row >= 0 && row < M_cap) ? sum : 0.0f;
+  }
+}
+
 // Padding rows (src_row == -1 below offsets[E]): bytes 0x00, scales 2^-126.  Padding
 // only occurs in the last 128-row block of a group; other blocks exit after their reads.
 // kPadSplit workgroups share a block: wave w of part p takes rows p * 4 + w + 32 j, a
@@ -294,6 +353,20 @@ hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T
   pad_fill_kernel<<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
   return hipGetLastError();
 }
+
+hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                       const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                       int64_t M_cap, uint8_t* q, float* s, const uint16_t* y_perm, float* dprobs,
+                                       hipStream_t st) {
+  if (T > 0)
+    permute_quant_dprobs_kernel<<<(unsigned)T, row_threads(H), 0, st>>>(dy, row_w, H, k, row_map, M_cap, q, s, y_perm,
+                                                                       dprobs);
+  pad_fill_kernel<<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
+  return hipGetLastError();
+}
+
+int max_k_dprobs() { return kMaxKDprobs; }
+int64_t max_h_dprobs() { return 16LL * kRowThreadsMax; }
 
 hipError_t launch_unpermute(const uint16_t* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k,
                             int64_t H, int64_t M_cap, uint16_t* y, hipStream_t st) {

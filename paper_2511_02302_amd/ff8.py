@@ -39,6 +39,8 @@ _SIGNATURES = {
                                         _c_int, _c_vp]),
     "ff8_swiglu_quant": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
     "ff8_swiglu_bwd_quant": (_c_int, [_c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_permute_quant_dprobs": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_vp, _c_vp, _c_i64,
+                                          _c_vp, _c_vp, _c_vp, _c_vp, _c_vp]),
     "ff8_swiglu_quant_keep_fp8": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp, _c_vp,
                                            _c_vp]),
     "ff8_swiglu_bwd_quant_fp8a": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp,
@@ -144,6 +146,16 @@ def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src
         _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2),
         None if workspace is None else ctypes.c_void_p(workspace.data_ptr()), ws, _stream(stream)),
         "ff8_permute_quant")
+
+
+def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y_perm, dprobs, stream=None):
+    T, H = dy.shape
+    M_cap = q.shape[0]
+    _check(load().ff8_permute_quant_dprobs(_ptr(dy, _bf16, "dy", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E,
+                                           _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
+                                           _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2),
+                                           _ptr(s, _f32, "s", 2), _ptr(y_perm, _bf16, "y_perm", 2),
+                                           _ptr(dprobs, _f32, "dprobs"), _stream(stream)), "ff8_permute_quant_dprobs")
 
 
 def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):

@@ -15,6 +15,10 @@ With fp8_checkpoint=True the forward also keeps A, the fc1 output, as a 1x128 FP
 checkpoint, and the backward reads A from it: the BF16 A is then only needed between
 fc1 and the activation (the paper stores the activations saved for the backward in
 FP8, section 4.2).
+
+With router_grad=True the backward permute of dY also computes the routing weights'
+gradient, dprobs[t, j] = <dY[t], Y_perm[row_map[t, j]]> (the backward of the weighted
+combine), in the same pass over dY.
 """
 
 from dataclasses import dataclass
@@ -44,9 +48,10 @@ def _empty(shape, dtype, device):
 class ExpertLayerFP8:
     """Buffers and step sequence of one expert layer (E local experts, top-k routing)."""
 
-    def __init__(self, T, H, E, k, I, device="cuda", fp8_checkpoint=False):
+    def __init__(self, T, H, E, k, I, device="cuda", fp8_checkpoint=False, router_grad=False):
         self.d = d = Dims(T, H, E, k, I)
         self.fp8_checkpoint = fp8_checkpoint
+        self.router_grad = router_grad
         self.device = dev = torch.device(device)
         M = self.M_cap = d.m_cap
         u8, f32, bf16, i32 = torch.uint8, torch.float32, torch.bfloat16, torch.int32
@@ -80,6 +85,8 @@ class ExpertLayerFP8:
         b["das"] = _empty((M, 2 * I // 128), f32, dev)
         b["dx_perm"] = _empty((M, H), bf16, dev)
         b["dx"] = _empty((T, H), bf16, dev)
+        if router_grad:
+            b["dprobs"] = _empty((T, k), f32, dev)
         for name, cols in (("x", H), ("h", I), ("dy", H), ("da", 2 * I)):
             b[name + "Tq"] = _empty((cols, M), u8, dev)
             b[name + "Ts"] = _empty((M // 128, cols), f32, dev)  # block-major column scales
@@ -110,7 +117,12 @@ class ExpertLayerFP8:
     def backward(self, dy, probs):
         b, d = self.buf, self.d
         off = b["offsets"]
-        ff8.ff8_permute_quant(dy, probs, d.k, d.E, None, True, b["row_map"], off, b["src_row"], b["dyq"], b["dys"])
+        if self.router_grad:
+            ff8.ff8_permute_quant_dprobs(dy, probs, d.k, d.E, b["row_map"], off, b["src_row"], b["dyq"], b["dys"],
+                                         b["y_perm"], b["dprobs"])
+        else:
+            ff8.ff8_permute_quant(dy, probs, d.k, d.E, None, True, b["row_map"], off, b["src_row"], b["dyq"],
+                                  b["dys"])
         ff8.ff8_grouped_gemm_dgrad(b["dyq"], b["dys"], b["w2q"], b["w2s"], off, b["dh"])
         if self.fp8_checkpoint:
             ff8.ff8_swiglu_bwd_quant_fp8a(b["aq"], b["as"], b["dh"], b["daq"], b["das"], off, d.E)

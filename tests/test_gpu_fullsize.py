@@ -220,6 +220,29 @@ def test_fp8_checkpoint_sampled_rows(run):
     del hq, hs, aq, a_s, daq, das
 
 
+def test_router_grad_sampled_tokens(run):
+    """B1 fused with the router gradient on the step's own dY and Y_perm: the quantized copies
+    equal the step's B1 output, dprobs at sampled tokens within the fp32 summation bound."""
+    shape, d, b, rng = run["shape"], run["d"], run["b"], run["rng"]
+    m_pad = int(run["off"][-1])
+    q, s = torch.empty_like(b["dyq"]), torch.empty_like(b["dys"])
+    dprobs = torch.empty((shape.T, shape.k), dtype=torch.float32, device="cuda")
+    ff8.ff8_permute_quant_dprobs(d["dy"], d["probs"], shape.k, shape.E, b["row_map"], b["offsets"], b["src_row"],
+                                 q, s, b["y_perm"], dprobs)
+    torch.cuda.synchronize()
+    assert torch.equal(q[:m_pad], b["dyq"][:m_pad]) and torch.equal(s[:m_pad], b["dys"][:m_pad])
+    t = np.sort(rng.choice(shape.T, size=64, replace=False))
+    rows = run["row_map"][t]
+    local = np.where(rows >= 0, np.arange(rows.size).reshape(rows.shape), -1)
+    yp = f64(b["y_perm"].index_select(0, _cuda_idx(np.maximum(rows, 0).reshape(-1))))
+    dy = f64(d["dy"].index_select(0, _cuda_idx(t)))
+    want = moe.router_grad(dy, yp, local)
+    mag = moe.router_grad(np.abs(dy), np.abs(yp), local)
+    got = f64(dprobs.index_select(0, _cuda_idx(t)))
+    assert np.all(np.abs(got - want) <= mag * 2.0 ** -16 + 1e-30), np.max(np.abs(got - want) / (mag + 1e-30))
+    del q, s, dprobs
+
+
 def test_unpermute_sampled_tokens(run):
     """F5 (routing-weighted) and B5 (plain) at sampled tokens: within one bf16 ulp of the
     float64 weighted sum of the GPU's own expert outputs."""

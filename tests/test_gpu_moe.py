@@ -274,6 +274,44 @@ def test_swiglu_fwd_bwd(case):
 
 
 @pytest.mark.parametrize("case", list(CASES))
+def test_permute_quant_dprobs(case):
+    """B1 fused with the router gradient: the quantized copies bit-identical to the oracle's
+    (and to the unfused entry point's), dprobs[t, j] = <dY[t], Y_perm[row]> within the fp32
+    summation bound, 0 for dropped slots."""
+    shape, inp = _inputs(case)
+    T, H, E, k = shape.T, shape.H, shape.E, shape.k
+    idx = inp["topk_idx"].clone()
+    idx[::7, 0] = -1  # dropped slots
+    M_cap, row_map, offsets, src_row, ws = _routing_device(shape, inp)
+    xq = torch.empty((M_cap, H), dtype=torch.uint8, device="cuda")
+    xs = torch.empty((M_cap, H // 128), dtype=torch.float32, device="cuda")
+    ff8.ff8_permute_quant(dev(inp["x"]), None, k, E, dev(idx), False, row_map, offsets, src_row, xq, xs, ws)
+    y_perm = dev(workloads.randn_bf16((M_cap, H), 1.0, seed=21))
+    dy, probs = dev(inp["dy"]), dev(inp["probs"])
+    q = poisoned((M_cap, H), torch.uint8)
+    s = poisoned((M_cap, H // 128), torch.float32)
+    dprobs = poisoned((T, k), torch.float32)
+    ff8.ff8_permute_quant_dprobs(dy, probs, k, E, row_map, offsets, src_row, q, s, y_perm, dprobs)
+    q2 = torch.empty_like(q)
+    s2 = torch.empty_like(s)
+    ff8.ff8_permute_quant(dy, probs, k, E, None, True, row_map, offsets, src_row, q2, s2)
+    torch.cuda.synchronize()
+    _, w_off, w_map, w_src = moe.route(host(idx), E)
+    m_pad = int(w_off[-1])
+    assert np.array_equal(host(row_map), w_map)
+    wq, wsc = moe.permute_quant_rows(f64(inp["dy"]), w_src, k, row_w=host(inp["probs"]))
+    assert np.array_equal(host(q[:m_pad]), wq) and np.array_equal(host(s[:m_pad]), wsc)
+    assert torch.equal(q[:m_pad], q2[:m_pad]) and torch.equal(s[:m_pad], s2[:m_pad])
+    assert untouched(q[m_pad:]) and untouched(s[m_pad:])
+    yp64, dy64 = f64(y_perm), f64(inp["dy"])
+    want = moe.router_grad(dy64, yp64, w_map)
+    mag = moe.router_grad(np.abs(dy64), np.abs(yp64), w_map)  # sum of |terms|
+    got = host(dprobs).astype(np.float64)
+    assert np.all(np.abs(got - want) <= mag * 2.0 ** -16 + 1e-30), np.max(np.abs(got - want) / (mag + 1e-30))
+    assert np.all(got[w_map < 0] == 0.0) and (w_map < 0).any()
+
+
+@pytest.mark.parametrize("case", list(CASES))
 def test_swiglu_fp8_checkpoint(case):
     """F3 keeping A as an FP8 checkpoint, and B3 reading A back from it (section 4.2):
     the checkpoint bit-exact, H and dA against the oracle on the same operands."""
@@ -331,14 +369,15 @@ def test_unpermute(k):
         assert np.all(np.abs(got - want) <= ulp + 1e-6), np.max(np.abs(got - want) / ulp)
 
 
-@pytest.mark.parametrize("ckpt", [False, True], ids=["bf16_a", "fp8_checkpoint"])
+@pytest.mark.parametrize("ckpt", [False, True], ids=["paper_rows", "fp8_checkpoint_and_dprobs"])
 @pytest.mark.parametrize("case", list(CASES))
 def test_layer_stagewise(case, ckpt):
     """Whole forward+backward through ExpertLayerFP8; every stage is checked against the
     oracle applied to the GPU's own upstream outputs (no error compounding).  With the FP8
-    checkpoint, A's checkpoint is bit-exact and the SwiGLU backward reads A from it."""
+    checkpoint, A's checkpoint is bit-exact and the SwiGLU backward reads A from it; the router
+    gradient of the same run is checked within its fp32 summation bound."""
     shape, inp = _inputs(case)
-    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt)
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt, router_grad=ckpt)
     d = {k: dev(v) for k, v in inp.items()}
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
@@ -364,6 +403,11 @@ def test_layer_stagewise(case, ckpt):
     assert rel_frob(f64(b["y"]), y) < 1e-3
     dyq, dys = moe.permute_quant_rows(f64(inp["dy"]), w_src, shape.k, row_w=host(inp["probs"]))
     assert np.array_equal(host(b["dyq"][:m_pad]), dyq) and np.array_equal(host(b["dys"][:m_pad]), dys)
+    if ckpt:
+        yp64 = f64(b["y_perm"][:m_pad])
+        want = moe.router_grad(f64(inp["dy"]), yp64, w_map)
+        mag = moe.router_grad(np.abs(f64(inp["dy"])), np.abs(yp64), w_map)
+        assert np.all(np.abs(host(b["dprobs"]) - want) <= mag * 2.0 ** -16 + 1e-30)
     dH = moe.grouped_gemm_dgrad(dyq, dys, w["w2q"], w["w2s"], off)
     assert rel_frob(f64(b["dh"][:m_pad]), dH) < GEMM_TOL
     dh_gpu = f64(b["dh"][:m_pad])

@@ -188,6 +188,38 @@ def test_fp8_checkpoint_of_a():
     assert np.linalg.norm(g_ck - g_ref) / np.linalg.norm(g_ref) < 0.05
 
 
+def test_router_grad_loop_and_directional_derivative():
+    """dprobs is the derivative of <dY, combine(w)> with respect to each routing weight: the
+    combine is linear in w, so a unit step in w[t, j] changes the loss by exactly dprobs[t, j]."""
+    rng = np.random.default_rng(9)
+    T, k, H, M = 12, 3, 40, 50
+    row_map = np.stack([rng.choice(M, size=k, replace=False) for _ in range(T)]).astype(np.int64)
+    row_map[2, 1] = -1
+    row_map[7, 0] = -1
+    y_perm = rng.standard_normal((M, H))
+    dy = rng.standard_normal((T, H))
+    w = rng.random((T, k))
+    dp = moe.router_grad(dy, y_perm, row_map)
+    for t in range(T):
+        for j in range(k):
+            r = row_map[t, j]
+            want = 0.0 if r < 0 else math.fsum(dy[t, h] * y_perm[r, h] for h in range(H))
+            assert dp[t, j] == pytest.approx(want, rel=1e-12, abs=1e-12)
+
+    def loss(wt):
+        y = np.zeros((T, H))
+        for j in range(k):
+            ok = row_map[:, j] >= 0
+            y[ok] += wt[ok, j][:, None] * y_perm[row_map[ok, j]]
+        return float(np.sum(dy * y))
+
+    base = loss(w)
+    for t, j in [(0, 0), (2, 1), (5, 2), (11, 1)]:
+        w2 = w.copy()
+        w2[t, j] += 1.0
+        assert loss(w2) - base == pytest.approx(dp[t, j], rel=1e-9, abs=1e-9)
+
+
 def test_unpermute_loop_and_gather():
     T, k, E, H = 30, 3, 5, 128
     idx = _routing(T, k, E, 8, drop=0.1)
