@@ -34,7 +34,8 @@
  *    tensors.  E is at most 1024.
  *  - Every pointer is a device pointer unless stated otherwise.  The caller
  *    owns all memory; the library allocates nothing and keeps no pointer after
- *    a call returns.
+ *    a call returns.  With T = 0 (an empty batch) the token-indexed arrays (x, dy,
+ *    row_map, row_w, y, dprobs, topk_idx) may be NULL.
  *  - stream is a hipStream_t passed as void* (NULL = the null stream).  Every
  *    call only enqueues work on it and returns; results are ready when the
  *    stream reaches that point.  Calls on one stream are ordered; concurrent

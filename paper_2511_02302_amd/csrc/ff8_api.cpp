@@ -112,8 +112,10 @@ int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t 
   REQUIRE_SHAPE(T >= 0 && mult128(H) && M_cap % 128 == 0);
   REQUIRE_SHAPE(M_cap >= ff8_rows_bound(T, k, E));
   REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
-  if (T > 0) REQUIRE_PTR(x);
-  REQUIRE_PTR(row_map); REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  if (T > 0) {  // an empty batch may pass NULL for its empty token-indexed arrays
+    REQUIRE_PTR(x); REQUIRE_PTR(row_map);
+  }
+  REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
   hipStream_t st = as_stream(stream);
   if (!reuse_map) {
     if (T > 0) REQUIRE_PTR(topk_idx);
@@ -135,10 +137,10 @@ int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, 
   REQUIRE_SHAPE(T >= 0 && mult128(H) && H <= ff8::max_h_dprobs() && M_cap % 128 == 0);
   REQUIRE_SHAPE(M_cap >= ff8_rows_bound(T, k, E));
   REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
-  if (T > 0) {
-    REQUIRE_PTR(dy); REQUIRE_PTR(row_w); REQUIRE_PTR(y_perm); REQUIRE_PTR(dprobs);
+  if (T > 0) {  // an empty batch may pass NULL for its empty token-indexed arrays
+    REQUIRE_PTR(dy); REQUIRE_PTR(row_w); REQUIRE_PTR(y_perm); REQUIRE_PTR(dprobs); REQUIRE_PTR(row_map);
   }
-  REQUIRE_PTR(row_map); REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
   return hip_status(ff8::launch_permute_quant_dprobs(dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s,
                                                      y_perm, dprobs, as_stream(stream)),
                     __func__);

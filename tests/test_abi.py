@@ -68,5 +68,8 @@ def test_validation_errors_without_gpu(lib):
     assert lib.ff8_permute_quant(fake, None, 16, 128, 2, 4, fake, 0, fake, fake, fake, 640, fake, fake,
                                  fake, 0, None) == 3
     assert lib.ff8_unpermute(fake, fake, None, 4, 0, 128, 128, fake, None) == 3
+    # an empty batch passes validation with NULL token-indexed arrays (no GPU here: the launch fails)
+    assert lib.ff8_permute_quant(None, None, 0, 128, 2, 4, None, 0, None, fake, fake, 512, fake, fake,
+                                 None, 0, None) != 1
     assert lib.ff8_swiglu_quant(fake, None, 0, 128, 100, fake, fake, None) == 2
     assert lib.ff8_baseline_copy(fake, fake, 17, None) == 2

@@ -30,6 +30,7 @@ def _skewed_routing(T, k, E, seed):
 CASES = {
     "tiny": (workloads.TINY, None),
     "ragged": (workloads.LayerShape("ragged T300 H384 E6 k2 I384", 300, 384, 6, 2, 384, "iid"), 7),
+    "one_expert": (workloads.LayerShape("one expert T200 H256 E1 k1 I256", 200, 256, 1, 1, 256, "iid"), None),
 }
 
 
@@ -251,9 +252,9 @@ def test_swiglu_fwd_bwd(case):
     M_cap = 1024
     a = workloads.randn_bf16((M_cap, 2 * I), 2.0, seed=8)
     dh = workloads.randn_bf16((M_cap, I), 1.0, seed=9)
-    offsets = dev(torch.tensor([0, 256, 256, 640, 896][: min(5, E + 1)] + [896] * max(0, E + 1 - 5),
-                               dtype=torch.int32))
-    m_pad = 896
+    off_list = [0, 256, 256, 640, 896][: min(5, E + 1)] + [896] * max(0, E + 1 - 5)
+    offsets = dev(torch.tensor(off_list, dtype=torch.int32))
+    m_pad = off_list[-1]
     hq = poisoned((M_cap, I), torch.uint8)
     hs = poisoned((M_cap, I // 128), torch.float32)
     ff8.ff8_swiglu_quant(dev(a), hq, hs, offsets, E)
@@ -320,9 +321,9 @@ def test_swiglu_fp8_checkpoint(case):
     M_cap = 1024
     a = workloads.randn_bf16((M_cap, 2 * I), 2.0, seed=8)
     dh = workloads.randn_bf16((M_cap, I), 1.0, seed=9)
-    offsets = dev(torch.tensor([0, 256, 256, 640, 896][: min(5, E + 1)] + [896] * max(0, E + 1 - 5),
-                               dtype=torch.int32))
-    m_pad = 896
+    off_list = [0, 256, 256, 640, 896][: min(5, E + 1)] + [896] * max(0, E + 1 - 5)
+    offsets = dev(torch.tensor(off_list, dtype=torch.int32))
+    m_pad = off_list[-1]
     hq = poisoned((M_cap, I), torch.uint8)
     hs = poisoned((M_cap, I // 128), torch.float32)
     aq = poisoned((M_cap, 2 * I), torch.uint8)
@@ -367,6 +368,25 @@ def test_unpermute(k):
             assert np.array_equal(got, want)
         ulp = np.ldexp(1.0, np.frexp(np.maximum(np.abs(want), 1e-30))[1] - 8)
         assert np.all(np.abs(got - want) <= ulp + 1e-6), np.max(np.abs(got - want) / ulp)
+
+
+def test_layer_empty_batch():
+    """T = 0: no routed rows; every kernel launches over empty groups, the weight gradients
+    come out zero, and no row buffer is written."""
+    shape = workloads.LayerShape("empty T0 H256 E4 k2 I256", 0, 256, 4, 2, 256, "iid")
+    inp = workloads.layer_inputs(shape, seed=3)
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=True, router_grad=True)
+    for n in ("xq", "a", "hq", "y_perm", "dyq", "dh", "daq", "dx_perm"):
+        L.buf[n].view(torch.uint8).fill_(0xA5)
+    d = {k: dev(v) for k, v in inp.items()}
+    L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
+    torch.cuda.synchronize()
+    b = L.buf
+    assert host(b["offsets"]).tolist() == [0] * (shape.E + 1)
+    assert bool((b["dw1"] == 0).all()) and bool((b["dw2"] == 0).all())
+    for n in ("xq", "a", "hq", "y_perm", "dyq", "dh", "daq", "dx_perm"):
+        assert bool((b[n].view(torch.uint8) == 0xA5).all()), n
+    assert b["y"].numel() == 0 and b["dx"].numel() == 0
 
 
 @pytest.mark.parametrize("ckpt", [False, True], ids=["paper_rows", "fp8_checkpoint_and_dprobs"])
