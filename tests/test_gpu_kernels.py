@@ -143,7 +143,8 @@ def _row_scaled_fp8(rows, cols, seed, kmax=12):
     return q, s
 
 
-@pytest.mark.parametrize("rows,cols,n_rows", [(128, 128, 128), (640, 384, 640), (1024, 256, 512), (896, 128, 384)])
+@pytest.mark.parametrize("rows,cols,n_rows", [(128, 128, 128), (640, 384, 640), (1024, 256, 512), (896, 128, 384),
+                                         (16384, 256, 12800)])  # the last: diagonal order
 def test_sat_bit_exact(rows, cols, n_rows):
     q, s = _row_scaled_fp8(rows, cols, seed=rows + cols)
     qT = poisoned((cols, rows), torch.uint8)
