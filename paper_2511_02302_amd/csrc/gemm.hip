@@ -133,8 +133,6 @@ __device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t 
                : "memory");
 }
 
-__device__ __forceinline__ uint32_t e8m0(float s) { return __float_as_uint(s) >> 23; }
-
 __device__ __forceinline__ i32x8 with_half(i32x8 f, const u32x4& x, int half) {
   f[4 * half + 0] = (int)x[0];
   f[4 * half + 1] = (int)x[1];
