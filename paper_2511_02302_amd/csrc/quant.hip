@@ -89,6 +89,49 @@ __global__ __launch_bounds__(kThreads) void quant_block128_kernel(const uint16_t
   if (threadIdx.x == 0) s[blk] = exp2i(t);
 }
 
+// Two horizontally adjacent 128x128 blocks per workgroup: 32 lanes span a 256-column row
+// segment (512 bytes per load instruction pair of rows), 8 rows per pass, 16 passes.
+__global__ __launch_bounds__(kThreads) void quant_block128x2_kernel(const uint16_t* __restrict__ w, int64_t cols,
+                                                                    int64_t n_pairs, uint8_t* __restrict__ q,
+                                                                    float* __restrict__ s) {
+  __shared__ uint32_t wave_max[kThreads / 64][2];
+  const int64_t pr = blockIdx.x;
+  const int64_t rb = pr / n_pairs, cp = pr - rb * n_pairs;
+  const int cc = threadIdx.x & 31, r0 = threadIdx.x >> 5;
+  const int64_t base = (rb * kTile + r0) * cols + cp * 2 * kTile + cc * 8;
+  u32x4 v[16];
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    v[i] = ldnt16(w + base + (int64_t)i * 8 * cols);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      m = max(m, abs_bits(bf16_lo(v[i][j])));
+      m = max(m, abs_bits(bf16_hi(v[i][j])));
+    }
+  }
+  m = max16_u32(m);                                   // per 16-lane group: one block, one row group
+  m = max(m, (uint32_t)__shfl_xor((int)m, 32));       // both row groups of the wave
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) wave_max[wv][0] = m;
+  if (lane == 16) wave_max[wv][1] = m;
+  __syncthreads();
+  const int h = cc >> 4;  // this lane's block
+  m = max(max(wave_max[0][h], wave_max[1][h]), max(wave_max[2][h], wave_max[3][h]));
+  const int t = scale_exponent(__uint_as_float(m));
+  const float inv = exp2i(-t);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float f[8];
+    unpack_bf16x8(v[i], f);
+    u32x2 r;
+    r[0] = cvt_e4m3x4(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv);
+    r[1] = cvt_e4m3x4(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv);
+    stnt8(q + base + (int64_t)i * 8 * cols, r);
+  }
+  if (threadIdx.x == 0 || threadIdx.x == 16) s[rb * 2 * n_pairs + cp * 2 + h] = exp2i(t);
+}
+
 __device__ __forceinline__ float sat448(float f) { return fminf(fmaxf(f, -448.0f), 448.0f); }
 
 __global__ __launch_bounds__(kThreads) void cast_f32_e4m3_kernel(const float* __restrict__ x, int64_t n,
@@ -212,6 +255,10 @@ hipError_t launch_quant_rowwise(const uint16_t* x, int64_t rows, int64_t cols, u
 hipError_t launch_quant_block128(const uint16_t* w, int64_t rows, int64_t cols, uint8_t* q, float* s,
                                  hipStream_t st) {
   const int64_t nbc = cols / kTile, blocks = rows / kTile * nbc;
+  if (nbc % 2 == 0) {
+    quant_block128x2_kernel<<<(unsigned)(blocks / 2), kThreads, 0, st>>>(w, cols, nbc / 2, q, s);
+    return hipGetLastError();
+  }
   quant_block128_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(w, cols, nbc, q, s);
   return hipGetLastError();
 }
