@@ -49,6 +49,7 @@ def parse():
     ap.add_argument("--no-cast-ops", action="store_true")
     ap.add_argument("--no-fp8-checkpoint", action="store_true")
     ap.add_argument("--no-router-grad", action="store_true")
+    ap.add_argument("--no-align16", action="store_true")
     return ap.parse_args()
 
 
@@ -116,7 +117,8 @@ def run_step(L, d, ev=None, ckpt=None, dprobs=None):
     stages = [
         lambda: L.quantize_weights(d["w1"], d["w2"]),
         lambda: ff8.ff8_permute_quant(d["x"], None, dm.k, dm.E, d["topk_idx"], False, b["row_map"], off,
-                                      b["src_row"], b["xq"], b["xs"], b["ws"]),
+                                      b["src_row"], b["xq"], b["xs"], b["ws"],
+                                      align=None if dm.align == 128 else dm.align),
         lambda: ff8.ff8_grouped_gemm_fprop(b["xq"], b["xs"], b["w1q"], b["w1s"], off, b["a"]),
         f3,
         lambda: ff8.ff8_grouped_gemm_fprop(b["hq"], b["hs"], b["w2q"], b["w2s"], off, b["y_perm"]),
@@ -201,6 +203,35 @@ def router_grad(torch, L, d, shape, M, steps, warmup, ms_base, b1_base_ms):
                                         "frac_hbm": round(gbs / HBM_PEAK_GBS, 3), "bytes": by},
             "B1_without_dprobs_ms": round(b1_base_ms, 4),
             "ms_per_step": round(ms_step, 4), "ms_per_step_without": round(ms_base, 4)}
+
+
+def align16(torch, d, shape, M, steps, warmup, ms_base):
+    """The step with the expert groups padded to 16 rows (the paper's padding) instead of 128:
+    fewer padding rows, 128-row blocks shared by neighbouring experts (partial K blocks in
+    wgrad).  A separate layer object (its M_cap differs)."""
+    from paper_2511_02302_amd.layer import ExpertLayerFP8
+
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, align=16)
+    for _ in range(warmup):
+        run_step(L, d)
+    torch.cuda.synchronize()
+    names = list(stage_costs(shape, M))
+    timer = StageTimer(torch, names, steps)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run_step(L, d, timer.ev[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    st = timer.ms()
+    m_pad = int(L.buf["offsets"][-1].item())
+    costs = stage_costs(shape, M)
+    gemm_flops = sum(v for kind, v in costs.values() if kind == "mfma")
+    out = {"ms_per_step": round(ms_step, 4), "ms_per_step_align128": round(ms_base, 4),
+           "value": round(gemm_flops / (ms_step * 1e-3) / 1e12, 2), "padded_rows": m_pad, "routed_rows": M,
+           "stages_ms": {n: round(st[n], 4) for n in names}}
+    del L
+    torch.cuda.empty_cache()
+    return out
 
 
 def cast_ops(torch, reps=20):
@@ -431,6 +462,8 @@ def main():
     if not args.no_router_grad:
         rec["router_grad"] = router_grad(torch, L, d, shape, M, args.steps, args.warmup, ms_step,
                                          st_ms["B1_permute_quant_dy"])
+    if not args.no_align16:
+        rec["align16"] = align16(torch, d, shape, M, args.steps, args.warmup, ms_step)
     if not args.no_cast_ops:
         del L, d
         torch.cuda.empty_cache()

@@ -29,7 +29,7 @@
  *    written.  Grids are sized from M_cap, so no call synchronizes with the host.
  *    Because they are never copied to the host, offsets are not validated: they
  *    must satisfy 0 = offsets[0] <= offsets[1] <= ... <= offsets[E] <= M_cap with
- *    every difference a multiple of 128, as ff8_permute_quant writes them.  Other
+ *    every difference a multiple of 16, as ff8_permute_quant(_aligned) writes them.  Other
  *    values give undefined results and may make kernels access memory outside the
  *    tensors.  E is at most 1024.
  *  - Every pointer is a device pointer unless stated otherwise.  The caller
@@ -101,6 +101,13 @@ int ff8_quant_block128(const ff8_bf16* w, int64_t rows, int64_t cols, ff8_e4m3* 
  */
 int64_t ff8_rows_bound(int64_t T, int k, int E);
 
+/*
+ * ff8_rows_bound_aligned -- the same for groups padded to `align` rows (16, 32, 64 or
+ * 128): roundup(T*k + (align-1)*E, 128).  align = 16 is the paper's padding (section
+ * 3.3.1).  Returns -1 for invalid arguments.
+ */
+int64_t ff8_rows_bound_aligned(int64_t T, int k, int E, int align);
+
 /* Bytes of device workspace ff8_permute_quant needs (host helper). */
 size_t ff8_permute_workspace_bytes(int64_t T, int k, int E);
 
@@ -126,12 +133,27 @@ size_t ff8_permute_workspace_bytes(int64_t T, int k, int E);
  *   workspace device scratch of at least ff8_permute_workspace_bytes(T, k, E)
  *            bytes (ws_bytes gives its size); contents need not be initialized.
  *            May be NULL when reuse_map == 1.
- * Requires 1 <= k <= E, E <= 1024, M_cap >= ff8_rows_bound(T, k, E), H % 128 == 0.
+ * Requires 1 <= k <= E, E <= 1024, M_cap >= ff8_rows_bound(T, k, E), H % 128 == 0
+ * (with reuse_map = 1, M_cap >= ff8_rows_bound_aligned(T, k, E, 16) suffices).
  */
 int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                       const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets,
                       int32_t* src_row, int64_t M_cap, ff8_e4m3* q, float* s, void* workspace,
                       size_t ws_bytes, void* stream);
+
+/*
+ * ff8_permute_quant_aligned -- ff8_permute_quant with groups padded to a multiple of
+ *   `align` rows (16, 32, 64 or 128) instead of 128; align = 16 is the paper's padding
+ *   (section 3.3.1).  Requires M_cap >= ff8_rows_bound_aligned(T, k, E, align).  Every
+ *   other entry point accepts offsets padded to 16: a 128-row block of a grouped tensor
+ *   may then hold rows of two experts (the transpose takes S_max over the whole block,
+ *   or over the rows below offsets[E] in the last one, and wgrad masks the rows of other
+ *   experts out of its first and last K block).
+ */
+int ff8_permute_quant_aligned(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                              const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets,
+                              int32_t* src_row, int64_t M_cap, ff8_e4m3* q, float* s, void* workspace,
+                              size_t ws_bytes, int align, void* stream);
 
 /*
  * ff8_permute_quant_dprobs -- the backward permute of dY (ff8_permute_quant with reuse_map = 1

@@ -45,11 +45,11 @@ def quantize_weights(w1, w2):
     return out
 
 
-def forward(x, topk_idx, probs, w1q, w1s, w2q, w2s, E, fp8_checkpoint=False):
-    """F1..F5.  Returns a dict of every intermediate (numpy arrays)."""
+def forward(x, topk_idx, probs, w1q, w1s, w2q, w2s, E, fp8_checkpoint=False, align=moe.ALIGN):
+    """F1..F5 (expert groups padded to `align` rows).  Returns a dict of every intermediate."""
     T, k = topk_idx.shape
     st = {}
-    counts, offsets, row_map, src_row = moe.route(topk_idx, E)
+    counts, offsets, row_map, src_row = moe.route(topk_idx, E, align)
     st.update(counts=counts, offsets=offsets, row_map=row_map, src_row=src_row)
     st["xq"], st["xs"] = moe.permute_quant_rows(x, src_row, k)
     st["a"] = bf16_round(moe.grouped_gemm_fprop(st["xq"], st["xs"], w1q, w1s, offsets))

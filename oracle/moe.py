@@ -27,19 +27,21 @@ Row/column conventions (weights in [out, in] layout):
 
 import numpy as np
 
-from .codec import bf16_round
+from .codec import bf16_round, e4m3_decode
 from .quant import TILE, T_MIN, quant_rowwise, dequant_rowwise, dequant_block128, scale_from_exponent
 
 ALIGN = 128
 
 
-def rows_bound(T, k, E):
-    """Upper bound on the padded row count: every expert pads at most 127 rows."""
-    return -(-(T * k + (ALIGN - 1) * E) // ALIGN) * ALIGN
+def rows_bound(T, k, E, align=ALIGN):
+    """Upper bound on the padded row count, as a multiple of 128: every expert pads at
+    most align - 1 rows."""
+    return -(-(T * k + (align - 1) * E) // ALIGN) * ALIGN
 
 
-def route(topk_idx, E):
-    """Group the routed (token, slot) pairs by expert and pad each group to 128 rows.
+def route(topk_idx, E, align=ALIGN):
+    """Group the routed (token, slot) pairs by expert and pad each group to a multiple of
+    `align` rows (128, or the paper's 16).
 
     Returns counts [E], offsets [E+1] (exclusive scan of the padded counts in
     expert order), row_map [T, k] (row of each pair, -1 if dropped) and
@@ -48,7 +50,7 @@ def route(topk_idx, E):
     topk_idx = np.asarray(topk_idx, dtype=np.int64)
     T, k = topk_idx.shape
     counts = np.array([np.count_nonzero(topk_idx == e) for e in range(E)], dtype=np.int64)
-    padded = -(-counts // ALIGN) * ALIGN
+    padded = -(-counts // align) * align
     offsets = np.concatenate([[0], np.cumsum(padded)]).astype(np.int64)
     row_map = np.full((T, k), -1, dtype=np.int64)
     src_row = np.full(int(offsets[-1]), -1, dtype=np.int64)
@@ -116,8 +118,13 @@ def grouped_gemm_wgrad(gTq, gT_s, xTq, xT_s, offsets):
     """
     E = len(offsets) - 1
     m_pad = int(offsets[-1])
-    GT = dequant_rowwise(gTq[:, :m_pad], gT_s[:, : m_pad // TILE])
-    XT = dequant_rowwise(xTq[:, :m_pad], xT_s[:, : m_pad // TILE])
+    nb = -(-m_pad // TILE)  # groups padded to 16 may end inside a 128-token block
+
+    def dequant_cols(q, sc):
+        return e4m3_decode(q[:, :m_pad]) * np.repeat(np.asarray(sc, dtype=np.float64)[:, :nb], TILE, axis=1)[:, :m_pad]
+
+    GT = dequant_cols(gTq, gT_s)
+    XT = dequant_cols(xTq, xT_s)
     dw = np.zeros((E, gTq.shape[0], xTq.shape[0]), dtype=np.float64)
     for e in range(E):
         r0, r1 = offsets[e], offsets[e + 1]

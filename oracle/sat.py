@@ -30,22 +30,26 @@ from .quant import TILE, exponent_of_scale, scale_from_exponent, quant_rowwise, 
 
 
 def scaling_aware_transpose(q, s, n_rows=None):
-    """Algorithm 1 on the first n_rows rows (multiple of 128; default all rows).
+    """Algorithm 1 on the first n_rows rows (default all rows).
 
-    Returns (qT uint8 [cols, n_rows], sT float32 [cols, n_rows/128]).
+    Blocks are 128 consecutive rows.  When n_rows is not a multiple of 128 the last block
+    is partial: its S_max is taken over the rows it has (a group padded to 16 rows ends
+    inside a block).  Returns (qT uint8 [cols, n_rows], sT float32 [cols, ceil(n_rows/128)]).
     """
     q = np.asarray(q)
     rows, cols = q.shape
     n = rows if n_rows is None else int(n_rows)
-    assert n % TILE == 0 and cols % TILE == 0 and n <= rows
-    t_row = exponent_of_scale(np.asarray(s)[:n])            # [n, cols/128]
-    blocks = t_row.reshape(n // TILE, TILE, cols // TILE)
-    t_max = blocks.max(axis=1)                               # [n/128, cols/128]: log2 S_max
-    k = (t_max[:, None, :] - blocks).reshape(n, cols // TILE)  # k_i >= 0 per row and column tile
+    assert cols % TILE == 0 and n <= rows
+    nb = -(-n // TILE)
+    t_row = np.full((nb * TILE, cols // TILE), np.iinfo(np.int64).min // 2, dtype=np.int64)
+    t_row[:n] = exponent_of_scale(np.asarray(s)[:n])        # [n, cols/128]; missing rows never win the max
+    blocks = t_row.reshape(nb, TILE, cols // TILE)
+    t_max = blocks.max(axis=1)                               # [nb, cols/128]: log2 S_max
+    k = (t_max[:, None, :] - blocks).reshape(nb * TILE, cols // TILE)[:n]  # k_i >= 0 per row and column tile
     k_elem = np.repeat(k, TILE, axis=1)                      # [n, cols]
     shifted = e4m3_encode(e4m3_decode(q[:n]) * np.ldexp(1.0, -k_elem))
     qT = np.ascontiguousarray(shifted.T)
-    sT = np.repeat(scale_from_exponent(t_max).T, TILE, axis=0)  # [cols, n/128]
+    sT = np.repeat(scale_from_exponent(t_max).T, TILE, axis=0)  # [cols, nb]
     return qT, np.ascontiguousarray(sT)
 
 

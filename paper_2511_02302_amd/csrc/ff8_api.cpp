@@ -93,24 +93,29 @@ int ff8_quant_block128(const ff8_bf16* w, int64_t rows, int64_t cols, ff8_e4m3* 
   return hip_status(ff8::launch_quant_block128(w, rows, cols, q, s, as_stream(stream)), __func__);
 }
 
-int64_t ff8_rows_bound(int64_t T, int k, int E) {
-  if (T < 0 || k < 1 || E < 1 || k > E) return -1;
-  const int64_t need = T * k + 127LL * E;
+int64_t ff8_rows_bound_aligned(int64_t T, int k, int E, int align) {
+  if (T < 0 || k < 1 || E < 1 || k > E || !(align == 16 || align == 32 || align == 64 || align == 128)) return -1;
+  const int64_t need = T * k + (int64_t)(align - 1) * E;
   return (need + 127) / 128 * 128;
 }
+
+int64_t ff8_rows_bound(int64_t T, int k, int E) { return ff8_rows_bound_aligned(T, k, E, 128); }
 
 size_t ff8_permute_workspace_bytes(int64_t T, int k, int E) {
   if (T < 0 || k < 1 || E < 1) return 0;
   return ff8::permute_workspace_bytes(T, k, E);
 }
 
-int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
-                      const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
-                      int64_t M_cap, ff8_e4m3* q, float* s, void* workspace, size_t ws_bytes, void* stream) {
+int ff8_permute_quant_aligned(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                              const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets,
+                              int32_t* src_row, int64_t M_cap, ff8_e4m3* q, float* s, void* workspace,
+                              size_t ws_bytes, int align, void* stream) {
   REQUIRE_ARG(reuse_map == 0 || reuse_map == 1);
   REQUIRE_ARG(k >= 1 && E >= 1 && k <= E && E <= 1024);
+  REQUIRE_ARG(align == 16 || align == 32 || align == 64 || align == 128);
   REQUIRE_SHAPE(T >= 0 && mult128(H) && M_cap % 128 == 0);
-  REQUIRE_SHAPE(M_cap >= ff8_rows_bound(T, k, E));
+  // a reused map may come from any alignment: only the smallest bound is known here
+  REQUIRE_SHAPE(M_cap >= ff8_rows_bound_aligned(T, k, E, reuse_map ? 16 : align));
   REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
   if (T > 0) {  // an empty batch may pass NULL for its empty token-indexed arrays
     REQUIRE_PTR(x); REQUIRE_PTR(row_map);
@@ -122,12 +127,20 @@ int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t 
     const size_t need = ff8::permute_workspace_bytes(T, k, E);
     if (need > 0) REQUIRE_PTR(workspace);
     REQUIRE_ARG(ws_bytes >= need);
-    const int rc = hip_status(ff8::launch_route(topk_idx, T, k, E, row_map, offsets, src_row, M_cap, workspace, st),
-                              "ff8_permute_quant(route)");
+    const int rc = hip_status(
+        ff8::launch_route(topk_idx, T, k, E, align, row_map, offsets, src_row, M_cap, workspace, st),
+        "ff8_permute_quant(route)");
     if (rc != FF8_OK) return rc;
   }
   return hip_status(ff8::launch_permute_quant(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st),
                     __func__);
+}
+
+int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                      const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
+                      int64_t M_cap, ff8_e4m3* q, float* s, void* workspace, size_t ws_bytes, void* stream) {
+  return ff8_permute_quant_aligned(x, row_w, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
+                                   workspace, ws_bytes, 128, stream);
 }
 
 int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
@@ -135,7 +148,7 @@ int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, 
                              ff8_e4m3* q, float* s, const ff8_bf16* y_perm, float* dprobs, void* stream) {
   REQUIRE_ARG(k >= 1 && E >= 1 && k <= E && E <= 1024 && k <= ff8::max_k_dprobs());
   REQUIRE_SHAPE(T >= 0 && mult128(H) && H <= ff8::max_h_dprobs() && M_cap % 128 == 0);
-  REQUIRE_SHAPE(M_cap >= ff8_rows_bound(T, k, E));
+  REQUIRE_SHAPE(M_cap >= ff8_rows_bound_aligned(T, k, E, 16));  // the map may come from any alignment
   REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
   if (T > 0) {  // an empty batch may pass NULL for its empty token-indexed arrays
     REQUIRE_PTR(dy); REQUIRE_PTR(row_w); REQUIRE_PTR(y_perm); REQUIRE_PTR(dprobs); REQUIRE_PTR(row_map);

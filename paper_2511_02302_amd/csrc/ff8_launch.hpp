@@ -23,8 +23,8 @@ hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t co
                       uint8_t* qT, float* sT, hipStream_t st);
 
 size_t permute_workspace_bytes(int64_t T, int k, int E);
-hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int32_t* row_map, int32_t* offsets,
-                        int32_t* src_row, int64_t M_cap, void* workspace, hipStream_t st);
+hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int align, int32_t* row_map,
+                        int32_t* offsets, int32_t* src_row, int64_t M_cap, void* workspace, hipStream_t st);
 hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                                 const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                 int64_t M_cap, uint8_t* q, float* s, hipStream_t st);

@@ -175,6 +175,7 @@ struct Tile {
   int wave, lane, wp, wq;
   int nk;
   int k_rot;  // K stages this tile's loop is rotated by (a multiple of the scale batch)
+  int k_lo, k_hi;  // wgrad: valid K bytes [k_lo, 128) of the first stage and [0, k_hi) of the last
   // Stage ks of the loop reads K block (ks + k_rot) mod nk.
   __device__ __forceinline__ int kphys(int ks) const {
     const int k = ks + k_rot;
@@ -382,17 +383,50 @@ struct Tile {
     }
   }
 
+  // wgrad with groups padded to 16 rows: the first and last K blocks of an expert may hold
+  // tokens of its neighbours (or rows past offsets[E]).  Zero both operands' fragment bytes
+  // of this half-step outside [lo, hi) -- whole 16-byte pieces, since lo and hi are
+  // multiples of 16 -- so that those tokens add nothing (and no stale byte can be NaN).
+  // Lane l holds K bytes 64 H + 32 (l / 32) + 0..31 of its row: dwords 0-3, then 4-7.
+  template <bool kSetA>
+  __device__ __forceinline__ void mask_k(int lo, int hi) {
+    i32x8 (&fp)[4] = kSetA ? fpA : fpB;
+    i32x8 (&fq)[4] = kSetA ? fqA : fqB;
+    const int kb = (kSetA ? 0 : 64) + 32 * (lane >> 5);
+    const bool v0 = kb >= lo && kb < hi, v1 = kb + 16 >= lo && kb + 16 < hi;
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        fp[a][d] = v0 ? fp[a][d] : 0;
+        fp[a][4 + d] = v1 ? fp[a][4 + d] : 0;
+        fq[a][d] = v0 ? fq[a][d] : 0;
+        fq[a][4 + d] = v1 ? fq[a][4 + d] : 0;
+      }
+  }
+
   // Stage ks, S4 = ks % 4 (buffer S4 % 2).  Between the halves, wait for this wave's DMA
   // (stage ks+1, and the scale batch) and its reads of stage ks, then barrier: stage
   // ks+1 is visible to all and buffer ks % 2 is free for stage ks+2.  Stages past the
   // end are reloads of the last one (in bounds, never multiplied).
-  template <int S4>
+  // kMask (wgrad tiles whose first or last K block is shared with another expert): a
+  // separate instantiation of the loop, so that the loop of every other tile is unchanged.
+  template <int S4, bool kMask>
   __device__ __forceinline__ void stage(int ks) {
     constexpr int B = S4 % 2;
+    int lo = 0, hi = kBK;
+    if constexpr (kMask) {
+      lo = ks == 0 ? k_lo : 0;
+      hi = ks == nk - 1 ? k_hi : kBK;
+      if (lo > 0 || hi < kBK) mask_k<true>(lo, hi);  // uniform: first or last stage only
+    }
     half0_from<B, S4, 0>();
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kMask) {
+      if (lo > 0 || hi < kBK) mask_k<false>(lo, hi);
+    }
     half1_from<B, S4, 0>(ks + 2 < nk ? ks + 2 : nk - 1, ks + 1);
     if constexpr (S4 == 3) {
 #pragma unroll
@@ -409,6 +443,7 @@ struct Tile {
 struct TileInfo {
   int e, blk;
   int q0, q_end, k0, p0, nk;  // rows, columns and stages all stay below 2^31
+  int k_lo, k_hi;             // wgrad: valid K bytes of the first / last stage
 };
 
 // Tile w_in of XCD block blk (kBQ x kBP tiles, p fastest).  False for tiles past the
@@ -436,6 +471,8 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in
     t.q_end = __builtin_amdgcn_readfirstlane(g_off[e + 1]);
     t.k0 = 0;
     t.nk = g.Kdim / kBK;
+    t.k_lo = 0;
+    t.k_hi = kBK;
   } else {
     if (qg >= g.E * g.n_qt) return false;
     const int e = qg / g.n_qt;
@@ -444,8 +481,13 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in
     t.q_end = g.Nq;
     const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
     const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
-    t.k0 = o0;
-    t.nk = (o1 - o0) / kBK;
+    // K runs over whole 128-token blocks from the one holding o0; with groups padded to 16
+    // the first and last may be shared with neighbouring experts (masked in the loop)
+    const int kb0 = o0 & ~(kBK - 1);
+    t.k0 = kb0;
+    t.nk = o1 > o0 ? (o1 - kb0 + kBK - 1) / kBK : 0;
+    t.k_lo = o0 - kb0;
+    t.k_hi = o1 > o0 ? o1 - (kb0 + (t.nk - 1) * kBK) : kBK;
   }
   return true;
 }
@@ -460,6 +502,8 @@ __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, con
   const uint32_t q0 = (uint32_t)t.q0, k0 = (uint32_t)t.k0, p0 = (uint32_t)t.p0;
   const uint32_t Np = (uint32_t)g.Np, Kdim = (uint32_t)g.Kdim, M_cap = (uint32_t)g.M_cap;
   T.nk = t.nk;
+  T.k_lo = t.k_lo;
+  T.k_hi = t.k_hi;
   const uint32_t q_ld = (MODE == kWgrad) ? M_cap : Kdim;
   const uint32_t q_rows = (MODE == kWgrad) ? (uint32_t)g.Nq : M_cap;
   // K-major row of pattern h (h = 0, 1) for this lane: group w + 4h, row 8 group + l / 8,
@@ -774,11 +818,20 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
         T.template read_scale_rows<true, 0, 4>(0, raw);
         T.template pack_scales<true, 0, 4>(raw, T.cq);
       }
-      for (int ks = 0; ks < nk; ks += 4) {
-        T.template stage<0>(ks);
-        if (ks + 1 < nk) T.template stage<1>(ks + 1);
-        if (ks + 2 < nk) T.template stage<2>(ks + 2);
-        if (ks + 3 < nk) T.template stage<3>(ks + 3);
+      if (MODE == kWgrad && (T.k_lo > 0 || T.k_hi < kBK)) {
+        for (int ks = 0; ks < nk; ks += 4) {
+          T.template stage<0, MODE == kWgrad>(ks);
+          if (ks + 1 < nk) T.template stage<1, MODE == kWgrad>(ks + 1);
+          if (ks + 2 < nk) T.template stage<2, MODE == kWgrad>(ks + 2);
+          if (ks + 3 < nk) T.template stage<3, MODE == kWgrad>(ks + 3);
+        }
+      } else {
+        for (int ks = 0; ks < nk; ks += 4) {
+          T.template stage<0, false>(ks);
+          if (ks + 1 < nk) T.template stage<1, false>(ks + 1);
+          if (ks + 2 < nk) T.template stage<2, false>(ks + 2);
+          if (ks + 3 < nk) T.template stage<3, false>(ks + 3);
+        }
       }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs have landed
     }

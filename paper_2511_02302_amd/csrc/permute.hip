@@ -50,7 +50,8 @@ __global__ __launch_bounds__(kThreads) void route_count_kernel(const int32_t* __
 // it sums them, the parts' sums are scanned per expert in LDS, and each thread then
 // rewrites its range as exclusive bases.  All chunk loads of a pass are independent.
 __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ counts, int64_t n_chunks, int E,
-                                                          int32_t* __restrict__ offsets, int32_t* __restrict__ src_row) {
+                                                          int align, int32_t* __restrict__ offsets,
+                                                          int32_t* __restrict__ src_row) {
   __shared__ int part_sum[1024];  // [e][part], then exclusive prefix within e
   __shared__ int totals[1024];
   __shared__ int offs[1025];
@@ -78,7 +79,7 @@ __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ 
     int acc = 0;
     for (int i = 0; i < E; ++i) {
       offs[i] = acc;
-      acc += (totals[i] + kTile - 1) / kTile * kTile;
+      acc += (totals[i] + align - 1) / align * align;
     }
     offs[E] = acc;
   }
@@ -245,14 +246,14 @@ __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __res
                                                             const int32_t* __restrict__ src_row, int H,
                                                             uint8_t* __restrict__ q, float* __restrict__ s) {
   const int blk = blockIdx.x / kPadSplit, part = blockIdx.x - blk * kPadSplit;
-  const int64_t r0 = (int64_t)blk * kTile;
-  if (r0 >= offsets[E]) return;
+  const int64_t r0 = (int64_t)blk * kTile, r_end = offsets[E];
+  if (r0 >= r_end) return;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c16 = H / 16, sh = H / kTile;
   const u32x4 z = {0u, 0u, 0u, 0u};
   for (int i = part * (kThreads / 64) + wave; i < kTile; i += kPadSplit * (kThreads / 64)) {
     const int64_t r = r0 + i;
-    if (src_row[r] >= 0) continue;  // wave-uniform
+    if (r >= r_end || src_row[r] >= 0) continue;  // wave-uniform (groups padded to 16 may end inside a block)
     uint8_t* row = q + r * H;
     for (int c = lane; c < c16; c += 64) stnt16(row + c * 16, z);
     for (int c = lane; c < sh; c += 64) s[r * sh + c] = exp2i(kTMin);
@@ -330,13 +331,13 @@ size_t permute_workspace_bytes(int64_t T, int k, int E) {
   return (size_t)n_chunks_of(T) * (size_t)E * sizeof(int32_t);
 }
 
-hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int32_t* row_map, int32_t* offsets,
+hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int align, int32_t* row_map, int32_t* offsets,
                         int32_t* src_row, int64_t M_cap, void* workspace, hipStream_t st) {
   (void)M_cap;
   const int64_t nc = n_chunks_of(T);
   int32_t* counts = static_cast<int32_t*>(workspace);
   if (nc > 0) route_count_kernel<<<(unsigned)nc, kThreads, 0, st>>>(topk_idx, T, k, E, counts);
-  route_scan_kernel<<<1, 1024, 0, st>>>(counts, nc, E, offsets, src_row);
+  route_scan_kernel<<<1, 1024, 0, st>>>(counts, nc, E, align, offsets, src_row);
   if (nc > 0) route_assign_kernel<<<(unsigned)nc, 64, 0, st>>>(topk_idx, T, k, E, counts, row_map, src_row);
   return hipGetLastError();
 }

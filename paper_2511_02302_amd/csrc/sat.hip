@@ -20,6 +20,8 @@
 //      output order (XOR-swizzled 8-byte chunks, conflict-free);
 //   5. the 128x128 output block is streamed out with 16-byte non-temporal stores, 8
 //      lanes per 128-byte output row segment.
+// Groups padded to 16 rows can end inside a block: the last block's S_max covers only the
+// rows below m_rows (offsets[E]), and only those columns of qT are written.
 // The column-wise scales are block-major, sT [rows/128][cols]: block rb's S_max goes to the
 // 128 consecutive floats of its column tile (one coalesced 512-byte store per block), and
 // a consumer reads one contiguous run per 128-row block for any range of columns.
@@ -93,8 +95,9 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
   if (tid < 128) {
 #pragma unroll
     for (int bi = 0; bi < kRB; ++bi) {
-      int t_row = -256;
-      if (bi < n_valid) t_row = (int)(__float_as_uint(s[((rb0 + bi) * kTile + tid) * n_cb + cb]) >> 23) - 127;
+      int t_row = -256;  // rows at and beyond m_rows (a last block cut by 16-row padding) never win S_max
+      if (bi < n_valid && (rb0 + bi) * kTile + tid < m_rows)
+        t_row = (int)(__float_as_uint(s[((rb0 + bi) * kTile + tid) * n_cb + cb]) >> 23) - 127;
       t_rows[bi][tid] = t_row;
       const uint32_t m = max64_u32((uint32_t)(t_row + 256));
       if ((tid & 63) == 0) wmax[bi][tid >> 6] = m;
@@ -162,7 +165,8 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
       o[1] = a[1];
       o[2] = b[0];
       o[3] = b[1];
-      stnt16(qT + ((int64_t)cb * kTile + orow) * rows + rb * kTile + c16 * 16, o);
+      if (rb * kTile + c16 * 16 < m_rows)  // m_rows is a multiple of 16: whole 16-byte pieces
+        stnt16(qT + ((int64_t)cb * kTile + orow) * rows + rb * kTile + c16 * 16, o);
     }
     __syncthreads();  // the tile is rewritten by the next block
   }

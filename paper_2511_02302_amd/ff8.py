@@ -27,9 +27,12 @@ _SIGNATURES = {
     "ff8_quant_rowwise": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
     "ff8_quant_block128": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
     "ff8_rows_bound": (_c_i64, [_c_i64, _c_int, _c_int]),
+    "ff8_rows_bound_aligned": (_c_i64, [_c_i64, _c_int, _c_int, _c_int]),
     "ff8_permute_workspace_bytes": (_c_size, [_c_i64, _c_int, _c_int]),
     "ff8_permute_quant": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp, _c_vp,
                                    _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_vp]),
+    "ff8_permute_quant_aligned": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp,
+                                           _c_vp, _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_int, _c_vp]),
     "ff8_scaling_aware_transpose": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
     "ff8_grouped_gemm_fprop": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
                                         _c_vp]),
@@ -115,6 +118,10 @@ def ff8_version():
     return load().ff8_version()
 
 
+def ff8_rows_bound_aligned(T, k, E, align):
+    return int(load().ff8_rows_bound_aligned(T, k, E, align))
+
+
 def ff8_rows_bound(T, k, E):
     return int(load().ff8_rows_bound(T, k, E))
 
@@ -136,16 +143,20 @@ def ff8_quant_block128(w, q, s, stream=None):
 
 
 def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src_row, q, s, workspace=None,
-                      stream=None):
+                      stream=None, align=None):
+    """align None calls ff8_permute_quant (groups padded to 128 rows); 16/32/64/128 calls
+    ff8_permute_quant_aligned."""
     T, H = x.shape
     M_cap = q.shape[0]
     ws = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(load().ff8_permute_quant(
-        _ptr(x, _bf16, "x", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E, _ptr(topk_idx, _i32, "topk_idx"),
-        int(reuse_map), _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
-        _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2),
-        None if workspace is None else ctypes.c_void_p(workspace.data_ptr()), ws, _stream(stream)),
-        "ff8_permute_quant")
+    args = [_ptr(x, _bf16, "x", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E, _ptr(topk_idx, _i32, "topk_idx"),
+            int(reuse_map), _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
+            _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2),
+            None if workspace is None else ctypes.c_void_p(workspace.data_ptr()), ws]
+    if align is None:
+        _check(load().ff8_permute_quant(*args, _stream(stream)), "ff8_permute_quant")
+    else:
+        _check(load().ff8_permute_quant_aligned(*args, int(align), _stream(stream)), "ff8_permute_quant_aligned")
 
 
 def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y_perm, dprobs, stream=None):

@@ -19,6 +19,9 @@ FP8, section 4.2).
 With router_grad=True the backward permute of dY also computes the routing weights'
 gradient, dprobs[t, j] = <dY[t], Y_perm[row_map[t, j]]> (the backward of the weighted
 combine), in the same pass over dY.
+
+align=16 pads the expert groups to 16 rows, the paper's padding (section 3.3.1), instead
+of 128.
 """
 
 from dataclasses import dataclass
@@ -35,10 +38,11 @@ class Dims:
     E: int
     k: int
     I: int
+    align: int = 128
 
     @property
     def m_cap(self):
-        return ff8.ff8_rows_bound(self.T, self.k, self.E)
+        return ff8.ff8_rows_bound_aligned(self.T, self.k, self.E, self.align)
 
 
 def _empty(shape, dtype, device):
@@ -48,8 +52,8 @@ def _empty(shape, dtype, device):
 class ExpertLayerFP8:
     """Buffers and step sequence of one expert layer (E local experts, top-k routing)."""
 
-    def __init__(self, T, H, E, k, I, device="cuda", fp8_checkpoint=False, router_grad=False):
-        self.d = d = Dims(T, H, E, k, I)
+    def __init__(self, T, H, E, k, I, device="cuda", fp8_checkpoint=False, router_grad=False, align=128):
+        self.d = d = Dims(T, H, E, k, I, align)
         self.fp8_checkpoint = fp8_checkpoint
         self.router_grad = router_grad
         self.device = dev = torch.device(device)
@@ -103,7 +107,7 @@ class ExpertLayerFP8:
     def forward(self, x, topk_idx, probs):
         b, d = self.buf, self.d
         ff8.ff8_permute_quant(x, None, d.k, d.E, topk_idx, False, b["row_map"], b["offsets"], b["src_row"],
-                              b["xq"], b["xs"], b["ws"])
+                              b["xq"], b["xs"], b["ws"], align=None if d.align == 128 else d.align)
         ff8.ff8_grouped_gemm_fprop(b["xq"], b["xs"], b["w1q"], b["w1s"], b["offsets"], b["a"])
         if self.fp8_checkpoint:
             ff8.ff8_swiglu_quant_keep_fp8(b["a"], b["hq"], b["hs"], b["aq"], b["as"], b["offsets"], d.E)

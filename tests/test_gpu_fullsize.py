@@ -20,7 +20,8 @@ from test_gpu_moe import GEMM_TOL, _swiglu_bounds, _swiglu_check
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = {"dsv3": workloads.DSV3, "skew": workloads.SKEW}
+# (shape, row alignment of the expert groups): 128, and the paper's 16 on the DeepSeek-V3 share
+SHAPES = {"dsv3": (workloads.DSV3, 128), "skew": (workloads.SKEW, 128), "dsv3_align16": (workloads.DSV3, 16)}
 N_GEMM = 256  # sampled elements per GEMM output
 
 
@@ -35,13 +36,13 @@ def _rows(t, idx):
 
 @pytest.fixture(scope="module", params=list(SHAPES))
 def run(request):
-    shape = SHAPES[request.param]
-    print(f"\nfull-size layer step: {shape.name}", flush=True)
+    shape, align = SHAPES[request.param]
+    print(f"\nfull-size layer step: {shape.name}, groups padded to {align}", flush=True)
     d = workloads.layer_inputs(shape, seed=0, device="cuda")
-    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, align=align)
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
-    _, off, row_map, src_row = moe.route(host(d["topk_idx"]), shape.E)
+    _, off, row_map, src_row = moe.route(host(d["topk_idx"]), shape.E, align)
     yield {"shape": shape, "d": d, "b": L.buf, "off": off.astype(np.int64), "row_map": row_map,
            "src_row": src_row, "rng": np.random.default_rng(zlib.crc32(request.param.encode()))}
     del L, d
@@ -165,10 +166,11 @@ def _wgrad_samples(run, gT, xT, out):
         n = rng.integers(N, size=N_GEMM // 4)
         c = rng.integers(K, size=N_GEMM // 4)
         got = host(b[out][int(e)][_cuda_idx(n), _cuda_idx(c)])
-        g = quant.dequant_rowwise(host(b[gT + "q"][_cuda_idx(n), lo:hi]),
-                                  host(b[gT + "s"][lo // 128:hi // 128][:, _cuda_idx(n)]).T)
-        x = quant.dequant_rowwise(host(b[xT + "q"][_cuda_idx(c), lo:hi]),
-                                  host(b[xT + "s"][lo // 128:hi // 128][:, _cuda_idx(c)]).T)
+        blk = _cuda_idx(np.arange(lo, hi) // 128)  # each token's 128-row block (groups may share one)
+        g = codec.e4m3_decode(host(b[gT + "q"][_cuda_idx(n), lo:hi])) * \
+            host(b[gT + "s"].index_select(0, blk)[:, _cuda_idx(n)]).T.astype(np.float64)
+        x = codec.e4m3_decode(host(b[xT + "q"][_cuda_idx(c), lo:hi])) * \
+            host(b[xT + "s"].index_select(0, blk)[:, _cuda_idx(c)]).T.astype(np.float64)
         _check_gemm_samples(got, np.sum(g * x, axis=1), np.sum(np.abs(g * x), axis=1), bf16_out=False)
     for e in np.nonzero(off[1:] == off[:-1])[0]:
         assert not bool(b[out][int(e)].any()), f"expert {e} has no rows but a nonzero gradient"
@@ -270,3 +272,9 @@ def test_sat_sampled_blocks(run):
             wqT, wsT = sat.scaling_aware_transpose(host(q[rs, cs]), host(s[rs, cb:cb + 1]))
             assert np.array_equal(host(qT[cs, rs]), wqT), (name, rb, cb)
             assert np.array_equal(host(sT[rb:rb + 1, cs]).T, wsT), (name, rb, cb)
+        if m_pad % 128:  # groups padded to 16: the last block is partial
+            rb, n = m_pad // 128, m_pad % 128
+            rs, cs = slice(rb * 128, m_pad), slice(0, 256)
+            wqT, wsT = sat.scaling_aware_transpose(host(q[rs, cs]), host(s[rs, 0:2]), n)
+            assert np.array_equal(host(qT[cs, rs]), wqT), (name, "last block")
+            assert np.array_equal(host(sT[rb:rb + 1, cs]).T, wsT), (name, "last block")

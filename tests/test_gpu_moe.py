@@ -389,15 +389,19 @@ def test_layer_empty_batch():
     assert b["y"].numel() == 0 and b["dx"].numel() == 0
 
 
-@pytest.mark.parametrize("ckpt", [False, True], ids=["paper_rows", "fp8_checkpoint_and_dprobs"])
+@pytest.mark.parametrize("mode", ["paper_rows", "fp8_checkpoint_and_dprobs", "align16"])
 @pytest.mark.parametrize("case", list(CASES))
-def test_layer_stagewise(case, ckpt):
+def test_layer_stagewise(case, mode):
     """Whole forward+backward through ExpertLayerFP8; every stage is checked against the
     oracle applied to the GPU's own upstream outputs (no error compounding).  With the FP8
     checkpoint, A's checkpoint is bit-exact and the SwiGLU backward reads A from it; the router
-    gradient of the same run is checked within its fp32 summation bound."""
+    gradient of the same run is checked within its fp32 summation bound.  align16 pads the
+    groups to 16 rows (the paper's padding): 128-row blocks then straddle experts."""
     shape, inp = _inputs(case)
-    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt, router_grad=ckpt)
+    ckpt = mode == "fp8_checkpoint_and_dprobs"
+    align = 16 if mode == "align16" else 128
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt, router_grad=ckpt,
+                       align=align)
     d = {k: dev(v) for k, v in inp.items()}
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
@@ -407,8 +411,10 @@ def test_layer_stagewise(case, ckpt):
     w = olayer.quantize_weights(f64(inp["w1"]), f64(inp["w2"]))
     for n in ("w1q", "w1s", "w2q", "w2s"):
         assert np.array_equal(host(b[n]), w[n]), n
-    counts, w_off, w_map, w_src = moe.route(host(inp["topk_idx"]), shape.E)
+    counts, w_off, w_map, w_src = moe.route(host(inp["topk_idx"]), shape.E, align)
     assert np.array_equal(off, w_off) and np.array_equal(host(b["row_map"]), w_map)
+    if align == 16:
+        assert np.any(w_off % 128 != 0)  # some group boundary inside a 128-row block
     xq, xs = moe.permute_quant_rows(f64(inp["x"]), w_src, shape.k)
     assert np.array_equal(host(b["xq"][:m_pad]), xq) and np.array_equal(host(b["xs"][:m_pad]), xs)
     A = moe.grouped_gemm_fprop(xq, xs, w["w1q"], w["w1s"], off)
@@ -446,7 +452,7 @@ def test_layer_stagewise(case, ckpt):
     for name in ("x", "h", "dy", "da"):
         qT, sT = sat.scaling_aware_transpose(host(b[name + "q"][:m_pad]), host(b[name + "s"][:m_pad]))
         assert np.array_equal(host(b[name + "Tq"][:, :m_pad]), qT), name
-        assert np.array_equal(host(b[name + "Ts"][: m_pad // 128]).T, sT), name
+        assert np.array_equal(host(b[name + "Ts"][: -(-m_pad // 128)]).T, sT), name
     dW2 = moe.grouped_gemm_wgrad(host(b["dyTq"]), host(b["dyTs"]).T, host(b["hTq"]), host(b["hTs"]).T, off)
     assert rel_frob(host(b["dw2"]), dW2) < GEMM_TOL
     dW1 = moe.grouped_gemm_wgrad(host(b["daTq"]), host(b["daTs"]).T, host(b["xTq"]), host(b["xTs"]).T, off)

@@ -26,10 +26,11 @@ def _routing(T, k, E, seed, drop=0.0):
     return idx
 
 
-def test_route_brute_force():
+@pytest.mark.parametrize("align", [128, 16])
+def test_route_brute_force(align):
     for (T, k, E, seed, drop) in [(37, 2, 5, 0, 0.0), (300, 4, 6, 1, 0.1), (5, 1, 9, 2, 0.0)]:
         idx = _routing(T, k, E, seed, drop)
-        counts, offsets, row_map, src_row = moe.route(idx, E)
+        counts, offsets, row_map, src_row = moe.route(idx, E, align)
         # pure-Python reference: walk experts in order, tokens ascending
         row = 0
         ref_map = {}
@@ -42,7 +43,7 @@ def test_route_brute_force():
                         ref_map[(t, j)] = row
                         row += 1
             n = row - start
-            row = start + ((n + 127) // 128) * 128
+            row = start + ((n + align - 1) // align) * align
             ref_off.append(row)
         assert offsets.tolist() == ref_off
         for t in range(T):
@@ -51,8 +52,8 @@ def test_route_brute_force():
         real = src_row >= 0
         assert real.sum() == sum(1 for v in idx.ravel() if v >= 0)
         assert np.array_equal(np.sort(src_row[real]), np.sort(np.nonzero(idx.ravel() >= 0)[0]))
-        assert all(o % 128 == 0 for o in ref_off)
-        assert offsets[-1] <= moe.rows_bound(T, k, E)
+        assert all(o % align == 0 for o in ref_off)
+        assert offsets[-1] <= moe.rows_bound(T, k, E, align) and moe.rows_bound(T, k, E, align) % 128 == 0
         assert np.array_equal(counts, np.bincount(idx[idx >= 0].ravel(), minlength=E))
 
 

@@ -126,3 +126,19 @@ def test_double_quantization_error_ordering():
     assert sat_err < 1e-5 and n1_err < 1e-5
     assert n2_err > 1e-2
     assert n2_err > 1000 * sat_err
+
+
+def test_partial_last_block_equals_zero_padding():
+    """A last block with fewer than 128 rows (groups padded to 16) transposes as if the missing
+    rows were all-zero rows at scale 2^-126, which never raise S_max."""
+    rng = np.random.default_rng(31)
+    x = rng.standard_normal((176, 256)) * np.exp2(rng.integers(-6, 6, size=(176, 1)))
+    q, s = quant_rowwise(x)
+    qT, sT = scaling_aware_transpose(q, s, 176)
+    assert qT.shape == (256, 176) and sT.shape == (256, 2)
+    qp = np.concatenate([q, np.zeros((80, 256), dtype=np.uint8)])
+    sp = np.concatenate([s, np.full((80, 2), np.float32(2.0 ** -126))])
+    qT2, sT2 = scaling_aware_transpose(qp, sp)
+    assert np.array_equal(qT, qT2[:, :176]) and np.array_equal(sT, sT2)
+    # the partial block's scale is the max over its 48 rows only
+    assert np.array_equal(exponent_of_scale(sT[::128, 1]), exponent_of_scale(s[128:176]).max(axis=0))
