@@ -121,7 +121,7 @@ def grouped_gemm_wgrad(gTq, gT_s, xTq, xT_s, offsets):
     nb = -(-m_pad // TILE)  # groups padded to 16 may end inside a 128-token block
 
     def dequant_cols(q, sc):
-        return e4m3_decode(q[:, :m_pad]) * np.repeat(np.asarray(sc, dtype=np.float64)[:, :nb], TILE, axis=1)[:, :m_pad]
+        return e4m3_decode(q[:, :m_pad]) * np.repeat(np.asarray(sc)[:, :nb].astype(np.float64), TILE, axis=1)[:, :m_pad]
 
     GT = dequant_cols(gTq, gT_s)
     XT = dequant_cols(xTq, xT_s)
