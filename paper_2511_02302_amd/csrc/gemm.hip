@@ -174,7 +174,7 @@ struct Tile {
   static constexpr bool kBlockP = (MODE != kWgrad);
   int wave, lane, wp, wq;
   int nk;
-  int k_rot;  // K stages this tile's loop is rotated by (a multiple of the scale batch)
+  int k_rot;  // K stages this tile's loop is rotated by (fprop: a multiple of the scale batch)
   int k_lo, k_hi;  // wgrad: valid K bytes [k_lo, 128) of the first stage and [0, k_hi) of the last
   // Stage ks of the loop reads K block (ks + k_rot) mod nk.
   __device__ __forceinline__ int kphys(int ks) const {
@@ -188,7 +188,20 @@ struct Tile {
   // group * 1 KB -- so that within each pattern the swizzle (row group % 8) is constant
   // and consecutive instructions are one uniform step apart.  dgrad P (W_e rows n, 256
   // bytes): instruction i carries rows 32w + 4i .., patterns by i % 2.
-  template <int B, int I>
+  // wgrad with groups padded to 16 rows: an expert's first and last K blocks may hold tokens
+  // of its neighbours (or rows past offsets[E]).  Such a tile's loop is rotated so that these
+  // two blocks are its stages 0 and 1 (the last block first), whose DMAs are issued before
+  // the loop with kMask: lanes whose 16 tokens lie outside the expert load from the
+  // resource's end instead, which reads zeros, so those tokens add nothing and the loop
+  // itself is unchanged.  A K-major lane's 16-byte chunk is (l % 8) ^ kswz(row), the same
+  // for both patterns and both operands: (l % 8) ^ ((4 (w % 2) + l / 16) % 8).
+  __device__ __forceinline__ uint32_t masked_off(uint32_t off, uint32_t kp, uint32_t end) const {
+    const int l = lane;
+    const int c16 = 16 * ((l & 7) ^ ((4 * (wave & 1) + (l >> 4)) & 7));
+    const bool drop = (kp == 0 && c16 < k_lo) || ((int)kp == nk - 1 && c16 >= k_hi);
+    return drop ? end : off;
+  }
+  template <int B, int I, bool kMask = false>
   __device__ __forceinline__ void dma_tile(int ks) {
     const uint32_t stage = stage_lds<B>();
     const uint32_t kp = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(ks));  // uniform
@@ -199,13 +212,17 @@ struct Tile {
       } else {
         const uint32_t step = kp * (uint32_t)p_kstep + (uint32_t)(I & 3) * (uint32_t)p_istep;
         const uint32_t grp = (uint32_t)wave + (I < 4 ? 8 * I : 4 + 8 * (I - 4));
-        dma16(p_rsrc, p_voff[I >> 2] + step, stage + grp * 1024u);
+        uint32_t off = p_voff[I >> 2] + step;
+        if constexpr (kMask) off = masked_off(off, kp, (uint32_t)p_rsrc[2]);
+        dma16(p_rsrc, off, stage + grp * 1024u);
       }
     } else {
       constexpr int J = I - 8;
       const uint32_t step = kp * (uint32_t)q_kstep + (uint32_t)(J & 3) * (uint32_t)q_istep;
       const uint32_t grp = (uint32_t)wave + (J < 4 ? 8 * J : 4 + 8 * (J - 4));
-      dma16(q_rsrc, q_voff[J >> 2] + step, stage + kTileBytes + grp * 1024u);
+      uint32_t off = q_voff[J >> 2] + step;
+      if constexpr (kMask) off = masked_off(off, kp, (uint32_t)q_rsrc[2]);
+      dma16(q_rsrc, off, stage + kTileBytes + grp * 1024u);
     }
   }
   // Scale DMA of batch b (K blocks kb0..kb0+3 in loop order) into batch buffer b % 2:
@@ -219,17 +236,23 @@ struct Tile {
   // the last K block read neighbouring scales or zeros and are never multiplied.
   __device__ __forceinline__ void dma_scale_p(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1));
-    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-    if constexpr (kBlockP) dma4(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * 4u, lbase);
-    else dma16(sp_rsrc, sp_off + (kb0 + (uint32_t)wave) * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
+    if constexpr (kBlockP) {
+      const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
+      dma4(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * 4u, lbase);
+    } else {  // wgrad: wave w takes the block of stage 4 b + w (the rotation may wrap inside a batch)
+      const uint32_t kbw = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch + wave));
+      dma16(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
+    }
   }
   __device__ __forceinline__ void dma_scale_q(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1)) + kTP * kScaleBatch * 4;
-    const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-    if constexpr (MODE == kWgrad)
-      dma16(sq_rsrc, sq_off + (kb0 + (uint32_t)wave) * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
-    else
+    if constexpr (MODE == kWgrad) {
+      const uint32_t kbw = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch + wave));
+      dma16(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
+    } else {
+      const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
       dma16(sq_rsrc, sq_off + kb0 * 4u, lbase + (uint32_t)wave * 1024u);
+    }
   }
 
   // Fragment read J of half h of stage buffer B into register set kSetA.
@@ -383,50 +406,17 @@ struct Tile {
     }
   }
 
-  // wgrad with groups padded to 16 rows: the first and last K blocks of an expert may hold
-  // tokens of its neighbours (or rows past offsets[E]).  Zero both operands' fragment bytes
-  // of this half-step outside [lo, hi) -- whole 16-byte pieces, since lo and hi are
-  // multiples of 16 -- so that those tokens add nothing (and no stale byte can be NaN).
-  // Lane l holds K bytes 64 H + 32 (l / 32) + 0..31 of its row: dwords 0-3, then 4-7.
-  template <bool kSetA>
-  __device__ __forceinline__ void mask_k(int lo, int hi) {
-    i32x8 (&fp)[4] = kSetA ? fpA : fpB;
-    i32x8 (&fq)[4] = kSetA ? fqA : fqB;
-    const int kb = (kSetA ? 0 : 64) + 32 * (lane >> 5);
-    const bool v0 = kb >= lo && kb < hi, v1 = kb + 16 >= lo && kb + 16 < hi;
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        fp[a][d] = v0 ? fp[a][d] : 0;
-        fp[a][4 + d] = v1 ? fp[a][4 + d] : 0;
-        fq[a][d] = v0 ? fq[a][d] : 0;
-        fq[a][4 + d] = v1 ? fq[a][4 + d] : 0;
-      }
-  }
-
   // Stage ks, S4 = ks % 4 (buffer S4 % 2).  Between the halves, wait for this wave's DMA
   // (stage ks+1, and the scale batch) and its reads of stage ks, then barrier: stage
   // ks+1 is visible to all and buffer ks % 2 is free for stage ks+2.  Stages past the
   // end are reloads of the last one (in bounds, never multiplied).
-  // kMask (wgrad tiles whose first or last K block is shared with another expert): a
-  // separate instantiation of the loop, so that the loop of every other tile is unchanged.
-  template <int S4, bool kMask>
+  template <int S4>
   __device__ __forceinline__ void stage(int ks) {
     constexpr int B = S4 % 2;
-    int lo = 0, hi = kBK;
-    if constexpr (kMask) {
-      lo = ks == 0 ? k_lo : 0;
-      hi = ks == nk - 1 ? k_hi : kBK;
-      if (lo > 0 || hi < kBK) mask_k<true>(lo, hi);  // uniform: first or last stage only
-    }
     half0_from<B, S4, 0>();
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (kMask) {
-      if (lo > 0 || hi < kBK) mask_k<false>(lo, hi);
-    }
     half1_from<B, S4, 0>(ks + 2 < nk ? ks + 2 : nk - 1, ks + 1);
     if constexpr (S4 == 3) {
 #pragma unroll
@@ -585,6 +575,9 @@ __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, con
   T.k_rot = (kStaggerK<MODE> && (T.nk & (kScaleBatch - 1)) == 0 && T.nk >= 2 * kScaleBatch)
                 ? ((t.blk * 5) % (T.nk / kScaleBatch)) * kScaleBatch
                 : 0;
+  // wgrad, an expert's K range cut by 16-row padding: the last block, then the first, as
+  // stages 0 and 1, so that the only masked DMAs are the two issued before the loop
+  if (MODE == kWgrad && (T.k_lo > 0 || T.k_hi < kBK) && T.nk > 1) T.k_rot = T.nk - 1;
 }
 
 // Output of one tile through stage buffer 1 only (16 KB per wave), so that the next
@@ -685,12 +678,12 @@ __device__ __forceinline__ void epilogue(Tile<MODE>& T, const GemmArgs& g, const
 // First-stage DMA of a tile: stage 0 into buffer 0, then the scale batch 0 (buffer 0).
 template <int MODE>
 __device__ __forceinline__ void dma_first_stage(Tile<MODE>& T) {
-  T.template dma_tile<0, 0>(0); T.template dma_tile<0, 1>(0); T.template dma_tile<0, 2>(0);
-  T.template dma_tile<0, 3>(0); T.template dma_tile<0, 4>(0); T.template dma_tile<0, 5>(0);
-  T.template dma_tile<0, 6>(0); T.template dma_tile<0, 7>(0); T.template dma_tile<0, 8>(0);
-  T.template dma_tile<0, 9>(0); T.template dma_tile<0, 10>(0); T.template dma_tile<0, 11>(0);
-  T.template dma_tile<0, 12>(0); T.template dma_tile<0, 13>(0); T.template dma_tile<0, 14>(0);
-  T.template dma_tile<0, 15>(0);
+  T.template dma_tile<0, 0, MODE == kWgrad>(0); T.template dma_tile<0, 1, MODE == kWgrad>(0); T.template dma_tile<0, 2, MODE == kWgrad>(0);
+  T.template dma_tile<0, 3, MODE == kWgrad>(0); T.template dma_tile<0, 4, MODE == kWgrad>(0); T.template dma_tile<0, 5, MODE == kWgrad>(0);
+  T.template dma_tile<0, 6, MODE == kWgrad>(0); T.template dma_tile<0, 7, MODE == kWgrad>(0); T.template dma_tile<0, 8, MODE == kWgrad>(0);
+  T.template dma_tile<0, 9, MODE == kWgrad>(0); T.template dma_tile<0, 10, MODE == kWgrad>(0); T.template dma_tile<0, 11, MODE == kWgrad>(0);
+  T.template dma_tile<0, 12, MODE == kWgrad>(0); T.template dma_tile<0, 13, MODE == kWgrad>(0); T.template dma_tile<0, 14, MODE == kWgrad>(0);
+  T.template dma_tile<0, 15, MODE == kWgrad>(0);
   T.dma_scale_p(0);
   T.dma_scale_q(0);
 }
@@ -700,12 +693,12 @@ constexpr int kStage1Dma = 16;
 template <int MODE>
 __device__ __forceinline__ void dma_second_stage(Tile<MODE>& T) {
   const int s1 = T.nk > 1 ? 1 : 0;
-  T.template dma_tile<1, 0>(s1); T.template dma_tile<1, 1>(s1); T.template dma_tile<1, 2>(s1);
-  T.template dma_tile<1, 3>(s1); T.template dma_tile<1, 4>(s1); T.template dma_tile<1, 5>(s1);
-  T.template dma_tile<1, 6>(s1); T.template dma_tile<1, 7>(s1); T.template dma_tile<1, 8>(s1);
-  T.template dma_tile<1, 9>(s1); T.template dma_tile<1, 10>(s1); T.template dma_tile<1, 11>(s1);
-  T.template dma_tile<1, 12>(s1); T.template dma_tile<1, 13>(s1); T.template dma_tile<1, 14>(s1);
-  T.template dma_tile<1, 15>(s1);
+  T.template dma_tile<1, 0, MODE == kWgrad>(s1); T.template dma_tile<1, 1, MODE == kWgrad>(s1); T.template dma_tile<1, 2, MODE == kWgrad>(s1);
+  T.template dma_tile<1, 3, MODE == kWgrad>(s1); T.template dma_tile<1, 4, MODE == kWgrad>(s1); T.template dma_tile<1, 5, MODE == kWgrad>(s1);
+  T.template dma_tile<1, 6, MODE == kWgrad>(s1); T.template dma_tile<1, 7, MODE == kWgrad>(s1); T.template dma_tile<1, 8, MODE == kWgrad>(s1);
+  T.template dma_tile<1, 9, MODE == kWgrad>(s1); T.template dma_tile<1, 10, MODE == kWgrad>(s1); T.template dma_tile<1, 11, MODE == kWgrad>(s1);
+  T.template dma_tile<1, 12, MODE == kWgrad>(s1); T.template dma_tile<1, 13, MODE == kWgrad>(s1); T.template dma_tile<1, 14, MODE == kWgrad>(s1);
+  T.template dma_tile<1, 15, MODE == kWgrad>(s1);
 }
 
 // Semi-persistent: the grid is a sequence of groups of S workgroups per XCD (S = 32 on
@@ -818,20 +811,11 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
         T.template read_scale_rows<true, 0, 4>(0, raw);
         T.template pack_scales<true, 0, 4>(raw, T.cq);
       }
-      if (MODE == kWgrad && (T.k_lo > 0 || T.k_hi < kBK)) {
-        for (int ks = 0; ks < nk; ks += 4) {
-          T.template stage<0, MODE == kWgrad>(ks);
-          if (ks + 1 < nk) T.template stage<1, MODE == kWgrad>(ks + 1);
-          if (ks + 2 < nk) T.template stage<2, MODE == kWgrad>(ks + 2);
-          if (ks + 3 < nk) T.template stage<3, MODE == kWgrad>(ks + 3);
-        }
-      } else {
-        for (int ks = 0; ks < nk; ks += 4) {
-          T.template stage<0, false>(ks);
-          if (ks + 1 < nk) T.template stage<1, false>(ks + 1);
-          if (ks + 2 < nk) T.template stage<2, false>(ks + 2);
-          if (ks + 3 < nk) T.template stage<3, false>(ks + 3);
-        }
+      for (int ks = 0; ks < nk; ks += 4) {
+        T.template stage<0>(ks);
+        if (ks + 1 < nk) T.template stage<1>(ks + 1);
+        if (ks + 2 < nk) T.template stage<2>(ks + 2);
+        if (ks + 3 < nk) T.template stage<3>(ks + 3);
       }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the tail's reload DMAs have landed
     }
