@@ -382,11 +382,11 @@ struct Tile {
       half0_from<B, S4, I + 1>();
     }
   }
-  // Second half-step: MFMAs on set B.  The DMA of stage ks+2 into buffer B (free now)
-  // and, when ks % 4 == 0, the next scale batch are issued over the first four MFMAs,
-  // giving them the rest of this stage and the first half of the next to land; the
-  // reads of stage ks+1's first half (other buffer) into set A follow over the first
-  // eight; in the last stage of a batch the next batch's scales are read and packed.
+  // Second half-step: MFMAs on set B.  The DMA of stage ks+2 into buffer B (free now) is
+  // spread over the sixteen MFMAs, kDmaPerSlot per slot, with the next scale batch among
+  // them when ks % 4 == 0 (it lands by the middle of the next stage); the reads of stage
+  // ks+1's first half (other buffer) into set A go out over the first eight; in the last
+  // stage of a batch the next batch's scales are read and packed.
   template <int B, int S4, int I>
   __device__ __forceinline__ void half1_from(int ks_dma, int ks_next) {
     if constexpr (I < 16) {
