@@ -1,8 +1,10 @@
 """ctypes binding of libff8.so: one Python function per C entry point, same names.
 
-Argument marshalling only: each function checks dtypes, shapes, devices and
-contiguity of the torch tensors it is given, passes raw device pointers and the
-current HIP stream to the C ABI, and raises Ff8Error on a non-zero status.  No
+Argument marshalling only: each function checks dtypes, devices and contiguity of
+the torch tensors it is given, and that every tensor's shape matches the extents the
+C ABI takes from the first operand (the C side receives plain pointers and cannot see
+an undersized buffer), passes raw device pointers and the current HIP stream to the
+C ABI, and raises Ff8Error on a non-zero status.  No
 function allocates, computes or falls back to anything: if libff8.so is missing
 the first call raises.
 """
@@ -111,6 +113,18 @@ def _ptr(t, dtype, name, ndim=None):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _shape(t, shape, name):
+    """t is None or has exactly this shape."""
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _numel(t, n, name):
+    """t is None or holds exactly n elements (any shape)."""
+    if t is not None and t.numel() != n:
+        raise ValueError(f"{name} must hold {n} elements, got {t.numel()}")
+
+
 _bf16, _u8, _f32, _i32 = torch.bfloat16, torch.uint8, torch.float32, torch.int32
 
 
@@ -132,12 +146,14 @@ def ff8_permute_workspace_bytes(T, k, E):
 
 def ff8_quant_rowwise(x, q, s, stream=None):
     rows, cols = x.shape
+    _shape(q, (rows, cols), "q"); _shape(s, (rows, cols // 128), "s")
     _check(load().ff8_quant_rowwise(_ptr(x, _bf16, "x", 2), rows, cols, _ptr(q, _u8, "q"), _ptr(s, _f32, "s"),
                                     _stream(stream)), "ff8_quant_rowwise")
 
 
 def ff8_quant_block128(w, q, s, stream=None):
     rows, cols = w.reshape(-1, w.shape[-1]).shape
+    _shape(q, w.shape, "q"); _numel(s, (rows // 128) * (cols // 128), "s")
     _check(load().ff8_quant_block128(_ptr(w, _bf16, "w"), rows, cols, _ptr(q, _u8, "q"), _ptr(s, _f32, "s"),
                                      _stream(stream)), "ff8_quant_block128")
 
@@ -148,6 +164,9 @@ def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src
     ff8_permute_quant_aligned."""
     T, H = x.shape
     M_cap = q.shape[0]
+    _numel(row_w, T * k, "row_w"); _numel(topk_idx, T * k, "topk_idx"); _numel(row_map, T * k, "row_map")
+    _numel(offsets, E + 1, "offsets"); _numel(src_row, M_cap, "src_row")
+    _shape(q, (M_cap, H), "q"); _shape(s, (M_cap, H // 128), "s")
     ws = 0 if workspace is None else workspace.numel() * workspace.element_size()
     args = [_ptr(x, _bf16, "x", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E, _ptr(topk_idx, _i32, "topk_idx"),
             int(reuse_map), _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
@@ -162,6 +181,9 @@ def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src
 def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y_perm, dprobs, stream=None):
     T, H = dy.shape
     M_cap = q.shape[0]
+    _numel(row_w, T * k, "row_w"); _numel(row_map, T * k, "row_map"); _numel(dprobs, T * k, "dprobs")
+    _numel(offsets, E + 1, "offsets"); _numel(src_row, M_cap, "src_row")
+    _shape(q, (M_cap, H), "q"); _shape(s, (M_cap, H // 128), "s"); _shape(y_perm, (M_cap, H), "y_perm")
     _check(load().ff8_permute_quant_dprobs(_ptr(dy, _bf16, "dy", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E,
                                            _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
                                            _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2),
@@ -171,6 +193,9 @@ def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y
 
 def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):
     rows, cols = q.shape
+    _shape(s, (rows, cols // 128), "s"); _shape(qT, (cols, rows), "qT"); _shape(sT, (rows // 128, cols), "sT")
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
     _check(load().ff8_scaling_aware_transpose(
         _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2), rows, cols, _ptr(offsets, _i32, "offsets"), E,
         _ptr(qT, _u8, "qT", 2), _ptr(sT, _f32, "sT", 2), _stream(stream)), "ff8_scaling_aware_transpose")
@@ -179,6 +204,8 @@ def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):
 def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):
     M_cap, K = a.shape
     E, N, _ = w.shape
+    _shape(a_s, (M_cap, K // 128), "a_s"); _shape(w, (E, N, K), "w"); _numel(w_s, E * (N // 128) * (K // 128), "w_s")
+    _numel(offsets, E + 1, "offsets"); _shape(out, (M_cap, N), "out")
     _check(load().ff8_grouped_gemm_fprop(
         _ptr(a, _u8, "a", 2), _ptr(a_s, _f32, "a_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, _f32, "w_s"),
         _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)),
@@ -188,6 +215,8 @@ def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):
 def ff8_grouped_gemm_dgrad(g, g_s, w, w_s, offsets, out, stream=None):
     M_cap, N = g.shape
     E, _, K = w.shape
+    _shape(g_s, (M_cap, N // 128), "g_s"); _shape(w, (E, N, K), "w"); _numel(w_s, E * (N // 128) * (K // 128), "w_s")
+    _numel(offsets, E + 1, "offsets"); _shape(out, (M_cap, K), "out")
     _check(load().ff8_grouped_gemm_dgrad(
         _ptr(g, _u8, "g", 2), _ptr(g_s, _f32, "g_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, _f32, "w_s"),
         _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)),
@@ -198,6 +227,8 @@ def ff8_grouped_gemm_wgrad(gT, gT_s, xT, xT_s, offsets, dw, accumulate=False, st
     N, M_cap = gT.shape
     K = xT.shape[0]
     E = dw.shape[0]
+    _shape(gT_s, (M_cap // 128, N), "gT_s"); _shape(xT, (K, M_cap), "xT"); _shape(xT_s, (M_cap // 128, K), "xT_s")
+    _numel(offsets, E + 1, "offsets"); _shape(dw, (E, N, K), "dw")
     _check(load().ff8_grouped_gemm_wgrad(
         _ptr(gT, _u8, "gT", 2), _ptr(gT_s, _f32, "gT_s"), _ptr(xT, _u8, "xT", 2), _ptr(xT_s, _f32, "xT_s"),
         _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(dw, _f32, "dw", 3), int(bool(accumulate)),
@@ -206,6 +237,9 @@ def ff8_grouped_gemm_wgrad(gT, gT_s, xT, xT_s, offsets, dw, accumulate=False, st
 
 def ff8_swiglu_quant(a, hq, hs, offsets=None, E=0, stream=None):
     M_cap, I2 = a.shape
+    _shape(hq, (M_cap, I2 // 2), "hq"); _shape(hs, (M_cap, I2 // 256), "hs")
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
     _check(load().ff8_swiglu_quant(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
                                    _ptr(hq, _u8, "hq", 2), _ptr(hs, _f32, "hs", 2), _stream(stream)),
            "ff8_swiglu_quant")
@@ -213,6 +247,9 @@ def ff8_swiglu_quant(a, hq, hs, offsets=None, E=0, stream=None):
 
 def ff8_swiglu_bwd_quant(a, dh, daq, das, offsets=None, E=0, stream=None):
     M_cap, I2 = a.shape
+    _shape(dh, (M_cap, I2 // 2), "dh"); _shape(daq, (M_cap, I2), "daq"); _shape(das, (M_cap, I2 // 128), "das")
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
     _check(load().ff8_swiglu_bwd_quant(_ptr(a, _bf16, "a", 2), _ptr(dh, _bf16, "dh", 2),
                                        _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2, _ptr(daq, _u8, "daq", 2),
                                        _ptr(das, _f32, "das", 2), _stream(stream)), "ff8_swiglu_bwd_quant")
@@ -220,6 +257,10 @@ def ff8_swiglu_bwd_quant(a, dh, daq, das, offsets=None, E=0, stream=None):
 
 def ff8_swiglu_quant_keep_fp8(a, hq, hs, a_q, a_s, offsets=None, E=0, stream=None):
     M_cap, I2 = a.shape
+    _shape(hq, (M_cap, I2 // 2), "hq"); _shape(hs, (M_cap, I2 // 256), "hs")
+    _shape(a_q, (M_cap, I2), "a_q"); _shape(a_s, (M_cap, I2 // 128), "a_s")
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
     _check(load().ff8_swiglu_quant_keep_fp8(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
                                             _ptr(hq, _u8, "hq", 2), _ptr(hs, _f32, "hs", 2), _ptr(a_q, _u8, "a_q", 2),
                                             _ptr(a_s, _f32, "a_s", 2), _stream(stream)), "ff8_swiglu_quant_keep_fp8")
@@ -227,6 +268,10 @@ def ff8_swiglu_quant_keep_fp8(a, hq, hs, a_q, a_s, offsets=None, E=0, stream=Non
 
 def ff8_swiglu_bwd_quant_fp8a(a_q, a_s, dh, daq, das, offsets=None, E=0, stream=None):
     M_cap, I2 = a_q.shape
+    _shape(a_s, (M_cap, I2 // 128), "a_s"); _shape(dh, (M_cap, I2 // 2), "dh")
+    _shape(daq, (M_cap, I2), "daq"); _shape(das, (M_cap, I2 // 128), "das")
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
     _check(load().ff8_swiglu_bwd_quant_fp8a(_ptr(a_q, _u8, "a_q", 2), _ptr(a_s, _f32, "a_s", 2),
                                             _ptr(dh, _bf16, "dh", 2), _ptr(offsets, _i32, "offsets"), E, M_cap,
                                             I2 // 2, _ptr(daq, _u8, "daq", 2), _ptr(das, _f32, "das", 2),
@@ -236,23 +281,27 @@ def ff8_swiglu_bwd_quant_fp8a(a_q, a_s, dh, daq, das, offsets=None, E=0, stream=
 def ff8_unpermute(y_perm, row_map, row_w, y, stream=None):
     M_cap, H = y_perm.shape
     T, k = row_map.shape
+    _numel(row_w, T * k, "row_w"); _shape(y, (T, H), "y")
     _check(load().ff8_unpermute(_ptr(y_perm, _bf16, "y_perm", 2), _ptr(row_map, _i32, "row_map", 2),
                                 _ptr(row_w, _f32, "row_w"), T, k, H, M_cap, _ptr(y, _bf16, "y", 2),
                                 _stream(stream)), "ff8_unpermute")
 
 
 def ff8_cast_f32_to_e4m3(x, q, stream=None):
+    _numel(q, x.numel(), "q")
     _check(load().ff8_cast_f32_to_e4m3(_ptr(x, _f32, "x"), x.numel(), _ptr(q, _u8, "q"), _stream(stream)),
            "ff8_cast_f32_to_e4m3")
 
 
 def ff8_cast_e4m3_to_f32(q, x, stream=None):
+    _numel(x, q.numel(), "x")
     _check(load().ff8_cast_e4m3_to_f32(_ptr(q, _u8, "q"), q.numel(), _ptr(x, _f32, "x"), _stream(stream)),
            "ff8_cast_e4m3_to_f32")
 
 
 def ff8_baseline_dequant_rowwise(q, s, out, stream=None):
     rows, cols = q.shape
+    _shape(s, (rows, cols // 128), "s"); _shape(out, (rows, cols), "out")
     _check(load().ff8_baseline_dequant_rowwise(_ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2), rows, cols,
                                                _ptr(out, _bf16, "out", 2), _stream(stream)),
            "ff8_baseline_dequant_rowwise")
@@ -260,12 +309,16 @@ def ff8_baseline_dequant_rowwise(q, s, out, stream=None):
 
 def ff8_baseline_transpose_bf16(x, out, stream=None):
     rows, cols = x.shape
+    _shape(out, (cols, rows), "out")
     _check(load().ff8_baseline_transpose_bf16(_ptr(x, _bf16, "x", 2), rows, cols, _ptr(out, _bf16, "out", 2),
                                               _stream(stream)), "ff8_baseline_transpose_bf16")
 
 
 def ff8_baseline_swiglu_bf16(a, h, offsets=None, E=0, stream=None):
     rows, I2 = a.shape
+    _shape(h, (rows, I2 // 2), "h")
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
     _check(load().ff8_baseline_swiglu_bf16(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, rows,
                                            I2 // 2, _ptr(h, _bf16, "h", 2), _stream(stream)),
            "ff8_baseline_swiglu_bf16")

@@ -73,3 +73,43 @@ def test_validation_errors_without_gpu(lib):
                                  None, 0, None) != 1
     assert lib.ff8_swiglu_quant(fake, None, 0, 128, 100, fake, fake, None) == 2
     assert lib.ff8_baseline_copy(fake, fake, 17, None) == 2
+    # operands of 4 GiB and more: the kernels address each operand with 32-bit byte offsets
+    assert lib.ff8_grouped_gemm_fprop(fake, fake, fake, fake, fake, 1, 1 << 22, 128, 1024, fake, None) == 2
+    assert b"4 GiB" in lib.ff8_last_error()
+    assert lib.ff8_grouped_gemm_fprop(fake, fake, fake, fake, fake, 1, (1 << 22) - 128, 128, 1024, fake, None) != 2
+    assert lib.ff8_grouped_gemm_dgrad(fake, fake, fake, fake, fake, 8, 128, 1 << 14, 1 << 15, fake, None) == 2
+    assert lib.ff8_grouped_gemm_wgrad(fake, fake, fake, fake, fake, 2, 1 << 25, 128, 128, fake, 0, None) == 2
+
+
+def test_binding_checks_every_shape():
+    """The C ABI receives plain pointers and cannot see an undersized buffer, so the binding
+    compares every tensor's shape with the extents it passes and raises before any call."""
+    torch = pytest.importorskip("torch")
+    u8, f32, bf16, i32 = torch.uint8, torch.float32, torch.bfloat16, torch.int32
+    e = lambda *shape, dtype=u8: torch.empty(shape, dtype=dtype)
+    M, K, N, E = 512, 256, 384, 4
+    bad_calls = [
+        lambda: ff8.ff8_quant_rowwise(e(M, K, dtype=bf16), e(M, K), e(M, 1, dtype=f32)),
+        lambda: ff8.ff8_quant_block128(e(N, K, dtype=bf16), e(N, K), e(2, 2, dtype=f32)),
+        lambda: ff8.ff8_scaling_aware_transpose(e(M, K), e(M, 2, dtype=f32), e(K, M - 128), e(4, K, dtype=f32)),
+        lambda: ff8.ff8_grouped_gemm_fprop(e(M, K), e(M, 2, dtype=f32), e(E, N, K), e(E, 3, 2, dtype=f32),
+                                           e(E + 1, dtype=i32), e(M - 128, N, dtype=bf16)),
+        lambda: ff8.ff8_grouped_gemm_dgrad(e(M, N), e(M, 3, dtype=f32), e(E, N, K), e(E, 3, 2, dtype=f32),
+                                           e(E, dtype=i32), e(M, K, dtype=bf16)),
+        lambda: ff8.ff8_grouped_gemm_wgrad(e(N, M), e(M // 128, N, dtype=f32), e(K, M), e(M // 128, K, dtype=f32),
+                                           e(E + 1, dtype=i32), e(E, K, N, dtype=f32)),
+        lambda: ff8.ff8_swiglu_quant(e(M, 2 * K, dtype=bf16), e(M, K), e(M, 1, dtype=f32)),
+        lambda: ff8.ff8_swiglu_bwd_quant(e(M, 2 * K, dtype=bf16), e(M, K, dtype=bf16), e(M, K), e(M, 4, dtype=f32)),
+        lambda: ff8.ff8_unpermute(e(M, K, dtype=bf16), e(128, 2, dtype=i32), e(128, 1, dtype=f32),
+                                  e(128, K, dtype=bf16)),
+        lambda: ff8.ff8_permute_quant(e(128, K, dtype=bf16), None, 2, E, e(128, 2, dtype=i32), False,
+                                      e(128, 2, dtype=i32), e(E + 1, dtype=i32), e(M - 1, dtype=i32), e(M, K),
+                                      e(M, 2, dtype=f32)),
+    ]
+    for i, call in enumerate(bad_calls):
+        with pytest.raises(ValueError, match="must (have shape|hold)"):
+            call()
+    # consistent shapes get past the shape checks (and stop at the device check here)
+    with pytest.raises(ValueError, match="device tensor"):
+        ff8.ff8_grouped_gemm_wgrad(e(N, M), e(M // 128, N, dtype=f32), e(K, M), e(M // 128, K, dtype=f32),
+                                   e(E + 1, dtype=i32), e(E, N, K, dtype=f32))
