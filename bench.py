@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--no-fp8-checkpoint", action="store_true")
     ap.add_argument("--no-router-grad", action="store_true")
     ap.add_argument("--no-align16", action="store_true")
+    ap.add_argument("--no-hip-graph", action="store_true")
     return ap.parse_args()
 
 
@@ -232,6 +233,32 @@ def align16(torch, d, shape, M, steps, warmup, ms_base):
     del L
     torch.cuda.empty_cache()
     return out
+
+
+def hip_graph(torch, L, d, steps, warmup, ms_eager, gemm_flops):
+    """The whole step captured once as a HIP graph and replayed.  The path makes no host
+    synchronization, allocation or memset, so one replay launches every kernel of the step
+    (the replays' outputs are checked against the eager step in the GPU tests)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run_step(L, d)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_step(L, d)
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    del graph
+    return {"ms_per_step": round(ms, 4), "TFLOP/s": round(gemm_flops / (ms * 1e-3) / 1e12, 2),
+            "ms_per_step_eager": round(ms_eager, 4)}
 
 
 def cast_ops(torch, reps=20):
@@ -464,6 +491,8 @@ def main():
                                          st_ms["B1_permute_quant_dy"])
     if not args.no_align16:
         rec["align16"] = align16(torch, d, shape, M, args.steps, args.warmup, ms_step)
+    if not args.no_hip_graph:
+        rec["hip_graph"] = hip_graph(torch, L, d, args.steps, args.warmup, ms_step, gemm_flops)
     if not args.no_cast_ops:
         del L, d
         torch.cuda.empty_cache()

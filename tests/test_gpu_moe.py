@@ -457,3 +457,39 @@ def test_layer_stagewise(case, mode):
     assert rel_frob(host(b["dw2"]), dW2) < GEMM_TOL
     dW1 = moe.grouped_gemm_wgrad(host(b["daTq"]), host(b["daTs"]).T, host(b["xTq"]), host(b["xTs"]).T, off)
     assert rel_frob(host(b["dw1"]), dW1) < GEMM_TOL
+
+
+@pytest.mark.parametrize("mode", ["paper_rows", "fp8_checkpoint_and_dprobs"])
+def test_layer_step_as_one_hip_graph(mode):
+    """The step makes no host synchronization, allocation or memset, so it can be captured
+    as one HIP graph.  Three replays, with eager work and synchronizations between them and
+    the outputs poisoned before each, reproduce the eager step bit for bit (every kernel is
+    deterministic)."""
+    shape, inp = _inputs("ragged")
+    ckpt = mode == "fp8_checkpoint_and_dprobs"
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt, router_grad=ckpt)
+    d = {k: dev(v) for k, v in inp.items()}
+    names = ["w1q", "w1s", "w2q", "w2s", "row_map", "offsets", "y", "dx", "dw1", "dw2"] + (["dprobs"] if ckpt else [])
+    step = lambda: L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    eager = {n: L.buf[n].clone() for n in names}
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    other = torch.randn(1 << 20, device="cuda")
+    for replay in range(3):
+        for n in names:
+            L.buf[n].view(torch.uint8).fill_(0xA5)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(L.buf[n].view(torch.uint8), eager[n].view(torch.uint8)), (replay, n)
+        other.mul_(1.5).add_(1.0)  # the program's own eager work between replays
+        torch.cuda.synchronize()
