@@ -862,15 +862,19 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
   g.accumulate = accumulate;
   g.P = b; g.sP = b_s; g.Q = a; g.sQ = a_s;
   unsigned grid;
+  // fprop / dgrad q tiles: expert e has ceil(rows_e / 256) <= rows_e / 256 + 1 of them, so
+  // at most M_cap / 256 + E in all, whatever the groups' padding (with 16-row padding and
+  // many small experts nearly every expert adds a partial tile)
+  const int64_t qt_bound = (M_cap + kTQ - 1) / kTQ + E;
   if (mode == kFprop) {  // out[m, n] = a[m, :] . w[e, n, :]
     g.Np = N; g.Kdim = K;
     g.n_pt = (int)((N + kTP - 1) / kTP);
-    grid = grid_blocks(blocks_of(g.n_pt, (M_cap + kTQ - 1) / kTQ + (E + 1) / 2), g.n_slots);
+    grid = grid_blocks(blocks_of(g.n_pt, qt_bound), g.n_slots);
     grouped_gemm_kernel<kFprop><<<grid, kThreads, 0, st>>>(g);
   } else if (mode == kDgrad) {  // out[m, k] = g[m, :] . w[e, :, k]
     g.Np = K; g.Kdim = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
-    grid = grid_blocks(blocks_of(g.n_pt, (M_cap + kTQ - 1) / kTQ + (E + 1) / 2), g.n_slots);
+    grid = grid_blocks(blocks_of(g.n_pt, qt_bound), g.n_slots);
     grouped_gemm_kernel<kDgrad><<<grid, kThreads, 0, st>>>(g);
   } else {  // dw[e, n, k] = sum_m gT[n, m] xT[k, m]
     g.Np = K; g.Nq = N;

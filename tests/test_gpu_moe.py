@@ -31,6 +31,9 @@ CASES = {
     "tiny": (workloads.TINY, None),
     "ragged": (workloads.LayerShape("ragged T300 H384 E6 k2 I384", 300, 384, 6, 2, 384, "iid"), 7),
     "one_expert": (workloads.LayerShape("one expert T200 H256 E1 k1 I256", 200, 256, 1, 1, 256, "iid"), None),
+    # the most experts the kernels take (per-expert tables of E + 1 entries): ~4 rows each, many empty
+    "max_experts": (workloads.LayerShape("max experts T2048 H256 E1024 k2 I256", 2048, 256, 1024, 2, 256, "iid"),
+                    None),
 }
 
 
