@@ -31,6 +31,9 @@ CASES = {
     "tiny": (workloads.TINY, None),
     "ragged": (workloads.LayerShape("ragged T300 H384 E6 k2 I384", 300, 384, 6, 2, 384, "iid"), 7),
     "one_expert": (workloads.LayerShape("one expert T200 H256 E1 k1 I256", 200, 256, 1, 1, 256, "iid"), None),
+    # the narrowest widths: H = I = 128, one K block in fc1 fprop, fc2 fprop and fc2 dgrad, and a
+    # 128-column W_e in dgrad (half of a 256-wide output tile)
+    "min_width": (workloads.LayerShape("min width T257 H128 E3 k2 I128", 257, 128, 3, 2, 128, "iid"), None),
     # the most experts the kernels take (per-expert tables of E + 1 entries): ~4 rows each, many empty
     "max_experts": (workloads.LayerShape("max experts T2048 H256 E1024 k2 I256", 2048, 256, 1024, 2, 256, "iid"),
                     None),
@@ -84,6 +87,29 @@ def test_permute_quant_build_and_reuse(case):
     assert np.array_equal(host(dq[:m_pad]), wq2)
     assert np.array_equal(host(dsc[:m_pad]), ws2)
     assert untouched(dq[m_pad:])
+
+
+@pytest.mark.parametrize("align", [16, 32, 64])
+@pytest.mark.parametrize("case", ["ragged", "max_experts"])
+def test_permute_quant_aligned(case, align):
+    """Every group alignment the API takes: offsets, maps and the quantized rows bit-exact,
+    padding rows zero, rows past the padded total untouched."""
+    shape, inp = _inputs(case)
+    M_cap = ff8.ff8_rows_bound_aligned(shape.T, shape.k, shape.E, align)
+    _, row_map, offsets, _, ws = _routing_device(shape, inp)
+    src_row = poisoned((M_cap,), torch.int32)
+    q = poisoned((M_cap, shape.H), torch.uint8)
+    s = poisoned((M_cap, shape.H // 128), torch.float32)
+    ff8.ff8_permute_quant(dev(inp["x"]), None, shape.k, shape.E, dev(inp["topk_idx"]), False, row_map, offsets,
+                          src_row, q, s, ws, align=align)
+    torch.cuda.synchronize()
+    counts, w_off, w_map, w_src = moe.route(host(inp["topk_idx"]), shape.E, align)
+    m_pad = int(w_off[-1])
+    assert np.all(w_off % align == 0) and np.array_equal(host(offsets), w_off)
+    assert np.array_equal(host(row_map), w_map) and np.array_equal(host(src_row)[:m_pad], w_src)
+    wq, ws_ = moe.permute_quant_rows(f64(inp["x"]), w_src, shape.k)
+    assert np.array_equal(host(q[:m_pad]), wq) and np.array_equal(host(s[:m_pad]), ws_)
+    assert untouched(q[m_pad:]) and untouched(s[m_pad:]) and untouched(src_row[m_pad:])
 
 
 def test_permute_padding_spans_block():
