@@ -23,7 +23,8 @@
  *    over rows 128b..128b+127.  Block (128x128) scaled weights: q [E, N, K],
  *    s [E, N/128, K/128].
  *  - Grouped (expert-contiguous) tensors have M_cap rows; expert e owns rows
- *    [offsets[e], offsets[e+1]), every group is padded to a multiple of 128 rows,
+ *    [offsets[e], offsets[e+1]), every group is padded to a multiple of the
+ *    alignment (128 rows, or 16, 32 or 64 through ff8_permute_quant_aligned),
  *    and offsets ([E+1] int32) live in DEVICE memory.  Kernels read offsets[E]
  *    (= M_pad) on the device; rows in [M_pad, M_cap) are neither read nor
  *    written.  Grids are sized from M_cap, so no call synchronizes with the host.
