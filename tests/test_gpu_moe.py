@@ -31,6 +31,9 @@ CASES = {
     "tiny": (workloads.TINY, None),
     "ragged": (workloads.LayerShape("ragged T300 H384 E6 k2 I384", 300, 384, 6, 2, 384, "iid"), 7),
     "one_expert": (workloads.LayerShape("one expert T200 H256 E1 k1 I256", 200, 256, 1, 1, 256, "iid"), None),
+    # every token routed to every expert (k = E), and a single token
+    "all_experts": (workloads.LayerShape("all experts T130 H256 E4 k4 I256", 130, 256, 4, 4, 256, "iid"), None),
+    "one_token": (workloads.LayerShape("one token T1 H256 E4 k2 I256", 1, 256, 4, 2, 256, "iid"), None),
     # the narrowest widths: H = I = 128, one K block in fc1 fprop, fc2 fprop and fc2 dgrad, and a
     # 128-column W_e in dgrad (half of a 256-wide output tile)
     "min_width": (workloads.LayerShape("min width T257 H128 E3 k2 I128", 257, 128, 3, 2, 128, "iid"), None),
