@@ -90,6 +90,9 @@ struct GemmArgs {
   int n_pt, n_qt;     // p tiles; q tiles (wgrad only)
   int accumulate;
   int n_slots;        // workgroups per XCD in one group of the grid
+  // wgrad expert shares (share = 0: none fit): each XCD takes one rect_q x rect_p-tile
+  // rectangle of every expert's n_qt x n_pt tiles, the 8 rectangles tiling it (rect_b along p)
+  int share, rect_q, rect_p, rect_b;
 };
 
 // K-major stage tile: 256 rows x 128 bytes, 16-byte chunk c of row r at c ^ kswz(r).  Any
@@ -436,6 +439,19 @@ struct TileInfo {
   int k_lo, k_hi;             // wgrad: valid K bytes of the first / last stage
 };
 
+// wgrad: the K range of expert e's tiles.  K runs over whole 128-token blocks from the one
+// holding offsets[e]; with groups padded to 16 the first and last may be shared with
+// neighbouring experts (masked in their DMAs).
+__device__ __forceinline__ void wgrad_k_range(const GemmArgs& g, int e, TileInfo& t) {
+  const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
+  const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
+  const int kb0 = o0 & ~(kBK - 1);
+  t.k0 = kb0;
+  t.nk = o1 > o0 ? (o1 - kb0 + kBK - 1) / kBK : 0;
+  t.k_lo = o0 - kb0;
+  t.k_hi = o1 > o0 ? o1 - (kb0 + (t.nk - 1) * kBK) : kBK;
+}
+
 // Tile w_in of XCD block blk (kBQ x kBP tiles, p fastest).  False for tiles past the
 // edges.  fprop/dgrad: q tiles are 256-row tiles of the expert groups (g_cum / g_off:
 // cumulative tile counts and row offsets per expert, in LDS).
@@ -469,15 +485,7 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in
     t.e = e;
     t.q0 = (int64_t)(qg - e * g.n_qt) * kTQ;
     t.q_end = g.Nq;
-    const int o0 = __builtin_amdgcn_readfirstlane(g.offsets[e]);
-    const int o1 = __builtin_amdgcn_readfirstlane(g.offsets[e + 1]);
-    // K runs over whole 128-token blocks from the one holding o0; with groups padded to 16
-    // the first and last may be shared with neighbouring experts (masked in the loop)
-    const int kb0 = o0 & ~(kBK - 1);
-    t.k0 = kb0;
-    t.nk = o1 > o0 ? (o1 - kb0 + kBK - 1) / kBK : 0;
-    t.k_lo = o0 - kb0;
-    t.k_hi = o1 > o0 ? o1 - (kb0 + (t.nk - 1) * kBK) : kBK;
+    wgrad_k_range(g, e, t);
   }
   return true;
 }
@@ -711,6 +719,13 @@ __device__ __forceinline__ void dma_second_stage(Tile<MODE>& T) {
 // the 8 XCDs together sweep one 16 x 16-tile window (about one expert).  Bounding a
 // workgroup to a few rounds keeps an XCD's workgroups from drifting apart (which costs L2
 // sharing) and lets faster CUs take more groups.
+// wgrad under skewed routing: every expert has the same tile count, so an expert's blocks
+// rarely divide evenly over the 8 XCDs, and the largest experts' extra blocks pile up on a
+// few of them.  When the largest expert has more than twice the mean rows (decided in every
+// workgroup from the offsets, identically), each XCD instead takes one of 8 equal rectangles
+// of every expert's tile grid (at least one round of 32 tiles each), which balances the XCDs
+// exactly; with near-uniform routing the blocks, which share more operand panels per round,
+// are kept.
 // Between tiles, the next tile's first stage (and scale batch) streams into stage buffer 0
 // while the finished tile's output is staged through buffer 1 and stored; its second
 // stage follows once the epilogue has left buffer 1.  All control flow is
@@ -724,13 +739,35 @@ constexpr int kRoundsPerWg = 4;           // work rounds (tiles) per workgroup
 // no memory access moves across the barrier.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// wgrad, expert-share schedule: item i of XCD x is tile l = i % share of expert e = i / share
+// in XCD x's rectangle (p fastest).  Every expert's tiles are split evenly over the 8 XCDs,
+// so the XCDs' loads stay equal however skewed the routing is (with XCD blocks, an expert's
+// block count is rarely a multiple of 8, and the largest experts' extra blocks pile up on a
+// few XCDs).
+__device__ __forceinline__ void decode_share_tile(const GemmArgs& g, int xcd, int i, TileInfo& t) {
+  const int e = i / g.share, l = i - e * g.share;
+  const int lq = l / g.rect_p, lp = l - lq * g.rect_p;
+  const int rq = xcd / g.rect_b, rp = xcd - rq * g.rect_b;
+  t.blk = 0;
+  t.e = e;
+  t.p0 = (rp * g.rect_p + lp) * kTP;
+  t.q0 = (rq * g.rect_q + lq) * kTQ;
+  t.q_end = g.Nq;
+  wgrad_k_range(g, e, t);
+}
+
 // Next tile of this workgroup from round k on, below round k_end (k advances past empty
 // edge tiles).
 template <int MODE>
 __device__ __forceinline__ bool next_tile(const GemmArgs& g, int xcd, int slot, int n_slots, int n_blocks, int k_end,
-                                          int& k, TileInfo& t) {
+                                          bool use_share, int& k, TileInfo& t) {
   for (; k < k_end; ++k) {
     const int i = k * n_slots + slot;
+    if (MODE == kWgrad && use_share) {
+      if (i >= g.E * g.share) return false;
+      decode_share_tile(g, xcd, i, t);
+      return true;
+    }
     const int blk = (i / kPersistSlots) * 8 + xcd;
     if (blk >= n_blocks) return false;
     if (decode_tile<MODE>(g, blk, i % kPersistSlots, t)) return true;
@@ -781,10 +818,28 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   } else {
     n_qg = g.E * g.n_qt;
   }
+  // wgrad: expert shares when the largest expert has more than twice the mean rows (one
+  // wave reduces the offsets; the flag is the same in every workgroup of the launch)
+  bool use_share = false;
+  if (MODE == kWgrad && g.share > 0) {
+    if (tid < 64) {
+      int mx = 0;
+      for (int base = 0; base < g.E; base += 64) {
+        const int i = base + tid;
+        const int r = i < g.E ? g.offsets[i + 1] - g.offsets[i] : 0;
+        mx = max(mx, r);
+      }
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) mx = max(mx, __shfl_xor(mx, d));
+      if (tid == 0) g_cum[0] = (int64_t)mx * g.E > 2 * (int64_t)(g.offsets[g.E] - g.offsets[0]);
+    }
+    __syncthreads();
+    use_share = __builtin_amdgcn_readfirstlane(g_cum[0]) != 0;
+  }
   const int n_blocks = ((g.n_pt + kBP - 1) / kBP) * ((n_qg + kBQ - 1) / kBQ);
   int k = group * kRoundsPerWg;
   TileInfo t;
-  if (!next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, k, t)) return;
+  if (!next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, use_share, k, t)) return;
   setup_tile<MODE>(T, g, t);
   if (T.nk > 0) dma_first_stage<MODE>(T);
   // Loop invariant: tile t is set up, its stage 0 and scale batch 0 are in flight (if it
@@ -822,7 +877,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     lds_barrier();  // every wave is done with the stage buffers and the scale batches
     TileInfo tn;
     ++k;
-    const bool more = next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, k, tn);
+    const bool more = next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, use_share, k, tn);
     if (more) {
       setup_tile<MODE>(T, g, tn);
       if (T.nk > 0) dma_first_stage<MODE>(T);  // buffer 0 and scale batch 0, under the epilogue
@@ -835,17 +890,19 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
 }
 
 // Grid: groups of n_slots workgroups per XCD (one per CU, the same number on each of the
-// 8 XCDs, at most kPersistSlots), enough groups of kRoundsPerWg rounds for n_blocks_max XCD
-// blocks (workgroups past the work actually present exit at once).
-unsigned grid_blocks(int64_t n_blocks_max, int& n_slots) {
+// 8 XCDs, at most kPersistSlots), enough groups of kRoundsPerWg rounds for `items` tiles per
+// XCD, or for n_blocks_max XCD blocks (workgroups past the work actually present exit at once).
+unsigned grid_items(int64_t items, int& n_slots) {  // items: work items (tiles) per XCD
   int cus = (device_cu_count() / 8) * 8;
   if (cus > 8 * kPersistSlots) cus = 8 * kPersistSlots;
   if (cus < 8) cus = 8;
   n_slots = cus / 8;
-  const int64_t items = (n_blocks_max + 7) / 8 * kPersistSlots;  // work items per XCD
   const int64_t rounds = (items + n_slots - 1) / n_slots;
   const int64_t groups = (rounds + kRoundsPerWg - 1) / kRoundsPerWg;
   return (unsigned)((groups > 0 ? groups : 1) * 8 * n_slots);
+}
+unsigned grid_blocks(int64_t n_blocks_max, int& n_slots) {
+  return grid_items((n_blocks_max + 7) / 8 * kPersistSlots, n_slots);
 }
 int64_t blocks_of(int n_pt, int64_t n_qg) { return (int64_t)((n_pt + kBP - 1) / kBP) * ((n_qg + kBQ - 1) / kBQ); }
 
@@ -880,7 +937,24 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
     g.Np = K; g.Nq = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
     g.n_qt = (int)((N + kTQ - 1) / kTQ);
-    grid = grid_blocks(blocks_of(g.n_pt, (int64_t)E * g.n_qt), g.n_slots);
+    // expert shares: the a x b split (a b = 8) of an expert's tiles into equal rectangles
+    // whose 32-tile rounds touch the fewest operand panels (ceil(32 / rect_p) + rect_p);
+    // XCD blocks when no split divides the tile grid
+    int best = 1 << 30;
+    for (int a = 1; a <= 8; a *= 2) {
+      const int b = 8 / a;
+      if (g.n_qt % a != 0 || g.n_pt % b != 0 || (g.n_qt / a) * (g.n_pt / b) < kPersistSlots) continue;
+      const int rq = g.n_qt / a, rp = g.n_pt / b;
+      const int panels = (kPersistSlots + rp - 1) / rp + rp;
+      if (panels < best) {
+        best = panels;
+        g.rect_q = rq; g.rect_p = rp; g.rect_b = b; g.share = rq * rp;
+      }
+    }
+    // either schedule may be chosen on the device: the grid covers both
+    const int64_t blocks_items = (blocks_of(g.n_pt, (int64_t)E * g.n_qt) + 7) / 8 * kPersistSlots;
+    const int64_t share_items = (int64_t)E * g.share;
+    grid = grid_items(share_items > blocks_items ? share_items : blocks_items, g.n_slots);
     grouped_gemm_kernel<kWgrad><<<grid, kThreads, 0, st>>>(g);
   }
   return hipGetLastError();

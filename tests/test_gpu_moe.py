@@ -525,3 +525,33 @@ def test_layer_step_as_one_hip_graph(mode):
             assert torch.equal(L.buf[n].view(torch.uint8), eager[n].view(torch.uint8)), (replay, n)
         other.mul_(1.5).add_(1.0)  # the program's own eager work between replays
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("rows", [[2048, 128, 0, 256], [2000, 128, 0, 272], [512, 512, 512, 512]],
+                         ids=["skewed", "skewed_align16", "uniform"])
+def test_wgrad_tile_schedules(rows):
+    """dW of four experts with 4096 x 4096 weights (16 x 16 tiles each).  When the largest
+    expert has more than twice the mean rows, the kernel splits every expert's tiles over
+    the 8 XCDs in equal 8 x 4-tile rectangles; otherwise it walks XCD blocks.  Both orders,
+    with 128- and 16-row groups, against the oracle over the whole output; operands are
+    random e4m3 codes with random power-of-two column-wise scales (rows outside the groups
+    hold data too, which the kernel must not add)."""
+    E, N, K = len(rows), 4096, 4096
+    off = np.concatenate([[0], np.cumsum(rows)]).astype(np.int64)
+    M_cap = int(-(-(off[-1] + 128) // 128) * 128)
+    rng = np.random.default_rng(sum(rows))
+    code = lambda shape: rng.choice(np.r_[0:127, 128:255].astype(np.uint8), size=shape)
+    gT, xT = code((N, M_cap)), code((K, M_cap))
+    gTs = np.exp2(rng.integers(-8, 0, size=(M_cap // 128, N))).astype(np.float32)
+    xTs = np.exp2(rng.integers(-4, 4, size=(M_cap // 128, K))).astype(np.float32)
+    dw = torch.full((E, N, K), 7.0, dtype=torch.float32, device="cuda")
+    ff8.ff8_grouped_gemm_wgrad(dev(torch.from_numpy(gT)), dev(torch.from_numpy(gTs)), dev(torch.from_numpy(xT)),
+                               dev(torch.from_numpy(xTs)), dev(torch.from_numpy(off.astype(np.int32))), dw)
+    torch.cuda.synchronize()
+    want = moe.grouped_gemm_wgrad(gT, gTs.T, xT, xTs.T, off)
+    got = host(dw)
+    for e in range(E):
+        if rows[e] == 0:
+            assert not got[e].any(), e
+        else:
+            assert rel_frob(got[e], want[e]) < GEMM_TOL, e
