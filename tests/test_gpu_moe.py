@@ -34,6 +34,8 @@ CASES = {
     # every token routed to every expert (k = E), and a single token
     "all_experts": (workloads.LayerShape("all experts T130 H256 E4 k4 I256", 130, 256, 4, 4, 256, "iid"), None),
     "one_token": (workloads.LayerShape("one token T1 H256 E4 k2 I256", 1, 256, 4, 2, 256, "iid"), None),
+    # the widest top-k the router-gradient kernel takes (k = 64), every expert chosen by every token
+    "widest_topk": (workloads.LayerShape("widest top-k T300 H256 E64 k64 I256", 300, 256, 64, 64, 256, "iid"), None),
     # the narrowest widths: H = I = 128, one K block in fc1 fprop, fc2 fprop and fc2 dgrad, and a
     # 128-column W_e in dgrad (half of a 256-wide output tile)
     "min_width": (workloads.LayerShape("min width T257 H128 E3 k2 I128", 257, 128, 3, 2, 128, "iid"), None),
