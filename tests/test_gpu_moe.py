@@ -16,6 +16,7 @@ from test_gpu_kernels import dev, host, f64, rel_frob, poisoned, untouched
 pytestmark = pytest.mark.gpu
 
 GEMM_TOL = 2e-3   # max relative Frobenius error of a GEMM output against the float64 oracle
+MAX_H_DPROBS = 8192  # the router-gradient kernel keeps one row of dY in registers (16 columns per lane)
 
 
 def _skewed_routing(T, k, E, seed):
@@ -34,6 +35,9 @@ CASES = {
     # every token routed to every expert (k = E), and a single token
     "all_experts": (workloads.LayerShape("all experts T130 H256 E4 k4 I256", 130, 256, 4, 4, 256, "iid"), None),
     "one_token": (workloads.LayerShape("one token T1 H256 E4 k2 I256", 1, 256, 4, 2, 256, "iid"), None),
+    # a hidden size past what one-pass row kernels cover (the permute and unpermute loop over
+    # 16-column chunks; fc1 contracts over 128 K blocks); wider than the router gradient takes
+    "wide_hidden": (workloads.LayerShape("wide hidden T64 H16384 E2 k2 I256", 64, 16384, 2, 2, 256, "iid"), None),
     # the widest top-k the router-gradient kernel takes (k = 64), every expert chosen by every token
     "widest_topk": (workloads.LayerShape("widest top-k T300 H256 E64 k64 I256", 300, 256, 64, 64, 256, "iid"), None),
     # the narrowest widths: H = I = 128, one K block in fc1 fprop, fc2 fprop and fc2 dgrad, and a
@@ -315,6 +319,14 @@ def test_permute_quant_dprobs(case):
     summation bound, 0 for dropped slots."""
     shape, inp = _inputs(case)
     T, H, E, k = shape.T, shape.H, shape.E, shape.k
+    if H > MAX_H_DPROBS:  # rejected on the host, before any launch
+        M_cap, row_map, offsets, src_row, _ = _routing_device(shape, inp)
+        e = lambda *sh, dt=torch.float32: torch.empty(sh, dtype=dt, device="cuda")
+        with pytest.raises(ff8.Ff8Error, match="bad shape"):
+            ff8.ff8_permute_quant_dprobs(dev(inp["dy"]), dev(inp["probs"]), k, E, row_map, offsets, src_row,
+                                         e(M_cap, H, dt=torch.uint8), e(M_cap, H // 128),
+                                         e(M_cap, H, dt=torch.bfloat16), e(T, k))
+        return
     idx = inp["topk_idx"].clone()
     idx[::7, 0] = -1  # dropped slots
     M_cap, row_map, offsets, src_row, ws = _routing_device(shape, inp)
@@ -434,7 +446,8 @@ def test_layer_stagewise(case, mode):
     shape, inp = _inputs(case)
     ckpt = mode == "fp8_checkpoint_and_dprobs"
     align = 16 if mode == "align16" else 128
-    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt, router_grad=ckpt,
+    rgrad = ckpt and shape.H <= MAX_H_DPROBS
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, fp8_checkpoint=ckpt, router_grad=rgrad,
                        align=align)
     d = {k: dev(v) for k, v in inp.items()}
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
@@ -463,7 +476,7 @@ def test_layer_stagewise(case, mode):
     assert rel_frob(f64(b["y"]), y) < 1e-3
     dyq, dys = moe.permute_quant_rows(f64(inp["dy"]), w_src, shape.k, row_w=host(inp["probs"]))
     assert np.array_equal(host(b["dyq"][:m_pad]), dyq) and np.array_equal(host(b["dys"][:m_pad]), dys)
-    if ckpt:
+    if rgrad:
         yp64 = f64(b["y_perm"][:m_pad])
         want = moe.router_grad(f64(inp["dy"]), yp64, w_map)
         mag = moe.router_grad(np.abs(f64(inp["dy"])), np.abs(yp64), w_map)
