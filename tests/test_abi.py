@@ -68,6 +68,14 @@ def test_validation_errors_without_gpu(lib):
     assert lib.ff8_permute_quant(fake, None, 16, 128, 2, 4, fake, 0, fake, fake, fake, 640, fake, fake,
                                  fake, 0, None) == 3
     assert lib.ff8_unpermute(fake, fake, None, 4, 0, 128, 128, fake, None) == 3
+    # T * k and M_cap must stay below 2^31 (int32 row maps and row indices)
+    big_T = 1 << 28
+    m_cap = lib.ff8_rows_bound(big_T, 8, 8)
+    assert lib.ff8_permute_quant(fake, None, big_T, 128, 8, 8, fake, 1, fake, fake, fake, m_cap, fake, fake,
+                                 None, 0, None) == 2
+    # the router gradient keeps a row of dY in registers: H above 8192 is rejected
+    assert lib.ff8_permute_quant_dprobs(fake, fake, 16, 8320, 2, 4, fake, fake, fake, 4096, fake, fake, fake, fake,
+                                        None) == 2
     # an empty batch passes validation with NULL token-indexed arrays (no GPU here: the launch fails)
     assert lib.ff8_permute_quant(None, None, 0, 128, 2, 4, None, 0, None, fake, fake, 512, fake, fake,
                                  None, 0, None) != 1
