@@ -121,3 +121,35 @@ def test_binding_checks_every_shape():
     with pytest.raises(ValueError, match="device tensor"):
         ff8.ff8_grouped_gemm_wgrad(e(N, M), e(M // 128, N, dtype=f32), e(K, M), e(M // 128, K, dtype=f32),
                                    e(E + 1, dtype=i32), e(E, N, K, dtype=f32))
+
+
+def test_header_compiles_as_c_and_links(tmp_path):
+    """include/ff8.h is plain C: a C99 program includes it, links libff8.so and calls the
+    host-only entry points (no GPU needed for these)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "abi.c"
+    src.write_text(r"""
+#include <stdio.h>
+#include <string.h>
+#include "ff8.h"
+int main(void) {
+  if (ff8_version() <= 0) return 1;
+  if (ff8_rows_bound(1024, 2, 8) != ff8_rows_bound_aligned(1024, 2, 8, 128)) return 2;
+  if (ff8_rows_bound_aligned(1024, 2, 8, 48) != -1) return 3;
+  int rc = ff8_quant_rowwise(NULL, 4, 128, (ff8_e4m3*)16, (float*)16, NULL);
+  if (rc != FF8_ERR_NULL || strlen(ff8_last_error()) == 0) return 4;
+  printf("%s\n", ff8_status_string(rc));
+  return 0;
+}
+""")
+    exe = tmp_path / "abi"
+    lib_dir = os.path.dirname(ff8.library_path())
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                        "-L", lib_dir, "-lff8", "-Wl,-rpath," + lib_dir], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip() == "null pointer", (r.returncode, r.stdout, r.stderr)
