@@ -570,3 +570,13 @@ def test_wgrad_tile_schedules(rows):
             assert not got[e].any(), e
         else:
             assert rel_frob(got[e], want[e]) < GEMM_TOL, e
+    # accumulating into the same gradient doubles it (experts without rows keep their zeros)
+    args = [dev(torch.from_numpy(a)) for a in (gT, gTs, xT, xTs, off.astype(np.int32))]
+    ff8.ff8_grouped_gemm_wgrad(*args, dw, accumulate=True)
+    torch.cuda.synchronize()
+    got = host(dw)
+    for e in range(E):
+        if rows[e] == 0:
+            assert not got[e].any(), e
+        else:
+            assert rel_frob(got[e], 2 * want[e]) < GEMM_TOL, e
