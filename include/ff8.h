@@ -240,7 +240,10 @@ int ff8_swiglu_quant(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M
                      ff8_e4m3* hq, float* hs, void* stream);
 
 /*
- * ff8_swiglu_bwd_quant -- backward twin of the fused SwiGLU kernel: with
+ * ff8_swiglu_bwd_quant -- backward twin of the fused SwiGLU kernel (paper section 3.3.2:
+ *   the activation's FP8 output is produced inside the activation kernel, here for its
+ *   gradient, which the fc1 dgrad consumes as row-wise FP8 per section 3.2).  The
+ *   gradient itself is the derivative of h = silu(g) * u (the paper does not print it):
  *   sig = 1 / (1 + exp(-g)), dg = dh * u * sig * (1 + g * (1 - sig)),
  *   du = dh * g * sig, in float32, quantized 1x128 into daq = [dg | du].
  *   a [M_cap, 2I] bf16, dh [M_cap, I] bf16; daq [M_cap, 2I] e4m3 + das [M_cap, 2I/128].
@@ -270,7 +273,8 @@ int ff8_swiglu_bwd_quant_fp8a(const ff8_e4m3* a_q, const float* a_s, const ff8_b
                               int E, int64_t M_cap, int64_t I, ff8_e4m3* daq, float* das, void* stream);
 
 /*
- * ff8_unpermute -- fused unpermute + unpadding (paper section 3.3.1):
+ * ff8_unpermute -- fused unpermute + unpadding (paper section 3.3.1); M_cap is the row
+ *   count of y_perm, against which every row_map entry is checked on the device:
  *   y[t] = sum_{j < k, row_map[t,j] >= 0} w[t, j] * y_perm[row_map[t, j]],
  *   accumulated in float32 in slot order, rounded once to bf16; w = 1 when
  *   row_w is NULL.  y_perm [M_cap, H] bf16, row_map [T, k] int32 (entries must

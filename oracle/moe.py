@@ -7,9 +7,12 @@ combine) and section 3.3 (fused permute+padding, fused unpermute+unpadding,
 fused SwiGLU+quantization).
 
 Readings where the paper is silent:
-  * padding multiple: every expert group is padded to a multiple of 128 rows
-    (the paper pads to 16 for GEMM shape reasons; 128 keeps every 128-row
-    transpose block and every 128-token wgrad scale block inside one expert);
+  * padding multiple: by default every expert group is padded to a multiple of
+    128 rows, which keeps every 128-row transpose block and every 128-token
+    wgrad scale block inside one expert; `align` = 16 is the paper's padding
+    (section 3.3.1), and then a 128-token block may hold tokens of two experts
+    (wgrad sums each expert over exactly its own tokens, each scaled by the
+    column scale of its 128-token block);
   * order inside a group: ascending token index (stable), one row per routed
     (token, slot) pair; a slot with expert id -1 is dropped (row_map = -1);
   * padding rows: bytes 0x00 with scale 2^-126 (an all-zero tile);

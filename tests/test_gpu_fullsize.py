@@ -39,6 +39,8 @@ def run(request):
     shape, align = SHAPES[request.param]
     print(f"\nfull-size layer step: {shape.name}, groups padded to {align}", flush=True)
     d = workloads.layer_inputs(shape, seed=0, device="cuda")
+    if shape.routing == "zipf":  # the stress case's populations, on the very routing the GPU runs
+        print(f"expert populations: {workloads.check_skew(d['topk_idx'], shape.E)}", flush=True)
     L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, align=align)
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
@@ -87,9 +89,9 @@ def test_weight_quant_sampled_blocks(run):
 
 
 def test_permute_quant_sampled_rows(run):
-    """F1 (plain) and B1 (routing-weighted) rows: bytes and scales bit-exact."""
+    """F1 (plain) and B1 (routing-weighted) rows: bytes and scales bit-exact on 2048 rows."""
     shape, d, b = run["shape"], run["d"], run["b"]
-    m, _ = _sample_rows(run, 128)
+    m, _ = _sample_rows(run, 2048)
     src = run["src_row"][m]
     t, j = src // shape.k, src % shape.k
     local = np.arange(m.size) * shape.k + j  # sampled row i reads local token i
@@ -184,7 +186,10 @@ def _wgrad_samples(run, gT, xT, out):
         x = codec.e4m3_decode(host(b[xT + "q"][_cuda_idx(c), lo:hi])) * \
             host(b[xT + "s"].index_select(0, blk)[:, _cuda_idx(c)]).T.astype(np.float64)
         _check_gemm_samples(got, np.sum(g * x, axis=1), np.sum(np.abs(g * x), axis=1), False, hi - lo)
-    for e in np.nonzero(off[1:] == off[:-1])[0]:
+    empty = np.nonzero(off[1:] == off[:-1])[0]
+    if run["shape"].routing == "zipf":
+        assert empty.size > 0, "the skewed layer must have experts without tokens"
+    for e in empty:
         assert not bool(b[out][int(e)].any()), f"expert {e} has no rows but a nonzero gradient"
 
 
@@ -273,20 +278,17 @@ def test_unpermute_sampled_tokens(run):
 
 
 def test_sat_sampled_blocks(run):
-    """B6: sampled 128x128 blocks of all four transposed tensors bit-exact, scales included."""
+    """B6: all four transposed tensors bit-exact, scales included, on 8 random whole 128-row
+    stripes (every column tile) and the last stripe (partial with groups padded to 16)."""
     b, rng = run["b"], run["rng"]
     m_pad = int(run["off"][-1])
+    n_rb = -(-m_pad // 128)
+    stripes = sorted(set(rng.choice(n_rb, size=min(8, n_rb), replace=False).tolist()) | {n_rb - 1})
     for name in ("x", "h", "dy", "da"):
         q, s, qT, sT = b[name + "q"], b[name + "s"], b[name + "Tq"], b[name + "Ts"]
-        for _ in range(6):
-            rb, cb = int(rng.integers(m_pad // 128)), int(rng.integers(q.shape[1] // 128))
-            rs, cs = slice(rb * 128, (rb + 1) * 128), slice(cb * 128, (cb + 1) * 128)
-            wqT, wsT = sat.scaling_aware_transpose(host(q[rs, cs]), host(s[rs, cb:cb + 1]))
-            assert np.array_equal(host(qT[cs, rs]), wqT), (name, rb, cb)
-            assert np.array_equal(host(sT[rb:rb + 1, cs]).T, wsT), (name, rb, cb)
-        if m_pad % 128:  # groups padded to 16: the last block is partial
-            rb, n = m_pad // 128, m_pad % 128
-            rs, cs = slice(rb * 128, m_pad), slice(0, 256)
-            wqT, wsT = sat.scaling_aware_transpose(host(q[rs, cs]), host(s[rs, 0:2]), n)
-            assert np.array_equal(host(qT[cs, rs]), wqT), (name, "last block")
-            assert np.array_equal(host(sT[rb:rb + 1, cs]).T, wsT), (name, "last block")
+        for rb in stripes:
+            r1 = min((rb + 1) * 128, m_pad)
+            rs = slice(rb * 128, r1)
+            wqT, wsT = sat.scaling_aware_transpose(host(q[rs]), host(s[rs]), r1 - rb * 128)
+            assert np.array_equal(host(qT[:, rs]), wqT), (name, rb)
+            assert np.array_equal(host(sT[rb:rb + 1]).T, wsT), (name, rb)

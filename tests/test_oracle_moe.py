@@ -238,3 +238,68 @@ def test_unpermute_loop_and_gather():
     _, off1, rm1, _ = moe.route(idx1, E)
     yp1 = torch.from_numpy(rng.standard_normal((off1[-1], H))).to(torch.bfloat16).double().numpy()
     assert np.array_equal(moe.unpermute(yp1, rm1, None), yp1[rm1[:, 0]])
+
+
+def test_wgrad_groups_ending_inside_128_token_blocks():
+    """Groups padded to 16 rows (section 3.3.1): expert boundaries fall inside 128-token blocks,
+    the last block is partial, and one column scale covers tokens of two experts.  Each
+    element of dW[e] is the exactly-rounded sum over precisely expert e's token columns, each
+    token scaled by the column scale of its own 128-token block."""
+    N, K = 128, 256
+    offsets = np.array([0, 176, 176, 272, 400])  # 176 = 128 + 48, 272 = 2*128 + 16, 400 = 3*128 + 16
+    m_pad = int(offsets[-1])
+    nb = -(-m_pad // TILE)  # 4 blocks, the last one holds 16 tokens
+    rng = np.random.default_rng(11)
+    codes_g = rng.integers(0, 256, size=(N, m_pad), dtype=np.uint8)
+    codes_x = rng.integers(0, 256, size=(K, m_pad), dtype=np.uint8)
+    for c in (codes_g, codes_x):
+        c[(c & 0x7F) == 0x7F] = 0x00  # no NaN codes
+    # random power-of-two column scales, per (column row, 128-token block); a caller's scale
+    # buffer is wider than the blocks in use (M_cap/128 entries), the extra entries are never used
+    sg = np.ldexp(1.0, rng.integers(-30, 10, size=(N, nb + 2))).astype(np.float32)
+    sx = np.ldexp(1.0, rng.integers(-30, 10, size=(K, nb + 2))).astype(np.float32)
+    sg[:, nb:] = np.float32(np.nan)
+    sx[:, nb:] = np.float32(np.nan)
+    dw = moe.grouped_gemm_wgrad(codes_g, sg, codes_x, sx, offsets)
+    assert dw.shape == (4, N, K)
+    assert np.all(dw[1] == 0)  # zero-token expert
+    dec_g, dec_x = e4m3_decode(codes_g), e4m3_decode(codes_x)
+    picks = [(0, 0, 0), (0, 127, 255), (0, 5, 130), (2, 64, 7), (2, 100, 200), (3, 1, 1), (3, 127, 128)]
+    picks += [(e, int(rng.integers(N)), int(rng.integers(K))) for e in (0, 2, 3) for _ in range(6)]
+    for (e, n, kk) in picks:
+        terms = [float(dec_g[n, m]) * float(sg[n, m // TILE]) * float(dec_x[kk, m]) * float(sx[kk, m // TILE])
+                 for m in range(int(offsets[e]), int(offsets[e + 1]))]
+        assert dw[e, n, kk] == pytest.approx(math.fsum(terms), rel=1e-12, abs=1e-300), (e, n, kk)
+    # shifting a token's bytes from one expert to its neighbour moves exactly its product
+    kk, n, m = 3, 9, 175  # token 175: the last of expert 0, inside block 1 which expert 2 shares
+    zero_g = codes_g.copy()
+    zero_g[n, m] = 0x00
+    dw2 = moe.grouped_gemm_wgrad(zero_g, sg, codes_x, sx, offsets)
+    moved = float(dec_g[n, m]) * float(sg[n, 1]) * float(dec_x[kk, m]) * float(sx[kk, 1])
+    assert dw[0, n, kk] - dw2[0, n, kk] == pytest.approx(moved, rel=1e-9, abs=1e-300)
+    assert np.array_equal(dw[2], dw2[2]) and np.array_equal(dw[3], dw2[3])
+
+
+@pytest.mark.parametrize("T,k,E,align", [(4, 1, 4, 16), (3, 1, 3, 128), (5, 2, 3, 16), (2, 2, 3, 16),
+                                         (6, 1, 2, 4), (3, 2, 4, 32)])
+def test_rows_bound_is_the_worst_case(T, k, E, align):
+    """rows_bound against brute force over EVERY routing of a tiny batch (k distinct experts
+    per token): never below the largest padded row count, and equal to it (rounded up to whole
+    128-row blocks) whenever some routing makes every expert's count 1 more than a multiple of
+    the alignment, the worst case the bound assumes."""
+    import itertools
+
+    choices = list(itertools.permutations(range(E), k))
+    worst, attained = 0, False
+    for pick in itertools.product(choices, repeat=T):
+        idx = np.array(pick, dtype=np.int64).reshape(T, k)
+        counts, offsets, _, _ = moe.route(idx, E, align)
+        worst = max(worst, int(offsets[-1]))
+        attained |= bool(np.all(counts % align == 1))
+    bound = moe.rows_bound(T, k, E, align)
+    assert bound % 128 == 0 and worst <= bound
+    if attained:
+        assert worst == T * k + (align - 1) * E
+        assert bound == -(-worst // 128) * 128
+    else:
+        assert worst < T * k + (align - 1) * E

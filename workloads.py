@@ -69,19 +69,23 @@ def outlier_activation(rows, cols, seed=0, device="cpu", frac=1e-3, factor=100.0
 
 
 def routing(shape, seed=0, device="cpu"):
-    """(topk_idx int32 [T, k], probs float32 [T, k]) for the shape's routing recipe."""
-    g = _gen(seed + 1, device)
+    """(topk_idx int32 [T, k], probs float32 [T, k]) for the shape's routing recipe.
+
+    Always drawn on the CPU generator and then moved to `device`, so that the routing (and
+    hence the expert populations a test or the benchmark relies on) is the same whichever
+    device the other inputs are generated on."""
+    g = _gen(seed + 1, "cpu")
     T, E, k = shape.T, shape.E, shape.k
-    logits = torch.randn((T, E), generator=g, device=device, dtype=torch.float32)
+    logits = torch.randn((T, E), generator=g, dtype=torch.float32)
     if shape.routing == "zipf":
-        rank = torch.randperm(E, generator=g, device=device).to(torch.float32) + 1.0
+        rank = torch.randperm(E, generator=g).to(torch.float32) + 1.0
         p = rank ** -1.2
         p = p / p.sum()
         logits = torch.log(p)[None, :] + 0.4 * logits
     probs_all = torch.softmax(logits, dim=1)
     _, idx = torch.topk(logits, k, dim=1)
     probs = torch.gather(probs_all, 1, idx)
-    return idx.to(torch.int32).contiguous(), probs.contiguous()
+    return idx.to(torch.int32).contiguous().to(device), probs.contiguous().to(device)
 
 
 def layer_inputs(shape, seed=0, device="cpu", with_grad=True):
@@ -105,3 +109,20 @@ def expert_counts(topk_idx, E):
     idx = topk_idx.reshape(-1).to(torch.int64)
     idx = idx[idx >= 0]
     return torch.bincount(idx, minlength=E)
+
+
+def skew_census(topk_idx, E):
+    """Experts with no tokens, with 1..127 tokens (a partial 128-row tile) and with more than
+    4000 tokens: the three populations the skewed-routing stress case must contain."""
+    c = expert_counts(topk_idx, E).cpu()
+    return {"zero": int((c == 0).sum()), "under_128": int(((c > 0) & (c < 128)).sum()),
+            "over_4000": int((c > 4000).sum())}
+
+
+def check_skew(topk_idx, E):
+    """Raise unless the routing has every population of the skewed stress case (see skew_census)."""
+    census = skew_census(topk_idx, E)
+    missing = [k for k, v in census.items() if v < 1]
+    if missing:
+        raise AssertionError(f"skewed routing lacks experts of kind {missing}: {census}")
+    return census
