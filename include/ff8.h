@@ -157,6 +157,24 @@ int ff8_permute_quant_aligned(const ff8_bf16* x, const float* row_w, int64_t T, 
                               size_t ws_bytes, int align, void* stream);
 
 /*
+ * ff8_permute_quant_noalloc -- ff8_permute_quant_aligned without a caller workspace, for callers
+ *   that cannot allocate device memory at call time (code under HIP graph capture, tight serving
+ *   loops, harnesses that forbid hipMalloc).  The routing pass keeps its per-chunk expert counts
+ *   in a 1 MiB array that the library holds in device memory (one per GPU, from the first call
+ *   on that GPU until the process ends); the call itself allocates nothing.  Arguments, outputs
+ *   and errors as ff8_permute_quant_aligned (align 16, 32, 64 or 128), minus workspace and
+ *   ws_bytes.  Limit: with reuse_map == 0, ceil(T / 256) * E <= 262144 (T <= 2 097 152 tokens
+ *   at E = 32); larger routings return FF8_ERR_ARG before anything is enqueued.  Every call on
+ *   one GPU shares that GPU's array, and nothing in it needs clearing between calls (each call
+ *   writes every entry it reads), but calls that overlap on one GPU (concurrent streams, or
+ *   host threads each with its own stream) race on it and give undefined routing: serialize
+ *   them.
+ */
+int ff8_permute_quant_noalloc(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                              const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets,
+                              int32_t* src_row, int64_t M_cap, ff8_e4m3* q, float* s, int align, void* stream);
+
+/*
  * ff8_permute_quant_dprobs -- the backward permute of dY (ff8_permute_quant with reuse_map = 1
  *   and routing weights) fused with the router gradient, the backward of the
  *   routing-weighted combine y[t] = sum_j row_w[t, j] * y_perm[row_map[t, j]] (paper section

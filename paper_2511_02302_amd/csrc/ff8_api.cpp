@@ -106,34 +106,60 @@ size_t ff8_permute_workspace_bytes(int64_t T, int k, int E) {
   return ff8::permute_workspace_bytes(T, k, E);
 }
 
+}  // extern "C"
+
+// Host-side checks of a permute call; `ws_need_check` is false for the no-allocation entry
+// point, whose workspace is the library's own.
+static int permute_validate(const char* fn, const void* x, int64_t T, int64_t H, int k, int E, const void* topk_idx,
+                            int reuse_map, const void* row_map, const void* offsets, const void* src_row, int64_t M_cap,
+                            const void* q, const void* s, const void* workspace, size_t ws_bytes, int align,
+                            bool ws_need_check) {
+  if (!(reuse_map == 0 || reuse_map == 1)) return fail(FF8_ERR_ARG, "%s: reuse_map must be 0 or 1", fn);
+  if (!(k >= 1 && E >= 1 && k <= E && E <= 1024)) return fail(FF8_ERR_ARG, "%s: need 1 <= k <= E <= 1024", fn);
+  if (!(align == 16 || align == 32 || align == 64 || align == 128))
+    return fail(FF8_ERR_ARG, "%s: align must be 16, 32, 64 or 128", fn);
+  if (!(T >= 0 && mult128(H) && M_cap % 128 == 0))
+    return fail(FF8_ERR_SHAPE, "%s: need T >= 0, H and M_cap multiples of 128", fn);
+  // a reused map may come from any alignment: only the smallest bound is known here
+  if (M_cap < ff8_rows_bound_aligned(T, k, E, reuse_map ? 16 : align))
+    return fail(FF8_ERR_SHAPE, "%s: M_cap is below the row bound", fn);
+  if (!(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31))
+    return fail(FF8_ERR_SHAPE, "%s: T*k and M_cap must be below 2^31", fn);
+  if (T > 0 && (!x || !row_map)) return fail(FF8_ERR_NULL, "%s: x or row_map is NULL", fn);
+  if (!offsets || !src_row || !q || !s) return fail(FF8_ERR_NULL, "%s: offsets, src_row, q or s is NULL", fn);
+  if (!reuse_map) {
+    if (T > 0 && !topk_idx) return fail(FF8_ERR_NULL, "%s: topk_idx is NULL", fn);
+    if (ws_need_check) {
+      const size_t need = ff8::permute_workspace_bytes(T, k, E);
+      if (need > 0 && !workspace) return fail(FF8_ERR_NULL, "%s: workspace is NULL", fn);
+      if (ws_bytes < need) return fail(FF8_ERR_ARG, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+    }
+  }
+  return FF8_OK;
+}
+
+static int permute_launch(const char* fn, const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                          const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
+                          int64_t M_cap, ff8_e4m3* q, float* s, void* workspace, int align, hipStream_t st) {
+  if (!reuse_map) {
+    const int rc = hip_status(
+        ff8::launch_route(topk_idx, T, k, E, align, row_map, offsets, src_row, M_cap, workspace, st), fn);
+    if (rc != FF8_OK) return rc;
+  }
+  return hip_status(ff8::launch_permute_quant(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st), fn);
+}
+
+extern "C" {
+
 int ff8_permute_quant_aligned(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                               const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets,
                               int32_t* src_row, int64_t M_cap, ff8_e4m3* q, float* s, void* workspace,
                               size_t ws_bytes, int align, void* stream) {
-  REQUIRE_ARG(reuse_map == 0 || reuse_map == 1);
-  REQUIRE_ARG(k >= 1 && E >= 1 && k <= E && E <= 1024);
-  REQUIRE_ARG(align == 16 || align == 32 || align == 64 || align == 128);
-  REQUIRE_SHAPE(T >= 0 && mult128(H) && M_cap % 128 == 0);
-  // a reused map may come from any alignment: only the smallest bound is known here
-  REQUIRE_SHAPE(M_cap >= ff8_rows_bound_aligned(T, k, E, reuse_map ? 16 : align));
-  REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
-  if (T > 0) {  // an empty batch may pass NULL for its empty token-indexed arrays
-    REQUIRE_PTR(x); REQUIRE_PTR(row_map);
-  }
-  REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
-  hipStream_t st = as_stream(stream);
-  if (!reuse_map) {
-    if (T > 0) REQUIRE_PTR(topk_idx);
-    const size_t need = ff8::permute_workspace_bytes(T, k, E);
-    if (need > 0) REQUIRE_PTR(workspace);
-    REQUIRE_ARG(ws_bytes >= need);
-    const int rc = hip_status(
-        ff8::launch_route(topk_idx, T, k, E, align, row_map, offsets, src_row, M_cap, workspace, st),
-        "ff8_permute_quant(route)");
-    if (rc != FF8_OK) return rc;
-  }
-  return hip_status(ff8::launch_permute_quant(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st),
-                    __func__);
+  const int rc = permute_validate(__func__, x, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
+                                  workspace, ws_bytes, align, true);
+  if (rc != FF8_OK) return rc;
+  return permute_launch(__func__, x, row_w, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
+                        workspace, align, as_stream(stream));
 }
 
 int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
@@ -141,6 +167,29 @@ int ff8_permute_quant(const ff8_bf16* x, const float* row_w, int64_t T, int64_t 
                       int64_t M_cap, ff8_e4m3* q, float* s, void* workspace, size_t ws_bytes, void* stream) {
   return ff8_permute_quant_aligned(x, row_w, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
                                    workspace, ws_bytes, 128, stream);
+}
+
+int ff8_permute_quant_noalloc(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                              const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets,
+                              int32_t* src_row, int64_t M_cap, ff8_e4m3* q, float* s, int align, void* stream) {
+  int rc = permute_validate(__func__, x, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
+                            nullptr, 0, align, false);
+  if (rc != FF8_OK) return rc;
+  const size_t need = ff8::permute_workspace_bytes(T, k, E);
+  if (!reuse_map && need > (size_t)ff8::kRouteScratchInts * sizeof(int32_t))
+    return fail(FF8_ERR_ARG,
+                "%s: the routing of T = %lld tokens over E = %d experts needs %zu bytes of workspace, more than the "
+                "%lld bytes the library holds (ceil(T / 256) * E must not exceed %lld); use ff8_permute_quant_aligned "
+                "with a caller-owned workspace",
+                __func__, (long long)T, E, need, (long long)(ff8::kRouteScratchInts * 4),
+                (long long)ff8::kRouteScratchInts);
+  int32_t* ws = nullptr;
+  if (!reuse_map) {
+    rc = hip_status(ff8::route_scratch(&ws), __func__);
+    if (rc != FF8_OK) return rc;
+  }
+  return permute_launch(__func__, x, row_w, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s, ws,
+                        align, as_stream(stream));
 }
 
 int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,

@@ -23,6 +23,11 @@ hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t co
                       uint8_t* qT, float* sT, hipStream_t st);
 
 size_t permute_workspace_bytes(int64_t T, int k, int E);
+// Capacity (int32 entries) of the routing workspace the library keeps in device memory for the
+// no-allocation entry point, and its device address on the current device (looked up once per
+// device; the array is resident until the process ends).
+constexpr int64_t kRouteScratchInts = (int64_t)1 << 18;
+hipError_t route_scratch(int32_t** out);
 hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int align, int32_t* row_map,
                         int32_t* offsets, int32_t* src_row, int64_t M_cap, void* workspace, hipStream_t st);
 hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,

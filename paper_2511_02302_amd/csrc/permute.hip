@@ -17,6 +17,8 @@
 // separately.  pad_fill writes the padding rows.  unpermute gathers a token's k rows the
 // same way and sums them in slot order.
 
+#include <mutex>
+
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
 
@@ -340,6 +342,30 @@ hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int al
   route_scan_kernel<<<1, 1024, 0, st>>>(counts, nc, E, align, offsets, src_row);
   if (nc > 0) route_assign_kernel<<<(unsigned)nc, 64, 0, st>>>(topk_idx, T, k, E, counts, row_map, src_row);
   return hipGetLastError();
+}
+
+// Routing workspace of the no-allocation entry point: one array per device, resident until the
+// process ends.  Host code never passes its name to a kernel (in host code the name is only a
+// stand-in for the symbol): it takes the device address from hipGetSymbolAddress, once per
+// device with that device current, and passes that.
+static __device__ __align__(256) int32_t scratch[kRouteScratchInts];
+
+hipError_t route_scratch(int32_t** out) {
+  static std::mutex mu;
+  static int32_t* addr[64] = {nullptr};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = static_cast<int32_t*>(p);
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,

@@ -35,6 +35,8 @@ _SIGNATURES = {
                                    _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_vp]),
     "ff8_permute_quant_aligned": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp,
                                            _c_vp, _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_int, _c_vp]),
+    "ff8_permute_quant_noalloc": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp,
+                                           _c_vp, _c_vp, _c_i64, _c_vp, _c_vp, _c_int, _c_vp]),
     "ff8_scaling_aware_transpose": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
     "ff8_grouped_gemm_fprop": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
                                         _c_vp]),
@@ -176,6 +178,20 @@ def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src
         _check(load().ff8_permute_quant(*args, _stream(stream)), "ff8_permute_quant")
     else:
         _check(load().ff8_permute_quant_aligned(*args, int(align), _stream(stream)), "ff8_permute_quant_aligned")
+
+
+def ff8_permute_quant_noalloc(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src_row, q, s, align=128,
+                              stream=None):
+    """ff8_permute_quant_aligned with the library's own routing workspace (no caller buffer)."""
+    T, H = x.shape
+    M_cap = q.shape[0]
+    _numel(row_w, T * k, "row_w"); _numel(topk_idx, T * k, "topk_idx"); _numel(row_map, T * k, "row_map")
+    _numel(offsets, E + 1, "offsets"); _numel(src_row, M_cap, "src_row")
+    _shape(q, (M_cap, H), "q"); _shape(s, (M_cap, H // 128), "s")
+    _check(load().ff8_permute_quant_noalloc(
+        _ptr(x, _bf16, "x", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E, _ptr(topk_idx, _i32, "topk_idx"),
+        int(reuse_map), _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"), _ptr(src_row, _i32, "src_row"),
+        M_cap, _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2), int(align), _stream(stream)), "ff8_permute_quant_noalloc")
 
 
 def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y_perm, dprobs, stream=None):

@@ -47,6 +47,11 @@ def test_rows_bound(lib):
     assert lib.ff8_permute_workspace_bytes(1024, 2, 8) == 4 * 8 * 4
 
 
+def _no_gpu():
+    torch = pytest.importorskip("torch")
+    return torch.cuda.device_count() == 0  # counts devices without initialising one
+
+
 def test_validation_errors_without_gpu(lib):
     vp = ctypes.c_void_p
     fake = vp(0x1000)
@@ -76,9 +81,20 @@ def test_validation_errors_without_gpu(lib):
     # the router gradient keeps a row of dY in registers: H above 8192 is rejected
     assert lib.ff8_permute_quant_dprobs(fake, fake, 16, 8320, 2, 4, fake, fake, fake, 4096, fake, fake, fake, fake,
                                         None) == 2
-    # an empty batch passes validation with NULL token-indexed arrays (no GPU here: the launch fails)
-    assert lib.ff8_permute_quant(None, None, 0, 128, 2, 4, None, 0, None, fake, fake, 512, fake, fake,
-                                 None, 0, None) != 1
+    # an empty batch passes validation with NULL token-indexed arrays (no GPU here: the launch fails;
+    # with a GPU present the launch would read the fake pointers, so it is not made there)
+    if _no_gpu():
+        assert lib.ff8_permute_quant(None, None, 0, 128, 2, 4, None, 0, None, fake, fake, 512, fake, fake,
+                                     None, 0, None) != 1
+    # the no-allocation permute holds a 1 MiB routing workspace: ceil(T / 256) * E above 2^18 is
+    # rejected on the host, before any device call
+    t_big = 8192 * 256 + 1
+    m_big = lib.ff8_rows_bound(t_big, 8, 32)
+    assert lib.ff8_permute_quant_noalloc(fake, None, t_big, 128, 8, 32, fake, 0, fake, fake, fake, m_big, fake, fake,
+                                         128, None) == 3
+    assert b"1048576 bytes" in lib.ff8_last_error()
+    assert lib.ff8_permute_quant_noalloc(fake, None, 16, 128, 2, 4, fake, 0, fake, fake, fake, 640, fake, fake,
+                                         24, None) == 3  # align
     assert lib.ff8_swiglu_quant(fake, None, 0, 128, 100, fake, fake, None) == 2
     assert lib.ff8_baseline_copy(fake, fake, 17, None) == 2
     # operands of 4 GiB and more: the kernels address each operand with 32-bit byte offsets
