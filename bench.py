@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--no-router-grad", action="store_true")
     ap.add_argument("--no-align16", action="store_true")
     ap.add_argument("--no-hip-graph", action="store_true")
+    ap.add_argument("--no-skew", action="store_true")
+    ap.add_argument("--no-cast-accuracy", action="store_true")
     return ap.parse_args()
 
 
@@ -180,6 +182,46 @@ def fp8_checkpoint(torch, L, d, shape, M, steps, warmup, ms_bf16_a):
     return out
 
 
+def checkpoint_memory(torch, shape, d, n_layers=2):
+    """Measured memory of the activations a stack of n_layers expert layers keeps between its
+    forwards and its backwards, with A kept in BF16 and as its FP8 checkpoint.  The layers
+    share one step-local workspace; each layer's saved state is allocated by its forward and
+    released by its backward.  `kept_per_layer` is torch's allocated bytes after the last
+    forward minus before the first, over n_layers; `peak_above_base` is the allocator's peak
+    over the whole forward+backward sequence (the workspace and the weights are allocated
+    before, so they are not in it)."""
+    from paper_2511_02302_amd.layer import ExpertLayerFP8, Workspace
+
+    out = {"layers": n_layers}
+    args = (shape.T, shape.H, shape.E, shape.k, shape.I)
+    for key, ckpt in (("bf16_a", False), ("fp8_checkpoint", True)):
+        ws = Workspace(ExpertLayerFP8(*args, fp8_checkpoint=ckpt).d, fp8_checkpoint=ckpt)
+        layers = [ExpertLayerFP8(*args, fp8_checkpoint=ckpt, workspace=ws) for _ in range(n_layers)]
+        for L in layers:
+            L.quantize_weights(d["w1"], d["w2"])
+            L.release_saved()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        x = d["x"]
+        for L in layers:
+            x = L.forward(x, d["topk_idx"], d["probs"])
+        torch.cuda.synchronize()
+        kept = torch.cuda.memory_allocated() - base
+        g = d["dy"]
+        for L in reversed(layers):
+            g, _, _ = L.backward(g, d["probs"], release=True)
+        torch.cuda.synchronize()
+        out[key] = {"kept_per_layer": kept // n_layers, "peak_above_base": torch.cuda.max_memory_allocated() - base,
+                    "accounted_per_layer": layers[0].saved_activation_bytes(), "workspace_bytes": ws.nbytes()}
+        del layers, ws, x, g
+        torch.cuda.empty_cache()
+    out["measured_saving_per_layer"] = out["bf16_a"]["kept_per_layer"] - out["fp8_checkpoint"]["kept_per_layer"]
+    out["measured_saving_frac"] = round(out["measured_saving_per_layer"] / out["bf16_a"]["kept_per_layer"], 4)
+    return out
+
+
 def router_grad(torch, L, d, shape, M, steps, warmup, ms_base, b1_base_ms):
     """The step with B1 fused with the router gradient dprobs[t, j] = <dY[t], Y_perm[row]>: its
     step time and B1's time and rate.  The fused B1 additionally reads the k rows of Y_perm of
@@ -231,6 +273,133 @@ def align16(torch, d, shape, M, steps, warmup, ms_base):
            "value": round(gemm_flops / (ms_step * 1e-3) / 1e12, 2), "padded_rows": m_pad, "routed_rows": M,
            "stages_ms": {n: round(st[n], 4) for n in names}}
     del L
+    torch.cuda.empty_cache()
+    return out
+
+
+def stage_table(costs, st_ms):
+    """Per-stage time and rate against the stage's roofline (FP8 MFMA or HBM)."""
+    out = {}
+    for n, (kind, amount) in costs.items():
+        t = st_ms[n]
+        if kind == "mfma":
+            ach = amount / (t * 1e-3) / 1e12
+            out[n] = {"ms": round(t, 4), "TFLOP/s": round(ach, 1), "frac_mfma": round(ach / FP8_PEAK_TFLOPS, 3)}
+        else:
+            ach = amount / (t * 1e-3) / 1e9
+            out[n] = {"ms": round(t, 4), "GB/s": round(ach, 1), "frac_hbm": round(ach / HBM_PEAK_GBS, 3)}
+    return out
+
+
+def timed_steps(torch, L, d, names, steps, warmup, **kw):
+    """Warm-up steps, then `steps` timed steps: (wall ms per step, per-stage event ms)."""
+    for _ in range(warmup):
+        run_step(L, d, **kw)
+    torch.cuda.synchronize()
+    timer = StageTimer(torch, names, steps)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run_step(L, d, timer.ev[i], **kw)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps, timer.ms()
+
+
+def skew(torch, steps, warmup):
+    """The Zipf(1.2)-skewed layer (8192 tokens, the DeepSeek-V3 widths): ragged groups with empty
+    experts, experts under one 128-row tile and experts over 4000 tokens, asserted on the very
+    routing the GPU runs.  Step time, GEMM rate on the real rows, and every stage's rate."""
+    import workloads
+    from paper_2511_02302_amd.layer import ExpertLayerFP8
+
+    shape = workloads.SKEW
+    d = workloads.layer_inputs(shape, seed=0, device="cuda")
+    census = workloads.check_skew(d["topk_idx"], shape.E)
+    counts = workloads.expert_counts(d["topk_idx"], shape.E).cpu()
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
+    M = int(counts.sum())
+    costs = stage_costs(shape, M)
+    names = list(costs)
+    ms_step, st = timed_steps(torch, L, d, names, steps, warmup)
+    gemm_flops = sum(v for kind, v in costs.values() if kind == "mfma")
+    gemm_ms = sum(st[n] for n in names if costs[n][0] == "mfma")
+    out = {"workload": shape.name, "routed_rows": M, "padded_rows": int(L.buf["offsets"][-1].item()),
+           "expert_tokens_min_max": [int(counts.min()), int(counts.max())], "populations": census,
+           "ms_per_step": round(ms_step, 4), "value": round(gemm_flops / (ms_step * 1e-3) / 1e12, 2),
+           "unit": "TFLOP/s", "frac_mfma_step": round(gemm_flops / (ms_step * 1e-3) / 1e12 / FP8_PEAK_TFLOPS, 4),
+           "gemm_only": {"TFLOP/s": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
+                         "frac_mfma": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / FP8_PEAK_TFLOPS, 4),
+                         "ms": round(gemm_ms, 3)},
+           "stages": stage_table(costs, st)}
+    del L, d
+    torch.cuda.empty_cache()
+    return out
+
+
+def cast_accuracy(torch):
+    """Conversion error on the cast-op activation (32768 x 7168 bf16 N(0,1), 0.1% x100 outliers),
+    every FP8 tensor made by the library's kernels (section 3.1, Eq. 1 and the exponent-shift
+    identity): relative to D(Q_row X), the extra error of the scaling-aware transpose, of the
+    naive power-of-two chain N1 (dequantize -> bf16 transpose -> requantize, the library's
+    baseline kernels), and of the naive fp32-scale chain N2 (s = amax/448 quantization applied
+    twice through a bf16 intermediate, written here with plain torch ops since it is the
+    comparison recipe, not part of the path), plus the single-quantization errors.  The error
+    norms themselves are computed with torch reductions."""
+    import workloads
+    from paper_2511_02302_amd import ff8
+
+    R, C = workloads.CAST_X
+    x = workloads.outlier_activation(R, C, seed=0, device="cuda")
+    f8 = torch.float8_e4m3fn
+    dec = lambda q: q.view(f8).float()  # exact decode of e4m3 bytes
+    rep = lambda s: s.repeat_interleave(128, dim=1)
+    q, s = torch.empty((R, C), dtype=torch.uint8, device="cuda"), torch.empty((R, C // 128), device="cuda")
+    ff8.ff8_quant_rowwise(x, q, s)
+    d_row = dec(q) * rep(s)                                   # D(Q_row X), [R, C]
+    d_rowT = d_row.t().contiguous()
+    del d_row
+    qT, sT = torch.empty((C, R), dtype=torch.uint8, device="cuda"), torch.empty((R // 128, C), device="cuda")
+    ff8.ff8_scaling_aware_transpose(q, s, qT, sT)
+    xT = x.float().t().contiguous()
+
+    def rel(a, b):
+        return float(torch.linalg.vector_norm(a - b) / torch.linalg.vector_norm(b))
+
+    out = {"workload": f"bf16 activation {R}x{C} N(0,1) with 0.1% x100 outliers, seed 0"}
+    d_sat = dec(qT) * rep(sT.t().contiguous())                # D(SAT(Q_row X)), [C, R]
+    changed = d_sat != d_rowT
+    out["sat_extra_rel_err"] = rel(d_sat, d_rowT)
+    out["sat_elements_changed_frac"] = float(changed.float().mean())
+    del d_sat, changed
+    tmp = torch.empty((R, C), dtype=torch.bfloat16, device="cuda")
+    tmpT = torch.empty((C, R), dtype=torch.bfloat16, device="cuda")
+    qn, sn = torch.empty((C, R), dtype=torch.uint8, device="cuda"), torch.empty((C, R // 128), device="cuda")
+    ff8.ff8_baseline_dequant_rowwise(q, s, tmp)
+    ff8.ff8_baseline_transpose_bf16(tmp, tmpT)
+    ff8.ff8_quant_rowwise(tmpT, qn, sn)
+    out["naive_pow2_N1_extra_rel_err"] = rel(dec(qn) * rep(sn), d_rowT)
+    del tmp, tmpT, qn, sn
+    out["row_quant_rel_err_vs_x"] = rel(d_rowT, xT)
+    # direct column-wise quantization of X (the error a column-wise operand should carry)
+    xTb = x.t().contiguous()
+    qc, sc = torch.empty((C, R), dtype=torch.uint8, device="cuda"), torch.empty((C, R // 128), device="cuda")
+    ff8.ff8_quant_rowwise(xTb, qc, sc)
+    out["col_quant_rel_err_vs_x"] = rel(dec(qc) * rep(sc), xT)
+    del qc, sc, xTb, d_rowT
+
+    def q_fp32(v):  # 1x128 tiles, s = amax / 448 in fp32, RNE, saturating
+        t = v.reshape(v.shape[0], -1, 128)
+        sc = t.abs().amax(dim=2, keepdim=True) / 448.0
+        sc = torch.where(sc == 0, torch.ones_like(sc), sc)
+        return ((t / sc).clamp(-448.0, 448.0).to(f8).float() * sc).reshape(v.shape)
+
+    d1 = q_fp32(x.float()).to(torch.bfloat16).float()         # N2 step 1, through bf16
+    d1T = d1.t().contiguous()
+    del d1
+    d2 = q_fp32(d1T)                                          # N2 step 2, column-wise
+    out["naive_fp32_N2_extra_rel_err"] = rel(d2, d1T)
+    out["naive_fp32_N2_total_rel_err_vs_x"] = rel(d2, xT)
+    out["fp32_single_quant_rel_err_vs_x"] = rel(d1T, xT)
+    del d1T, d2, xT, x, q, s, qT, sT
     torch.cuda.empty_cache()
     return out
 
@@ -370,6 +539,30 @@ def measured_traffic(stage):
     return None
 
 
+def oracle_full_tiny(seed=0):
+    """The float64 oracle on the whole tiny layer (1024 tokens, hidden 256, 8 experts, top-2,
+    intermediate 512): F0 and every step of the forward and backward, timed per phase."""
+    import numpy as np
+    import workloads
+    from oracle import layer as olayer
+
+    shape = workloads.TINY
+    inp = workloads.layer_inputs(shape, seed=seed)
+    f = lambda t: t.float().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    w = olayer.quantize_weights(f(inp["w1"]), f(inp["w2"]))
+    t1 = time.perf_counter()
+    st = olayer.forward(f(inp["x"]), inp["topk_idx"].numpy(), inp["probs"].numpy(), w["w1q"], w["w1s"], w["w2q"],
+                        w["w2s"], shape.E)
+    t2 = time.perf_counter()
+    olayer.backward(st, f(inp["dy"]), inp["probs"].numpy(), w["w1q"], w["w1s"], w["w2q"], w["w2s"])
+    t3 = time.perf_counter()
+    flops = olayer.gemm_flops(st["counts"], shape.H, shape.I)["total"]
+    return {"workload": shape.name, "seconds": {"F0": round(t1 - t0, 3), "forward": round(t2 - t1, 3),
+                                                "backward": round(t3 - t2, 3), "total": round(t3 - t0, 3)},
+            "TFLOP/s": round(flops / (t3 - t0) / 1e12, 7)}
+
+
 def cpu_baseline(shape, rows=2048, seed=0):
     """The float64 oracle, as it stands, on a bounded sample of the workload.
 
@@ -398,6 +591,7 @@ def cpu_baseline(shape, rows=2048, seed=0):
     flops = 18 * M * shape.H * shape.I
     cores = len(os.sched_getaffinity(0))
     return {"value": round(flops / full_s / 1e12, 7), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "full_tiny_layer": oracle_full_tiny(seed),
             "sample": f"expert 0 only: F0 on its W1 [{2 * shape.I}x{shape.H}] and W2 [{shape.H}x{shape.I}] "
                       f"({t1 - t0:.1f} s), F1..B8 on {rows} of its routed rows ({t2 - t1:.1f} s); "
                       f"scaled to the full step as {shape.E} x F0 + {M / rows:.1f} x rows = {full_s:.0f} s",
@@ -417,6 +611,7 @@ def main():
     shape = {"dsv3": workloads.DSV3, "skew": workloads.SKEW, "tiny": workloads.TINY}[args.workload]
     torch.cuda.set_device(0)
     d = workloads.layer_inputs(shape, seed=0, device="cuda")
+    census = workloads.check_skew(d["topk_idx"], shape.E) if shape.routing == "zipf" else None
     L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I)
     counts = workloads.expert_counts(d["topk_idx"], shape.E)
     M = int(counts.sum())
@@ -476,7 +671,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{shape.name} expert layer, fwd+bwd incl. 128x128 weight quant", "tokens": shape.T,
                    "hidden": shape.H, "experts": shape.E, "top_k": shape.k, "intermediate": shape.I,
-                   "routed_rows": M, "routing": shape.routing},
+                   "routed_rows": M, "routing": shape.routing, **({"populations": census} if census else {})},
         "frac_mfma_step": round(value / FP8_PEAK_TFLOPS, 4),
         "gemm_only": {"TFLOP/s": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
                       "frac_mfma": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / FP8_PEAK_TFLOPS, 4),
@@ -493,10 +688,17 @@ def main():
         rec["align16"] = align16(torch, d, shape, M, args.steps, args.warmup, ms_step)
     if not args.no_hip_graph:
         rec["hip_graph"] = hip_graph(torch, L, d, args.steps, args.warmup, ms_step, gemm_flops)
-    if not args.no_cast_ops:
+    if not args.no_fp8_checkpoint:
+        rec["fp8_checkpoint"]["measured_memory"] = checkpoint_memory(torch, shape, d)
+    if not args.no_cast_ops or not args.no_skew or not args.no_cast_accuracy:
         del L, d
         torch.cuda.empty_cache()
+    if not args.no_skew and args.workload != "skew":
+        rec["skew"] = skew(torch, args.steps, args.warmup)
+    if not args.no_cast_ops:
         rec["cast_ops"] = cast_ops(torch)
+    if not args.no_cast_accuracy:
+        rec["cast_accuracy"] = cast_accuracy(torch)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(shape)
     print(json.dumps(rec), flush=True)

@@ -506,6 +506,53 @@ def test_layer_stagewise(case, mode):
     assert rel_frob(host(b["dw1"]), dW1) < GEMM_TOL
 
 
+@pytest.mark.parametrize("ckpt", [False, True], ids=["bf16_a", "fp8_checkpoint"])
+def test_layer_stack_shared_workspace_and_saved_memory(ckpt):
+    """Three layers sharing one step-local workspace, run forward 0..2 then backward 2..0 (each
+    backward's dX feeding the next as dY) with the saved state released after each backward:
+    every output equals that of a layer with its own workspace run the same way, bit for bit;
+    the memory held between the forwards and the backwards is exactly the layers' saved state
+    (with the FP8 checkpoint, A's 1x128 FP8 form instead of BF16); it is all returned after the
+    backwards."""
+    from paper_2511_02302_amd.layer import Workspace
+
+    shape, inp = _inputs("ragged")
+    d = {k: dev(v) for k, v in inp.items()}
+    args = (shape.T, shape.H, shape.E, shape.k, shape.I)
+    ws = Workspace(ExpertLayerFP8(*args, fp8_checkpoint=ckpt).d, fp8_checkpoint=ckpt)
+    stack = [ExpertLayerFP8(*args, fp8_checkpoint=ckpt, workspace=ws) for _ in range(3)]
+    alone = [ExpertLayerFP8(*args, fp8_checkpoint=ckpt) for _ in range(3)]
+    outs = []
+    for layers in (stack, alone):
+        for L in layers:
+            L.quantize_weights(d["w1"], d["w2"])
+            L.release_saved()
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        x = d["x"]
+        for L in layers:
+            x = L.forward(x, d["topk_idx"], d["probs"])
+        torch.cuda.synchronize()
+        kept = torch.cuda.memory_allocated() - base
+        g = d["dy"]
+        for L in reversed(layers):
+            g, _, _ = L.backward(g, d["probs"], release=True)
+        torch.cuda.synchronize()
+        assert torch.cuda.memory_allocated() == base
+        per_layer = stack[0].saved_activation_bytes()
+        maps = 4 * (shape.T * shape.k + shape.E + 1 + stack[0].M_cap)
+        # torch's allocator rounds every block up to 512 bytes
+        assert 3 * (per_layer + maps) <= kept <= 3 * (per_layer + maps) + 3 * 16 * 512, (kept, per_layer, maps)
+        outs.append([{n: L.own[n].clone() for n in ("y", "dx", "dw1", "dw2")} for L in layers])
+    for i in range(3):
+        for n in ("y", "dx", "dw1", "dw2"):
+            assert torch.equal(outs[0][i][n].view(torch.uint8), outs[1][i][n].view(torch.uint8)), (i, n)
+    M, I = stack[0].M_cap, shape.I
+    fp8_xh = M * shape.H + M * shape.H // 32 + M * I + M * I // 32
+    want = fp8_xh + (M * 2 * I + M * 2 * I // 32 if ckpt else M * 2 * I * 2)
+    assert stack[0].saved_activation_bytes() == want
+
+
 @pytest.mark.parametrize("mode", ["paper_rows", "fp8_checkpoint_and_dprobs"])
 def test_layer_step_as_one_hip_graph(mode):
     """The step makes no host synchronization, allocation or memset, so it can be captured
