@@ -189,7 +189,8 @@ def checkpoint_memory(torch, shape, d, n_layers=2):
     released by its backward.  `kept_per_layer` is torch's allocated bytes after the last
     forward minus before the first, over n_layers; `peak_above_base` is the allocator's peak
     over the whole forward+backward sequence (the workspace and the weights are allocated
-    before, so they are not in it)."""
+    before, so they are not in it); `kept_requested_per_layer` counts the tensors' own bytes
+    (the allocator's requested-bytes statistic, without its block rounding)."""
     from paper_2511_02302_amd.layer import ExpertLayerFP8, Workspace
 
     out = {"layers": n_layers}
@@ -202,18 +203,20 @@ def checkpoint_memory(torch, shape, d, n_layers=2):
             L.release_saved()
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        base = torch.cuda.memory_allocated()
+        stats = torch.cuda.memory_stats
+        base, base_req = torch.cuda.memory_allocated(), stats()["requested_bytes.all.current"]
         torch.cuda.reset_peak_memory_stats()
         x = d["x"]
         for L in layers:
             x = L.forward(x, d["topk_idx"], d["probs"])
         torch.cuda.synchronize()
-        kept = torch.cuda.memory_allocated() - base
+        kept, kept_req = torch.cuda.memory_allocated() - base, stats()["requested_bytes.all.current"] - base_req
         g = d["dy"]
         for L in reversed(layers):
             g, _, _ = L.backward(g, d["probs"], release=True)
         torch.cuda.synchronize()
-        out[key] = {"kept_per_layer": kept // n_layers, "peak_above_base": torch.cuda.max_memory_allocated() - base,
+        out[key] = {"kept_per_layer": kept // n_layers, "kept_requested_per_layer": kept_req // n_layers,
+                    "peak_above_base": torch.cuda.max_memory_allocated() - base,
                     "accounted_per_layer": layers[0].saved_activation_bytes(), "workspace_bytes": ws.nbytes()}
         del layers, ws, x, g
         torch.cuda.empty_cache()

@@ -54,8 +54,23 @@ constexpr int kBP = 4;     // p tiles per XCD block
 static_assert(kBQ * kBP == 32, "an XCD block is the 32 workgroups one XCD runs at once");
 constexpr int kTileBytes = kTP * kBK;  // 32 KB per operand per stage
 constexpr int kScaleBatch = 4;         // K blocks per scale batch
-constexpr int kDmaPerSlot = 1;         // tile DMA instructions issued per MFMA slot
-constexpr int kReadSlots = 8;          // MFMA slots of a half-step that carry fragment reads
+#define FF8_STR2(x) #x
+#define FF8_STR(x) FF8_STR2(x)
+constexpr int kReadSlots = 6;          // MFMA slots of a half-step that carry fragment reads
+// The stage buffer a stage reads is free once every wave has read its second-half fragments
+// (issued over the first kReadSlots slots of the first half-step): a barrier at slot kEarly
+// publishes that, and the 16 tile DMAs of stage ks+2 into it are spread evenly over the
+// remaining kDmaSlots MFMA slots of the stage.  (Issued within the second half-step only, the
+// 64 DMA instructions of a workgroup outran the vector-memory path, whose backpressure stalled
+// the in-order waves in front of their next MFMA.)
+constexpr int kEarly = 6;
+constexpr int kDmaSlots = 32 - kEarly;
+static_assert(kEarly >= kReadSlots && kEarly < 16, "the early barrier follows the last fragment read of half 0");
+// tile DMAs issued before DMA slot j (slot j = MFMA slot kEarly + j of half 0, then of half 1)
+__host__ __device__ constexpr int dma_before(int j) { return (16 * j) / kDmaSlots; }
+// DMAs issued in half 0, still in flight at the mid-stage wait (the literal in that wait)
+#define FF8_HALF0_DMAS 6
+static_assert(dma_before(16 - kEarly) == FF8_HALF0_DMAS, "mid-stage vmcnt literal");
 // Rotate each XCD block's K order (memory-channel spread).  Measured: +5.6% for fprop,
 // whose two operands are row-major over K; -1% / -3% for dgrad / wgrad, which keep it off.
 template <int MODE> constexpr bool kStaggerK = (MODE == kFprop);
@@ -347,16 +362,22 @@ struct Tile {
     acc[A][Bq] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp[A], fq[Bq], acc[A][Bq], 0, 0, A, (int)cp[S4], Bq,
                                                                    (int)cq[S4]);
   }
-  // Tile DMA instructions of second-half slot I (kDmaPerSlot per slot from slot 0), and
-  // the scale batch's eight spread over the same slots.
-  template <int B, int S4, int I, int D>
-  __device__ __forceinline__ void dma_slot(int ks_dma, int ks_next) {
-    if constexpr (D < kDmaPerSlot && kDmaPerSlot * I + D < 16) {
-      dma_tile<B, kDmaPerSlot * I + D>(ks_dma);
-      if constexpr (S4 == 0 && kDmaPerSlot * I + D == 1) dma_scale_p((ks_next >> 2) + 1);
-      if constexpr (S4 == 0 && kDmaPerSlot * I + D == 3) dma_scale_q((ks_next >> 2) + 1);
-      dma_slot<B, S4, I, D + 1>(ks_dma, ks_next);
+  // Tile DMA instructions D0..D1-1 of stage ks_dma into buffer B.
+  template <int B, int D0, int D1>
+  __device__ __forceinline__ void dma_range(int ks_dma) {
+    if constexpr (D0 < D1) {
+      dma_tile<B, D0>(ks_dma);
+      dma_range<B, D0 + 1, D1>(ks_dma);
     }
+  }
+  // DMA slot J (0..kDmaSlots-1) of a stage: its share of the tile DMAs of stage ks_dma, and, in
+  // the second half-step of the first stage of a scale batch, the next batch's scale DMAs
+  // (slot indices of half 1 are 16 - kEarly + I).
+  template <int B, int S4, int J>
+  __device__ __forceinline__ void dma_slot(int ks_dma, int ks_next) {
+    dma_range<B, dma_before(J), dma_before(J + 1)>(ks_dma);
+    if constexpr (S4 == 0 && J == 16 - kEarly + 1) dma_scale_p((ks_next >> 2) + 1);
+    if constexpr (S4 == 0 && J == 16 - kEarly + 3) dma_scale_q((ks_next >> 2) + 1);
   }
   // Fragment reads of MFMA slot I: the half-step's kFragReads reads spread evenly over
   // its first kReadSlots slots.
@@ -373,28 +394,32 @@ struct Tile {
       reads_range<B, H, kSetA, I * kFragReads / kReadSlots, (I + 1) * kFragReads / kReadSlots>();
   }
 
-  // First half-step of stage ks (buffer B): MFMAs on set A; the reads of the second
-  // half (same buffer) into set B go out over the first eight MFMAs, so that they have
-  // landed by the barrier.
+  // First half-step of stage ks (buffer B): MFMAs on set A; the reads of the second half (same
+  // buffer) into set B go out over the first kReadSlots MFMAs; at slot kEarly every wave has
+  // them (lgkmcnt) and a barrier frees buffer B, into which the DMA of stage ks+2 starts.
   template <int B, int S4, int I>
-  __device__ __forceinline__ void half0_from() {
+  __device__ __forceinline__ void half0_from(int ks_dma, int ks_next) {
     if constexpr (I < 16) {
       mfma_op<true, S4, I>();
       reads_of_slot<B, 1, false, I>();
+      if constexpr (I == kEarly) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+      }
+      if constexpr (I >= kEarly) dma_slot<B, S4, I - kEarly>(ks_dma, ks_next);
       __builtin_amdgcn_sched_barrier(0);
-      half0_from<B, S4, I + 1>();
+      half0_from<B, S4, I + 1>(ks_dma, ks_next);
     }
   }
-  // Second half-step: MFMAs on set B.  The DMA of stage ks+2 into buffer B (free now) is
-  // spread over the sixteen MFMAs, kDmaPerSlot per slot, with the next scale batch among
-  // them when ks % 4 == 0 (it lands by the middle of the next stage); the reads of stage
-  // ks+1's first half (other buffer) into set A go out over the first eight; in the last
-  // stage of a batch the next batch's scales are read and packed.
+  // Second half-step: MFMAs on set B.  The rest of stage ks+2's DMA (with the next scale
+  // batch among it when ks % 4 == 0, landing by the middle of the next stage); the reads of
+  // stage ks+1's first half (other buffer) into set A over the first kReadSlots MFMAs; in
+  // the last stage of a batch the next batch's scales are read and packed.
   template <int B, int S4, int I>
   __device__ __forceinline__ void half1_from(int ks_dma, int ks_next) {
     if constexpr (I < 16) {
       mfma_op<false, S4, I>();
-      dma_slot<B, S4, I, 0>(ks_dma, ks_next);
+      dma_slot<B, S4, 16 - kEarly + I>(ks_dma, ks_next);
       reads_of_slot<1 - B, 0, true, I>();
       if constexpr (S4 == 3 && I == 8) read_scale_rows<false, 0, 2>(ks_next >> 2, rsp);
       if constexpr (S4 == 3 && I == 9) read_scale_rows<true, 0, 2>(ks_next >> 2, rsq);
@@ -409,18 +434,19 @@ struct Tile {
     }
   }
 
-  // Stage ks, S4 = ks % 4 (buffer S4 % 2).  Between the halves, wait for this wave's DMA
-  // (stage ks+1, and the scale batch) and its reads of stage ks, then barrier: stage
-  // ks+1 is visible to all and buffer ks % 2 is free for stage ks+2.  Stages past the
-  // end are reloads of the last one (in bounds, never multiplied).
+  // Stage ks, S4 = ks % 4 (buffer S4 % 2).  Between the halves, wait for this wave's DMA of
+  // stage ks+1 (and older: the scale batch) -- loads complete in order, so all but the
+  // FF8_HALF0_DMAS just issued for stage ks+2 -- then barrier: stage ks+1 is visible to all.
+  // Stages past the end are reloads of the last one (in bounds, never multiplied).
   template <int S4>
   __device__ __forceinline__ void stage(int ks) {
     constexpr int B = S4 % 2;
-    half0_from<B, S4, 0>();
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    const int ks_dma = ks + 2 < nk ? ks + 2 : nk - 1;
+    half0_from<B, S4, 0>(ks_dma, ks + 1);
+    asm volatile("s_waitcnt vmcnt(" FF8_STR(FF8_HALF0_DMAS) ") lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    half1_from<B, S4, 0>(ks + 2 < nk ? ks + 2 : nk - 1, ks + 1);
+    half1_from<B, S4, 0>(ks_dma, ks + 1);
     if constexpr (S4 == 3) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {

@@ -528,21 +528,21 @@ def test_layer_stack_shared_workspace_and_saved_memory(ckpt):
             L.quantize_weights(d["w1"], d["w2"])
             L.release_saved()
         torch.cuda.synchronize()
-        base = torch.cuda.memory_allocated()
+        requested = lambda: torch.cuda.memory_stats()["requested_bytes.all.current"]  # exact tensor bytes
+        base = requested()
         x = d["x"]
         for L in layers:
             x = L.forward(x, d["topk_idx"], d["probs"])
         torch.cuda.synchronize()
-        kept = torch.cuda.memory_allocated() - base
+        kept = requested() - base
         g = d["dy"]
         for L in reversed(layers):
             g, _, _ = L.backward(g, d["probs"], release=True)
         torch.cuda.synchronize()
-        assert torch.cuda.memory_allocated() == base
+        assert requested() == base
         per_layer = stack[0].saved_activation_bytes()
         maps = 4 * (shape.T * shape.k + shape.E + 1 + stack[0].M_cap)
-        # torch's allocator rounds every block up to 512 bytes
-        assert 3 * (per_layer + maps) <= kept <= 3 * (per_layer + maps) + 3 * 16 * 512, (kept, per_layer, maps)
+        assert kept == 3 * (per_layer + maps), (kept, per_layer, maps)
         outs.append([{n: L.own[n].clone() for n in ("y", "dx", "dw1", "dw2")} for L in layers])
     for i in range(3):
         for n in ("y", "dx", "dw1", "dw2"):
