@@ -53,6 +53,7 @@ def parse():
     ap.add_argument("--no-hip-graph", action="store_true")
     ap.add_argument("--no-skew", action="store_true")
     ap.add_argument("--no-cast-accuracy", action="store_true")
+    ap.add_argument("--no-e8m0", action="store_true")
     return ap.parse_args()
 
 
@@ -407,6 +408,29 @@ def cast_accuracy(torch):
     return out
 
 
+def e8m0_scales(torch, d, shape, M, steps, warmup, ms_base, st_base):
+    """The step with every scale tensor stored as UE8M0 bytes (T + 127) instead of float32: step
+    time, each stage's time against the float32-scale step, and the scale bytes of the step's
+    tensors in both formats (every FP8 byte and output is bit-identical; the GPU tests check)."""
+    from paper_2511_02302_amd.layer import ExpertLayerFP8
+
+    L = ExpertLayerFP8(shape.T, shape.H, shape.E, shape.k, shape.I, scale_fmt="e8m0")
+    names = list(stage_costs(shape, M))
+    ms_step, st = timed_steps(torch, L, d, names, steps, warmup)
+    scale_names = [n for n, t in L.buf.items() if n.endswith("s") and n not in ("ws",) and t.dtype == torch.uint8]
+    bytes8 = sum(L.buf[n].numel() for n in scale_names)
+    out = {"ms_per_step": round(ms_step, 4), "ms_per_step_f32_scales": round(ms_base, 4),
+           "scale_tensors": sorted(scale_names), "scale_bytes": bytes8, "scale_bytes_f32": 4 * bytes8,
+           "stage_ms": {n: round(st[n], 4) for n in names},
+           "stage_change_vs_f32": {n: round(st[n] / st_base[n] - 1.0, 4) for n in names}}
+    gemm = [n for n in names if stage_costs(shape, M)[n][0] == "mfma"]
+    out["gemm_ms"] = round(sum(st[n] for n in gemm), 4)
+    out["gemm_ms_f32_scales"] = round(sum(st_base[n] for n in gemm), 4)
+    del L
+    torch.cuda.empty_cache()
+    return out
+
+
 def hip_graph(torch, L, d, steps, warmup, ms_eager, gemm_flops):
     """The whole step captured once as a HIP graph and replayed.  The path makes no host
     synchronization, allocation or memset, so one replay launches every kernel of the step
@@ -693,6 +717,8 @@ def main():
         rec["hip_graph"] = hip_graph(torch, L, d, args.steps, args.warmup, ms_step, gemm_flops)
     if not args.no_fp8_checkpoint:
         rec["fp8_checkpoint"]["measured_memory"] = checkpoint_memory(torch, shape, d)
+    if not args.no_e8m0 and shape.H % 512 == 0 and shape.I % 512 == 0:
+        rec["e8m0_scales"] = e8m0_scales(torch, d, shape, M, args.steps, args.warmup, ms_step, st_ms)
     if not args.no_cast_ops or not args.no_skew or not args.no_cast_accuracy:
         del L, d
         torch.cuda.empty_cache()

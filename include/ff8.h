@@ -62,6 +62,7 @@ extern "C" {
 
 typedef uint16_t ff8_bf16;
 typedef uint8_t ff8_e4m3;
+typedef uint8_t ff8_e8m0;  /* UE8M0 scale byte: the scale 2^T is stored as T + 127 */
 
 enum ff8_status {
   FF8_OK = 0,
@@ -300,6 +301,44 @@ int ff8_swiglu_bwd_quant_fp8a(const ff8_e4m3* a_q, const float* a_s, const ff8_b
  */
 int ff8_unpermute(const ff8_bf16* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k,
                   int64_t H, int64_t M_cap, ff8_bf16* y, void* stream);
+
+/* ---- UE8M0 scale storage ----
+ * Paper section 2.1 names UE8M0 (unsigned, 8 exponent bits, no mantissa) as the scale format of
+ * its recipe, and the power-of-two constraint of section 3.1 makes every scale exactly such a
+ * value: the scale 2^T, T in [-126, 127], is the byte T + 127 (the float32 scale's exponent
+ * field).  The entry points below are the ones above with every scale tensor in this format:
+ * the same shapes and layouts, one byte per scale instead of four, and bit-identical FP8 bytes,
+ * routing maps and outputs.  Consumers read the bytes as stored.  The grouped GEMMs move four
+ * scale bytes per DMA lane: fprop needs K % 512 == 0, dgrad N % 512 == 0 and K % 512 == 0
+ * (FF8_ERR_SHAPE otherwise); wgrad takes any multiple of 128.
+ */
+int ff8_quant_rowwise_e8m0(const ff8_bf16* x, int64_t rows, int64_t cols, ff8_e4m3* q, ff8_e8m0* s, void* stream);
+int ff8_quant_block128_e8m0(const ff8_bf16* w, int64_t rows, int64_t cols, ff8_e4m3* q, ff8_e8m0* s, void* stream);
+/* ff8_permute_quant_aligned with UE8M0 scales (align 16, 32, 64 or 128; padding rows get byte 1, i.e. 2^-126). */
+int ff8_permute_quant_e8m0(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                           const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
+                           int64_t M_cap, ff8_e4m3* q, ff8_e8m0* s, void* workspace, size_t ws_bytes, int align,
+                           void* stream);
+int ff8_scaling_aware_transpose_e8m0(const ff8_e4m3* q, const ff8_e8m0* s, int64_t rows, int64_t cols,
+                                     const int32_t* offsets, int E, ff8_e4m3* qT, ff8_e8m0* sT, void* stream);
+int ff8_grouped_gemm_fprop_e8m0(const ff8_e4m3* a, const ff8_e8m0* a_s, const ff8_e4m3* w, const ff8_e8m0* w_s,
+                                const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
+                                void* stream);
+int ff8_grouped_gemm_dgrad_e8m0(const ff8_e4m3* g, const ff8_e8m0* g_s, const ff8_e4m3* w, const ff8_e8m0* w_s,
+                                const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
+                                void* stream);
+int ff8_grouped_gemm_wgrad_e8m0(const ff8_e4m3* gT, const ff8_e8m0* gT_s, const ff8_e4m3* xT, const ff8_e8m0* xT_s,
+                                const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, float* dw,
+                                int accumulate, void* stream);
+int ff8_swiglu_quant_e8m0(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I, ff8_e4m3* hq,
+                          ff8_e8m0* hs, void* stream);
+int ff8_swiglu_bwd_quant_e8m0(const ff8_bf16* a, const ff8_bf16* dh, const int32_t* offsets, int E, int64_t M_cap,
+                              int64_t I, ff8_e4m3* daq, ff8_e8m0* das, void* stream);
+int ff8_swiglu_quant_keep_fp8_e8m0(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                                   ff8_e4m3* hq, ff8_e8m0* hs, ff8_e4m3* a_q, ff8_e8m0* a_s, void* stream);
+int ff8_swiglu_bwd_quant_fp8a_e8m0(const ff8_e4m3* a_q, const ff8_e8m0* a_s, const ff8_bf16* dh,
+                                   const int32_t* offsets, int E, int64_t M_cap, int64_t I, ff8_e4m3* daq,
+                                   ff8_e8m0* das, void* stream);
 
 /* ---- element casts (the codec every quantizer uses; exposed for exhaustive checks) ---- */
 

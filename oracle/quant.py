@@ -50,6 +50,17 @@ def scale_from_exponent(t):
     return np.ldexp(np.float32(1.0), np.asarray(t, dtype=np.int64)).astype(np.float32)
 
 
+def scale_to_e8m0(s):
+    """UE8M0 byte of power-of-two scales 2^T (section 2.1 names UE8M0 as the recipe's scale
+    format; the power-of-two constraint of section 3.1 makes every scale one): T + 127."""
+    return (exponent_of_scale(s) + 127).astype(np.uint8)
+
+
+def e8m0_to_scale(b):
+    """Value of UE8M0 bytes as float32: 2^(b - 127)."""
+    return scale_from_exponent(np.asarray(b, dtype=np.int64) - 127)
+
+
 def exponent_of_scale(s):
     """Exact integer log2 of power-of-two scales (raises if a scale is not a power of two)."""
     s = np.asarray(s, dtype=np.float64)

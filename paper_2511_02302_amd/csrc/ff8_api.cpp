@@ -138,9 +138,10 @@ static int permute_validate(const char* fn, const void* x, int64_t T, int64_t H,
   return FF8_OK;
 }
 
+template <typename SC>
 static int permute_launch(const char* fn, const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                           const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
-                          int64_t M_cap, ff8_e4m3* q, float* s, void* workspace, int align, hipStream_t st) {
+                          int64_t M_cap, ff8_e4m3* q, SC* s, void* workspace, int align, hipStream_t st) {
   if (!reuse_map) {
     const int rc = hip_status(
         ff8::launch_route(topk_idx, T, k, E, align, row_map, offsets, src_row, M_cap, workspace, st), fn);
@@ -310,6 +311,111 @@ int ff8_unpermute(const ff8_bf16* y_perm, const int32_t* row_map, const float* r
     REQUIRE_PTR(y_perm); REQUIRE_PTR(row_map); REQUIRE_PTR(y);
   }
   return hip_status(ff8::launch_unpermute(y_perm, row_map, row_w, T, k, H, M_cap, y, as_stream(stream)), __func__);
+}
+
+/* ---- UE8M0 scale storage: the same operations with one scale byte T + 127 ---- */
+
+int ff8_quant_rowwise_e8m0(const ff8_bf16* x, int64_t rows, int64_t cols, ff8_e4m3* q, ff8_e8m0* s, void* stream) {
+  REQUIRE_PTR(x); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  REQUIRE_SHAPE(rows >= 1 && mult128(cols));
+  return hip_status(ff8::launch_quant_rowwise(x, rows, cols, q, s, as_stream(stream)), __func__);
+}
+
+int ff8_quant_block128_e8m0(const ff8_bf16* w, int64_t rows, int64_t cols, ff8_e4m3* q, ff8_e8m0* s, void* stream) {
+  REQUIRE_PTR(w); REQUIRE_PTR(q); REQUIRE_PTR(s);
+  REQUIRE_SHAPE(mult128(rows) && mult128(cols));
+  return hip_status(ff8::launch_quant_block128(w, rows, cols, q, s, as_stream(stream)), __func__);
+}
+
+int ff8_permute_quant_e8m0(const ff8_bf16* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                           const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
+                           int64_t M_cap, ff8_e4m3* q, ff8_e8m0* s, void* workspace, size_t ws_bytes, int align,
+                           void* stream) {
+  const int rc = permute_validate(__func__, x, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
+                                  workspace, ws_bytes, align, true);
+  if (rc != FF8_OK) return rc;
+  return permute_launch(__func__, x, row_w, T, H, k, E, topk_idx, reuse_map, row_map, offsets, src_row, M_cap, q, s,
+                        workspace, align, as_stream(stream));
+}
+
+int ff8_scaling_aware_transpose_e8m0(const ff8_e4m3* q, const ff8_e8m0* s, int64_t rows, int64_t cols,
+                                     const int32_t* offsets, int E, ff8_e4m3* qT, ff8_e8m0* sT, void* stream) {
+  REQUIRE_PTR(q); REQUIRE_PTR(s); REQUIRE_PTR(qT); REQUIRE_PTR(sT);
+  REQUIRE_SHAPE(mult128(rows) && mult128(cols));
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_sat(q, s, rows, cols, offsets, E, qT, sT, as_stream(stream)), __func__);
+}
+
+int ff8_grouped_gemm_fprop_e8m0(const ff8_e4m3* a, const ff8_e8m0* a_s, const ff8_e4m3* w, const ff8_e8m0* w_s,
+                                const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
+                                void* stream) {
+  const int rc = gemm_common(__func__, a, a_s, w, w_s, offsets, E, M_cap, N, K, out, true);
+  if (rc != FF8_OK) return rc;
+  REQUIRE_SHAPE(K % 512 == 0);  // the scale DMAs move dwords of four K-block bytes
+  return hip_status(ff8::launch_grouped_gemm(ff8::kFprop, a, a_s, w, w_s, offsets, E, M_cap, N, K, out, 0,
+                                             as_stream(stream)),
+                    __func__);
+}
+
+int ff8_grouped_gemm_dgrad_e8m0(const ff8_e4m3* g, const ff8_e8m0* g_s, const ff8_e4m3* w, const ff8_e8m0* w_s,
+                                const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
+                                void* stream) {
+  const int rc = gemm_common(__func__, g, g_s, w, w_s, offsets, E, M_cap, N, K, out, true);
+  if (rc != FF8_OK) return rc;
+  REQUIRE_SHAPE(N % 512 == 0 && K % 512 == 0);  // the scale DMAs move dwords of four scale bytes
+  return hip_status(ff8::launch_grouped_gemm(ff8::kDgrad, g, g_s, w, w_s, offsets, E, M_cap, N, K, out, 0,
+                                             as_stream(stream)),
+                    __func__);
+}
+
+int ff8_grouped_gemm_wgrad_e8m0(const ff8_e4m3* gT, const ff8_e8m0* gT_s, const ff8_e4m3* xT, const ff8_e8m0* xT_s,
+                                const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, float* dw,
+                                int accumulate, void* stream) {
+  const int rc = gemm_common(__func__, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw, false);
+  if (rc != FF8_OK) return rc;
+  REQUIRE_ARG(accumulate == 0 || accumulate == 1);
+  return hip_status(ff8::launch_grouped_gemm(ff8::kWgrad, gT, gT_s, xT, xT_s, offsets, E, M_cap, N, K, dw,
+                                             accumulate, as_stream(stream)),
+                    __func__);
+}
+
+int ff8_swiglu_quant_e8m0(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I, ff8_e4m3* hq,
+                          ff8_e8m0* hs, void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(hq); REQUIRE_PTR(hs);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_quant(a, offsets, E, M_cap, I, hq, hs, as_stream(stream)), __func__);
+}
+
+int ff8_swiglu_bwd_quant_e8m0(const ff8_bf16* a, const ff8_bf16* dh, const int32_t* offsets, int E, int64_t M_cap,
+                              int64_t I, ff8_e4m3* daq, ff8_e8m0* das, void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(dh); REQUIRE_PTR(daq); REQUIRE_PTR(das);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_bwd_quant(a, dh, offsets, E, M_cap, I, daq, das, as_stream(stream)), __func__);
+}
+
+int ff8_swiglu_quant_keep_fp8_e8m0(const ff8_bf16* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                                   ff8_e4m3* hq, ff8_e8m0* hs, ff8_e4m3* a_q, ff8_e8m0* a_s, void* stream) {
+  REQUIRE_PTR(a); REQUIRE_PTR(hq); REQUIRE_PTR(hs); REQUIRE_PTR(a_q); REQUIRE_PTR(a_s);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(ff8::launch_swiglu_quant_keep_fp8(a, offsets, E, M_cap, I, hq, hs, a_q, a_s, as_stream(stream)),
+                    __func__);
+}
+
+int ff8_swiglu_bwd_quant_fp8a_e8m0(const ff8_e4m3* a_q, const ff8_e8m0* a_s, const ff8_bf16* dh,
+                                   const int32_t* offsets, int E, int64_t M_cap, int64_t I, ff8_e4m3* daq,
+                                   ff8_e8m0* das, void* stream) {
+  REQUIRE_PTR(a_q); REQUIRE_PTR(a_s); REQUIRE_PTR(dh); REQUIRE_PTR(daq); REQUIRE_PTR(das);
+  REQUIRE_SHAPE(M_cap >= 1 && mult128(I));
+  REQUIRE_SHAPE(M_cap * (I / 8) / 256 < ((int64_t)1 << 31));  // grid size
+  if (offsets) REQUIRE_ARG(E >= 1);
+  return hip_status(
+      ff8::launch_swiglu_bwd_quant_fp8a(a_q, a_s, dh, offsets, E, M_cap, I, daq, das, as_stream(stream)), __func__);
 }
 
 int ff8_cast_f32_to_e4m3(const float* x, int64_t n, ff8_e4m3* q, void* stream) {

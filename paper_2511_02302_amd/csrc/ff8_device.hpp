@@ -51,6 +51,16 @@ __device__ __forceinline__ int scale_exponent(float amax) {
 }
 __device__ __forceinline__ float exp2i(int t) { return __uint_as_float((uint32_t)(t + 127) << 23); }
 
+// Scale storage.  A power-of-two scale 2^T is stored either as float32 (its exponent field
+// holds T + 127, mantissa zero) or as one UE8M0 byte holding the same T + 127.
+typedef uint8_t e8m0_t;
+__device__ __forceinline__ void put_scale(float* p, int t) { *p = exp2i(t); }
+__device__ __forceinline__ void put_scale(e8m0_t* p, int t) { *p = (e8m0_t)(t + 127); }
+__device__ __forceinline__ int scale_exp(float s) { return (int)(__float_as_uint(s) >> 23) - 127; }
+__device__ __forceinline__ int scale_exp(e8m0_t b) { return (int)b - 127; }
+__device__ __forceinline__ float scale_value(float s) { return s; }
+__device__ __forceinline__ float scale_value(e8m0_t b) { return exp2i((int)b - 127); }
+
 // Encode two floats already in [-448, 448] into the low (kHi = false) or high
 // (kHi = true) 16 bits of `old` with the hardware RNE conversion.
 template <bool kHi>

@@ -92,9 +92,9 @@ __device__ __forceinline__ uint32_t scale_lds(int b) {
 
 struct GemmArgs {
   const uint8_t* P;   // fprop: w; dgrad: w; wgrad: xT
-  const float* sP;
+  const void* sP;     // scales: float, or UE8M0 bytes
   const uint8_t* Q;   // fprop: a; dgrad: g; wgrad: gT
-  const float* sQ;
+  const void* sQ;
   const int32_t* offsets;
   void* out;
   int E;
@@ -168,16 +168,20 @@ __device__ __forceinline__ int opaque_lane() {
   return l;
 }
 
-// Per-thread state of one workgroup tile.
-template <int MODE>
+// Per-thread state of one workgroup tile.  SC: scale storage, float (fp32 powers of two)
+// or e8m0_t (UE8M0 bytes); either way the MFMA receives the E8M0 byte.
+template <int MODE, typename SC>
 struct Tile {
+  static constexpr bool kE8 = sizeof(SC) == 1;
+  static constexpr uint32_t kSB = sizeof(SC);  // bytes per stored scale
   f32x16 acc[4][4];
   i32x8 fpA[4], fqA[4], fpB[4], fqB[4];  // set A: first half-step, set B: second
   // Packed E8M0 scales of the current batch of four K blocks, per K block: byte R of
   // cp[j] is the scale of this lane's P row 128 wp + 32 R + l (cq: Q rows); np/nq are
   // the next batch, assembled during the last stage of the current one.
   uint32_t cp[4], cq[4], np[4], nq[4];
-  u32x4 rsp[4], rsq[4];  // raw fp32 scale rows of the next batch, between read and pack
+  u32x4 rsp[4], rsq[4];  // raw scale rows of the next batch, between read and pack
+  uint32_t p_shift;      // dgrad with UE8M0 scales: bit offset of the wave's weight-block byte in its dword
   // DMA sources: one resource per tensor; per-lane byte offsets of this tile's stage 0
   // for the two row-group patterns of the tile DMA (instruction i uses pattern i / 4,
   // dgrad P: i % 2), and wave-uniform steps between instructions and stages.
@@ -186,7 +190,7 @@ struct Tile {
   uint32_t sp_off, sq_off;       // scale DMA: this lane's source offset at K block 0
   int p_kstep, q_kstep;          // bytes per stage of the P / Q source
   int p_istep, q_istep;          // bytes between instructions of one pattern
-  int sp_kb, sq_kb;              // floats per K block of the P / Q scale sources
+  int sp_kb, sq_kb;              // scales per K block of the P / Q scale sources
   // fprop / dgrad: a wave's 128 P rows are one 128x128 weight block, so its P scale is one
   // value per K block (stored compactly as [tile half][4 K blocks]); wgrad: one per row.
   static constexpr bool kBlockP = (MODE != kWgrad);
@@ -245,31 +249,42 @@ struct Tile {
   }
   // Scale DMA of batch b (K blocks kb0..kb0+3 in loop order) into batch buffer b % 2:
   //   fprop / dgrad P (kBlockP): 8 lanes carry the tile's two weight blocks' 4 floats (the
-  //     rest duplicate them) -> LDS P rows 0 and 1, four floats each;
-  //   fprop / dgrad Q (row-major scales [rows][K/128]): lane l carries the four floats of
-  //     tile row 64 wave + l -> LDS [row][4];
+  //     rest duplicate them) -> LDS P rows 0 and 1, four floats each; with UE8M0 bytes each
+  //     lane carries the dword holding its byte (fprop: the 4 K blocks' bytes of its row;
+  //     dgrad: the K block's byte at bit offset p_shift);
+  //   fprop / dgrad Q (row-major scales [rows][K/128]): lane l carries the four scales of
+  //     tile row 64 wave + l (16 or 4 bytes) -> LDS [row][4];
   //   wgrad P and Q (block-major scales [M_cap/128][rows]): wave w carries K block kb0 + w,
-  //     lane l the tile rows 4l..4l+3, one contiguous 1 KB run -> LDS [K block][256 rows].
+  //     lane l the tile rows 4l..4l+3, one contiguous 1 KB (256-byte) run -> LDS [K block][256 rows].
   // Batches are rotated with the K order (k_rot is a multiple of the batch); blocks past
   // the last K block read neighbouring scales or zeros and are never multiplied.
   __device__ __forceinline__ void dma_scale_p(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1));
     if constexpr (kBlockP) {
       const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-      dma4(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * 4u, lbase);
+      dma4(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * kSB, lbase);
     } else {  // wgrad: wave w takes the block of stage 4 b + w (the rotation may wrap inside a batch)
       const uint32_t kbw = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch + wave));
-      dma16(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
+      if constexpr (kE8)
+        dma4(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb, lbase + (uint32_t)wave * 256u);
+      else
+        dma16(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
     }
   }
   __device__ __forceinline__ void dma_scale_q(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1)) + kTP * kScaleBatch * 4;
     if constexpr (MODE == kWgrad) {
       const uint32_t kbw = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch + wave));
-      dma16(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
+      if constexpr (kE8)
+        dma4(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb, lbase + (uint32_t)wave * 256u);
+      else
+        dma16(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
     } else {
       const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-      dma16(sq_rsrc, sq_off + kb0 * 4u, lbase + (uint32_t)wave * 1024u);
+      if constexpr (kE8)
+        dma4(sq_rsrc, sq_off + kb0, lbase + (uint32_t)wave * 256u);
+      else
+        dma16(sq_rsrc, sq_off + kb0 * 4u, lbase + (uint32_t)wave * 1024u);
     }
   }
 
@@ -322,6 +337,18 @@ struct Tile {
     const int l31 = opaque_lane() & 31;  // recomputed here rather than held through the tile
     if constexpr (!kQ && kBlockP) {
       if constexpr (R0 == 0) raw[0] = S[wp];
+    } else if constexpr (kE8) {
+      const uint8_t* B8 = reinterpret_cast<const uint8_t*>(&g_sc[b & 1][kQ ? kTP * kScaleBatch : 0]);
+      if constexpr (MODE == kWgrad) {  // [K block][256 row bytes]
+        const int row = (kQ ? 128 * wq : 128 * wp) + l31;
+#pragma unroll
+        for (int R = R0; R < R1; ++R)
+#pragma unroll
+          for (int j = 0; j < kScaleBatch; ++j) raw[R][j] = B8[j * kTP + row + 32 * R];
+      } else {  // Q rows: one dword of four K-block bytes each
+#pragma unroll
+        for (int R = R0; R < R1; ++R) raw[R][0] = reinterpret_cast<const uint32_t*>(B8)[128 * wq + 32 * R + l31];
+      }
     } else if constexpr (MODE == kWgrad) {  // [K block][256 rows]
       const float* F = &g_sc[b & 1][kQ ? kTP * kScaleBatch : 0];
       const int row = (kQ ? 128 * wq : 128 * wp) + l31;
@@ -335,10 +362,28 @@ struct Tile {
     }
   }
   // ... and pack them: word j holds the E8M0 byte (the fp32 exponent field of a
-  // positive power of two) of row R in byte R (rows R0..R1-1 added to the word).
+  // positive power of two, or the stored UE8M0 byte) of row R in byte R (rows R0..R1-1
+  // added to the word).
   template <bool kQ, int R0, int R1>
-  __device__ __forceinline__ static void pack_scales(const u32x4 (&raw)[4], uint32_t (&dst)[4]) {
-    if constexpr (!kQ && kBlockP) {
+  __device__ __forceinline__ void pack_scales(const u32x4 (&raw)[4], uint32_t (&dst)[4]) const {
+    if constexpr (kE8) {
+      if constexpr (!kQ && kBlockP) {
+        if constexpr (R0 == 0) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            dst[j] = (((MODE == kFprop) ? raw[0][0] >> (8 * j) : raw[0][j] >> p_shift) & 0xffu) * 0x01010101u;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t v = (R0 == 0) ? 0u : dst[j];
+#pragma unroll
+          for (int R = R0; R < R1; ++R)
+            v |= (((MODE == kWgrad) ? raw[R][j] : raw[R][0] >> (8 * j)) & 0xffu) << (8 * R);
+          dst[j] = v;
+        }
+      }
+    } else if constexpr (!kQ && kBlockP) {
       if constexpr (R0 == 0) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) dst[j] = (raw[0][j] >> 23) * 0x01010101u;
@@ -520,8 +565,9 @@ __device__ __forceinline__ bool decode_tile(const GemmArgs& g, int blk, int w_in
 // tile DMA instruction i writes LDS bytes 16 l .. of that instruction's 1 KB).  Offsets are
 // 32-bit (the host keeps every operand under 4 GiB); past an operand's end they may wrap,
 // which only feeds rows or columns that are never stored.
-template <int MODE>
-__device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, const TileInfo& t) {
+template <int MODE, typename SC>
+__device__ __forceinline__ void setup_tile(Tile<MODE, SC>& T, const GemmArgs& g, const TileInfo& t) {
+  constexpr uint32_t kSB = sizeof(SC);
   const uint32_t lane = (uint32_t)opaque_lane(), wave = (uint32_t)T.wave, e = (uint32_t)t.e;
   const uint32_t q0 = (uint32_t)t.q0, k0 = (uint32_t)t.k0, p0 = (uint32_t)t.p0;
   const uint32_t Np = (uint32_t)g.Np, Kdim = (uint32_t)g.Kdim, M_cap = (uint32_t)g.M_cap;
@@ -567,42 +613,47 @@ __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, con
   }
   // scale DMA sources (resources range-checked to the end of each scale tensor; offsets
   // are at K block 0 of the tile, the batch adds its K-block offset)
-  const float* sp_base;
+  const SC* sp_base;
   uint32_t sp_total, sq_total;
   if (MODE == kWgrad) {  // block-major: xT_s [M_cap/128][Np], gT_s [M_cap/128][Nq]
     const uint32_t Nq = (uint32_t)g.Nq, kb_first = k0 / kTile;
-    sp_base = g.sP;
+    sp_base = static_cast<const SC*>(g.sP);
     T.sp_kb = (int)Np;
     T.sq_kb = (int)Nq;
     sp_total = (M_cap / kTile) * Np;
     sq_total = (M_cap / kTile) * Nq;
-    T.sp_off = (kb_first * Np + p0 + 4 * lane) * 4;
-    T.sq_off = (kb_first * Nq + q0 + 4 * lane) * 4;
+    T.sp_off = (kb_first * Np + p0 + 4 * lane) * kSB;
+    T.sq_off = (kb_first * Nq + q0 + 4 * lane) * kSB;
   } else {
     // Q: row-major a_s / g_s [M_cap][Kdim/128], lane l of wave w carries tile row 64 w + l
     const uint32_t q_sld = Kdim / kTile;
     const uint32_t q = min(q0 + 64 * wave + lane, q_rows - 1);
     T.sq_kb = 1;
     sq_total = q_rows * q_sld;
-    T.sq_off = q * q_sld * 4;
+    T.sq_off = q * q_sld * kSB;
     // P: the tile's two weight block rows, four K blocks per lane group of four
     const uint32_t pb = min(p0 / kTile + ((lane >> 2) & 1), Np / kTile - 1);
     const uint32_t j = lane & 3;
     if (MODE == kFprop) {  // w_s [E][Np/128][Kdim/128]
-      sp_base = g.sP + (size_t)e * (Np / kTile) * (Kdim / kTile);
+      sp_base = static_cast<const SC*>(g.sP) + (size_t)e * (Np / kTile) * (Kdim / kTile);
       T.sp_kb = 1;
       sp_total = ((uint32_t)g.E - e) * (Np / kTile) * (Kdim / kTile);
-      T.sp_off = (pb * (Kdim / kTile) + j) * 4;
+      // UE8M0: every lane of a row loads the dword of its four K-block bytes (K/128 and the
+      // batch start are multiples of 4)
+      T.sp_off = (kSB == 1) ? pb * (Kdim / kTile) : (pb * (Kdim / kTile) + j) * 4;
     } else {  // w_s [E][Kdim/128][Np/128]
-      sp_base = g.sP + (size_t)e * (Kdim / kTile) * (Np / kTile);
+      sp_base = static_cast<const SC*>(g.sP) + (size_t)e * (Kdim / kTile) * (Np / kTile);
       T.sp_kb = (int)(Np / kTile);
       sp_total = ((uint32_t)g.E - e) * (Kdim / kTile) * (Np / kTile);
-      T.sp_off = (j * (Np / kTile) + pb) * 4;
+      // UE8M0: the dword holding the byte (Np/128 is a multiple of 4, so the byte's offset in
+      // it is pb % 4 for every K block); the wave's own block row gives the shift
+      T.sp_off = (kSB == 1) ? j * (Np / kTile) + (pb & ~3u) : (j * (Np / kTile) + pb) * 4;
+      T.p_shift = (uint32_t)__builtin_amdgcn_readfirstlane((int)(8 * (min(p0 / kTile + (uint32_t)T.wp, Np / kTile - 1) & 3u)));
     }
   }
-  const float* sq_base = g.sQ;
-  T.sp_rsrc = make_rsrc(sp_base, sp_total * 4);
-  T.sq_rsrc = make_rsrc(sq_base, sq_total * 4);
+  const SC* sq_base = static_cast<const SC*>(g.sQ);
+  T.sp_rsrc = make_rsrc(sp_base, sp_total * kSB);
+  T.sq_rsrc = make_rsrc(sq_base, sq_total * kSB);
   // Blocks start their K loops at different scale-batch-aligned stages, so that the XCDs
   // running together stream different K bands of the operand rows (spread over memory
   // channels) while the 32 tiles of one block still share every stage through their L2.
@@ -623,8 +674,8 @@ __device__ __forceinline__ void setup_tile(Tile<MODE>& T, const GemmArgs& g, con
 // The stores are non-temporal: the output is not re-read here, and streaming it keeps the
 // operand panels that the XCD's other workgroups are still reading in L2.  A wave only
 // rewrites its own region, after its own reads (LDS order), so passes need no barrier.
-template <int MODE>
-__device__ __forceinline__ void epilogue(Tile<MODE>& T, const GemmArgs& g, const TileInfo& t) {
+template <int MODE, typename SC>
+__device__ __forceinline__ void epilogue(Tile<MODE, SC>& T, const GemmArgs& g, const TileInfo& t) {
   const int lane = opaque_lane(), wave = T.wave, wp = T.wp, wq = T.wq;
   lds_u8* const region = (lds_u8*)g_st1 + wave * 16384;
   const int l31 = lane & 31, h = lane >> 5;
@@ -710,8 +761,8 @@ __device__ __forceinline__ void epilogue(Tile<MODE>& T, const GemmArgs& g, const
 }
 
 // First-stage DMA of a tile: stage 0 into buffer 0, then the scale batch 0 (buffer 0).
-template <int MODE>
-__device__ __forceinline__ void dma_first_stage(Tile<MODE>& T) {
+template <int MODE, typename SC>
+__device__ __forceinline__ void dma_first_stage(Tile<MODE, SC>& T) {
   T.template dma_tile<0, 0, MODE == kWgrad>(0); T.template dma_tile<0, 1, MODE == kWgrad>(0); T.template dma_tile<0, 2, MODE == kWgrad>(0);
   T.template dma_tile<0, 3, MODE == kWgrad>(0); T.template dma_tile<0, 4, MODE == kWgrad>(0); T.template dma_tile<0, 5, MODE == kWgrad>(0);
   T.template dma_tile<0, 6, MODE == kWgrad>(0); T.template dma_tile<0, 7, MODE == kWgrad>(0); T.template dma_tile<0, 8, MODE == kWgrad>(0);
@@ -724,8 +775,8 @@ __device__ __forceinline__ void dma_first_stage(Tile<MODE>& T) {
 // Second-stage DMA (stage 1, or a reload of stage 0 when nk == 1) into buffer 1: exactly
 // kStage1Dma instructions per wave, the newest in flight when stage 0 is awaited.
 constexpr int kStage1Dma = 16;
-template <int MODE>
-__device__ __forceinline__ void dma_second_stage(Tile<MODE>& T) {
+template <int MODE, typename SC>
+__device__ __forceinline__ void dma_second_stage(Tile<MODE, SC>& T) {
   const int s1 = T.nk > 1 ? 1 : 0;
   T.template dma_tile<1, 0, MODE == kWgrad>(s1); T.template dma_tile<1, 1, MODE == kWgrad>(s1); T.template dma_tile<1, 2, MODE == kWgrad>(s1);
   T.template dma_tile<1, 3, MODE == kWgrad>(s1); T.template dma_tile<1, 4, MODE == kWgrad>(s1); T.template dma_tile<1, 5, MODE == kWgrad>(s1);
@@ -801,10 +852,10 @@ __device__ __forceinline__ bool next_tile(const GemmArgs& g, int xcd, int slot, 
   return false;
 }
 
-template <int MODE>
+template <int MODE, typename SC>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   const int tid = threadIdx.x;
-  Tile<MODE> T;
+  Tile<MODE, SC> T;
   T.lane = tid & 63;
   T.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   T.wp = T.wave & 1;
@@ -866,8 +917,8 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
   int k = group * kRoundsPerWg;
   TileInfo t;
   if (!next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, use_share, k, t)) return;
-  setup_tile<MODE>(T, g, t);
-  if (T.nk > 0) dma_first_stage<MODE>(T);
+  setup_tile<MODE, SC>(T, g, t);
+  if (T.nk > 0) dma_first_stage<MODE, SC>(T);
   // Loop invariant: tile t is set up, its stage 0 and scale batch 0 are in flight (if it
   // has any K), and stage buffer 1 is free.
   for (;;) {
@@ -879,7 +930,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
         for (int v = 0; v < 16; ++v) T.acc[a][b][v] = 0.0f;
     const int nk = T.nk;
     if (nk > 0) {
-      dma_second_stage<MODE>(T);
+      dma_second_stage<MODE, SC>(T);
       // stage 0 and scale batch 0 have landed when at most the stage-1 DMAs are in flight
       // (loads retire in order; older epilogue stores still in flight only make this wait longer)
       asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory");
@@ -905,10 +956,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(GemmArgs g) {
     ++k;
     const bool more = next_tile<MODE>(g, xcd, slot, n_slots, n_blocks, k_end, use_share, k, tn);
     if (more) {
-      setup_tile<MODE>(T, g, tn);
-      if (T.nk > 0) dma_first_stage<MODE>(T);  // buffer 0 and scale batch 0, under the epilogue
+      setup_tile<MODE, SC>(T, g, tn);
+      if (T.nk > 0) dma_first_stage<MODE, SC>(T);  // buffer 0 and scale batch 0, under the epilogue
     }
-    if (!(MODE == kWgrad && t.nk == 0 && g.accumulate)) epilogue<MODE>(T, g, t);
+    if (!(MODE == kWgrad && t.nk == 0 && g.accumulate)) epilogue<MODE, SC>(T, g, t);
     if (!more) break;
     t = tn;
     lds_barrier();  // buffer 1 is free for the next tile's second stage
@@ -934,9 +985,10 @@ int64_t blocks_of(int n_pt, int64_t n_qg) { return (int64_t)((n_pt + kBP - 1) / 
 
 }  // namespace
 
-hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s, const uint8_t* b,
-                               const float* b_s, const int32_t* offsets, int E, int64_t M_cap, int64_t N,
-                               int64_t K, void* out, int accumulate, hipStream_t st) {
+template <typename SC>
+static hipError_t grouped_gemm_impl(GemmMode mode, const uint8_t* a, const SC* a_s, const uint8_t* b, const SC* b_s,
+                                    const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, void* out,
+                                    int accumulate, hipStream_t st) {
   GemmArgs g{};
   g.offsets = offsets;
   g.out = out;
@@ -953,12 +1005,12 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
     g.Np = N; g.Kdim = K;
     g.n_pt = (int)((N + kTP - 1) / kTP);
     grid = grid_blocks(blocks_of(g.n_pt, qt_bound), g.n_slots);
-    grouped_gemm_kernel<kFprop><<<grid, kThreads, 0, st>>>(g);
+    grouped_gemm_kernel<kFprop, SC><<<grid, kThreads, 0, st>>>(g);
   } else if (mode == kDgrad) {  // out[m, k] = g[m, :] . w[e, :, k]
     g.Np = K; g.Kdim = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
     grid = grid_blocks(blocks_of(g.n_pt, qt_bound), g.n_slots);
-    grouped_gemm_kernel<kDgrad><<<grid, kThreads, 0, st>>>(g);
+    grouped_gemm_kernel<kDgrad, SC><<<grid, kThreads, 0, st>>>(g);
   } else {  // dw[e, n, k] = sum_m gT[n, m] xT[k, m]
     g.Np = K; g.Nq = N;
     g.n_pt = (int)((K + kTP - 1) / kTP);
@@ -981,9 +1033,20 @@ hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s
     const int64_t blocks_items = (blocks_of(g.n_pt, (int64_t)E * g.n_qt) + 7) / 8 * kPersistSlots;
     const int64_t share_items = (int64_t)E * g.share;
     grid = grid_items(share_items > blocks_items ? share_items : blocks_items, g.n_slots);
-    grouped_gemm_kernel<kWgrad><<<grid, kThreads, 0, st>>>(g);
+    grouped_gemm_kernel<kWgrad, SC><<<grid, kThreads, 0, st>>>(g);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const float* a_s, const uint8_t* b,
+                               const float* b_s, const int32_t* offsets, int E, int64_t M_cap, int64_t N,
+                               int64_t K, void* out, int accumulate, hipStream_t st) {
+  return grouped_gemm_impl(mode, a, a_s, b, b_s, offsets, E, M_cap, N, K, out, accumulate, st);
+}
+hipError_t launch_grouped_gemm(GemmMode mode, const uint8_t* a, const e8m0_t* a_s, const uint8_t* b,
+                               const e8m0_t* b_s, const int32_t* offsets, int E, int64_t M_cap, int64_t N,
+                               int64_t K, void* out, int accumulate, hipStream_t st) {
+  return grouped_gemm_impl(mode, a, a_s, b, b_s, offsets, E, M_cap, N, K, out, accumulate, st);
 }
 
 }  // namespace ff8

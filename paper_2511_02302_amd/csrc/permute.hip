@@ -139,12 +139,12 @@ __global__ __launch_bounds__(64) void route_assign_kernel(const int32_t* __restr
 // lanes one 128-element tile (8-lane DPP amax).  The token's k destination rows and
 // weights are workgroup-uniform (scalar loads); every copy is one 16-byte store per lane,
 // so a wave writes 1 KB contiguous of one destination row.
-template <bool kWeighted>
+template <bool kWeighted, typename S>
 __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uint16_t* __restrict__ x,
                                                                        const float* __restrict__ row_w, int64_t H,
                                                                        int k, const int32_t* __restrict__ row_map,
                                                                        int64_t M_cap, uint8_t* __restrict__ q,
-                                                                       float* __restrict__ s) {
+                                                                       S* __restrict__ s) {
   const int64_t t = blockIdx.x;
   const int64_t n16 = H / 16, sh = H / kTile;
   for (int64_t c = threadIdx.x; c < n16; c += blockDim.x) {  // uniform per 8-lane tile
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uin
         const int row = row_map[t * k + j];
         if (row >= 0 && row < M_cap) {
           stnt16(q + (int64_t)row * H + c * 16, r);
-          if (leader) s[(int64_t)row * sh + (c >> 3)] = exp2i(tq);
+          if (leader) put_scale(&s[(int64_t)row * sh + (c >> 3)], tq);
         }
       }
     } else {
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uin
           int tq;
           const u32x4 r = quant16_tile8(vw, tq);
           stnt16(q + (int64_t)row * H + c * 16, r);
-          if (leader) s[(int64_t)row * sh + (c >> 3)] = exp2i(tq);
+          if (leader) put_scale(&s[(int64_t)row * sh + (c >> 3)], tq);
         }
       }
     }
@@ -244,9 +244,10 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_dprobs_kernel(
 // kPadSplit workgroups share a block: wave w of part p takes rows p * 4 + w + 32 j, a
 // fixed partition, so every padding row is written exactly once.
 constexpr int kPadSplit = 8;
+template <typename S>
 __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __restrict__ offsets, int E,
                                                             const int32_t* __restrict__ src_row, int H,
-                                                            uint8_t* __restrict__ q, float* __restrict__ s) {
+                                                            uint8_t* __restrict__ q, S* __restrict__ s) {
   const int blk = blockIdx.x / kPadSplit, part = blockIdx.x - blk * kPadSplit;
   const int64_t r0 = (int64_t)blk * kTile, r_end = offsets[E];
   if (r0 >= r_end) return;
@@ -258,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __res
     if (r >= r_end || src_row[r] >= 0) continue;  // wave-uniform (groups padded to 16 may end inside a block)
     uint8_t* row = q + r * H;
     for (int c = lane; c < c16; c += 64) stnt16(row + c * 16, z);
-    for (int c = lane; c < sh; c += 64) s[r * sh + c] = exp2i(kTMin);
+    for (int c = lane; c < sh; c += 64) put_scale(&s[r * sh + c], kTMin);
   }
 }
 
@@ -368,17 +369,29 @@ hipError_t route_scratch(int32_t** out) {
   return hipSuccess;
 }
 
+template <typename S>
+static hipError_t permute_quant_impl(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                     const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                     int64_t M_cap, uint8_t* q, S* s, hipStream_t st) {
+  if (T > 0) {
+    if (row_w)
+      permute_quant_kernel<true, S><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
+    else
+      permute_quant_kernel<false, S><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
+  }
+  pad_fill_kernel<S><<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
+  return hipGetLastError();
+}
+
 hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                                 const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                 int64_t M_cap, uint8_t* q, float* s, hipStream_t st) {
-  if (T > 0) {
-    if (row_w)
-      permute_quant_kernel<true><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
-    else
-      permute_quant_kernel<false><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
-  }
-  pad_fill_kernel<<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
-  return hipGetLastError();
+  return permute_quant_impl(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st);
+}
+hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                int64_t M_cap, uint8_t* q, e8m0_t* s, hipStream_t st) {
+  return permute_quant_impl(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st);
 }
 
 hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
@@ -388,7 +401,7 @@ hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, i
   if (T > 0)
     permute_quant_dprobs_kernel<<<(unsigned)T, row_threads(H), 0, st>>>(dy, row_w, H, k, row_map, M_cap, q, s, y_perm,
                                                                        dprobs);
-  pad_fill_kernel<<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
+  pad_fill_kernel<float><<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
   return hipGetLastError();
 }
 

@@ -24,9 +24,9 @@ int grid_for(int64_t work_items, int per_block, int max_per_cu) {
   return (int)(need < cap ? need : cap);
 }
 
-template <int U>
+template <int U, typename S>
 __global__ __launch_bounds__(kThreads) void quant_rowwise_kernel(const uint16_t* __restrict__ x, int64_t n_chunks,
-                                                                 uint8_t* __restrict__ q, float* __restrict__ s) {
+                                                                 uint8_t* __restrict__ q, S* __restrict__ s) {
   const int64_t stride = (int64_t)gridDim.x * kThreads * U;
   for (int64_t c0 = (int64_t)blockIdx.x * kThreads * U + threadIdx.x; c0 < n_chunks; c0 += stride) {
     u32x4 w[U];
@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kThreads) void quant_rowwise_kernel(const uint16_t*
         int t;
         const u32x2 r = quant8_tile16(v, t);
         stnt8(q + c * 8, r);
-        if ((threadIdx.x & 15) == 0) s[c >> 4] = exp2i(t);
+        if ((threadIdx.x & 15) == 0) put_scale(&s[c >> 4], t);
       }
     }
   }
@@ -52,9 +52,10 @@ __global__ __launch_bounds__(kThreads) void quant_rowwise_kernel(const uint16_t*
 
 // One workgroup per 128x128 block: 16 lanes span a 128-column row segment, 16 rows per
 // pass, 8 passes.  Block maximum = wave DPP reduction + a 4-entry LDS reduction.
+template <typename S>
 __global__ __launch_bounds__(kThreads) void quant_block128_kernel(const uint16_t* __restrict__ w, int64_t cols,
                                                                   int64_t n_col_blocks, uint8_t* __restrict__ q,
-                                                                  float* __restrict__ s) {
+                                                                  S* __restrict__ s) {
   __shared__ uint32_t wave_max[kThreads / 64];
   const int64_t blk = blockIdx.x;
   const int64_t rb = blk / n_col_blocks, cb = blk - rb * n_col_blocks;
@@ -86,14 +87,15 @@ __global__ __launch_bounds__(kThreads) void quant_block128_kernel(const uint16_t
     r[1] = cvt_e4m3x4(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv);
     stnt8(q + base + (int64_t)i * 16 * cols, r);
   }
-  if (threadIdx.x == 0) s[blk] = exp2i(t);
+  if (threadIdx.x == 0) put_scale(&s[blk], t);
 }
 
 // Two horizontally adjacent 128x128 blocks per workgroup: 32 lanes span a 256-column row
 // segment (512 bytes per load instruction pair of rows), 8 rows per pass, 16 passes.
+template <typename S>
 __global__ __launch_bounds__(kThreads) void quant_block128x2_kernel(const uint16_t* __restrict__ w, int64_t cols,
                                                                     int64_t n_pairs, uint8_t* __restrict__ q,
-                                                                    float* __restrict__ s) {
+                                                                    S* __restrict__ s) {
   __shared__ uint32_t wave_max[kThreads / 64][2];
   const int64_t pr = blockIdx.x;
   const int64_t rb = pr / n_pairs, cp = pr - rb * n_pairs;
@@ -129,7 +131,7 @@ __global__ __launch_bounds__(kThreads) void quant_block128x2_kernel(const uint16
     r[1] = cvt_e4m3x4(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv);
     stnt8(q + base + (int64_t)i * 8 * cols, r);
   }
-  if (threadIdx.x == 0 || threadIdx.x == 16) s[rb * 2 * n_pairs + cp * 2 + h] = exp2i(t);
+  if (threadIdx.x == 0 || threadIdx.x == 16) put_scale(&s[rb * 2 * n_pairs + cp * 2 + h], t);
 }
 
 __device__ __forceinline__ float sat448(float f) { return fminf(fmaxf(f, -448.0f), 448.0f); }
@@ -181,13 +183,14 @@ __global__ __launch_bounds__(kThreads) void cast_e4m3_f32_kernel(const uint8_t* 
   }
 }
 
+template <typename S>
 __global__ __launch_bounds__(kThreads) void dequant_rowwise_kernel(const uint8_t* __restrict__ q,
-                                                                   const float* __restrict__ s, int64_t n_chunks,
+                                                                   const S* __restrict__ s, int64_t n_chunks,
                                                                    uint16_t* __restrict__ out) {
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < n_chunks; c += stride) {
     const u32x2 b = ldnt8(q + c * 8);
-    const float sc = s[c >> 4];
+    const float sc = scale_value(s[c >> 4]);
     u32x4 o;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -243,24 +246,45 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(const u32x4* __restrict_
 
 }  // namespace
 
-hipError_t launch_quant_rowwise(const uint16_t* x, int64_t rows, int64_t cols, uint8_t* q, float* s,
-                                hipStream_t st) {
+namespace {
+
+template <typename S>
+hipError_t quant_rowwise_impl(const uint16_t* x, int64_t rows, int64_t cols, uint8_t* q, S* s, hipStream_t st) {
   const int64_t n_chunks = rows * cols / 8;
   constexpr int U = 4;
   const int grid = grid_for(n_chunks, kThreads * U, kStreamBlocksPerCU);
-  quant_rowwise_kernel<U><<<grid, kThreads, 0, st>>>(x, n_chunks, q, s);
+  quant_rowwise_kernel<U, S><<<grid, kThreads, 0, st>>>(x, n_chunks, q, s);
   return hipGetLastError();
 }
 
-hipError_t launch_quant_block128(const uint16_t* w, int64_t rows, int64_t cols, uint8_t* q, float* s,
-                                 hipStream_t st) {
+template <typename S>
+hipError_t quant_block128_impl(const uint16_t* w, int64_t rows, int64_t cols, uint8_t* q, S* s, hipStream_t st) {
   const int64_t nbc = cols / kTile, blocks = rows / kTile * nbc;
   if (nbc % 2 == 0) {
-    quant_block128x2_kernel<<<(unsigned)(blocks / 2), kThreads, 0, st>>>(w, cols, nbc / 2, q, s);
+    quant_block128x2_kernel<S><<<(unsigned)(blocks / 2), kThreads, 0, st>>>(w, cols, nbc / 2, q, s);
     return hipGetLastError();
   }
-  quant_block128_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(w, cols, nbc, q, s);
+  quant_block128_kernel<S><<<(unsigned)blocks, kThreads, 0, st>>>(w, cols, nbc, q, s);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quant_rowwise(const uint16_t* x, int64_t rows, int64_t cols, uint8_t* q, float* s,
+                                hipStream_t st) {
+  return quant_rowwise_impl(x, rows, cols, q, s, st);
+}
+hipError_t launch_quant_rowwise(const uint16_t* x, int64_t rows, int64_t cols, uint8_t* q, e8m0_t* s,
+                                hipStream_t st) {
+  return quant_rowwise_impl(x, rows, cols, q, s, st);
+}
+hipError_t launch_quant_block128(const uint16_t* w, int64_t rows, int64_t cols, uint8_t* q, float* s,
+                                 hipStream_t st) {
+  return quant_block128_impl(w, rows, cols, q, s, st);
+}
+hipError_t launch_quant_block128(const uint16_t* w, int64_t rows, int64_t cols, uint8_t* q, e8m0_t* s,
+                                 hipStream_t st) {
+  return quant_block128_impl(w, rows, cols, q, s, st);
 }
 
 hipError_t launch_cast_f32_e4m3(const float* x, int64_t n, uint8_t* q, hipStream_t st) {
@@ -273,11 +297,20 @@ hipError_t launch_cast_e4m3_f32(const uint8_t* q, int64_t n, float* x, hipStream
   return hipGetLastError();
 }
 
+template <typename S>
+static hipError_t dequant_rowwise_impl(const uint8_t* q, const S* s, int64_t rows, int64_t cols, uint16_t* out,
+                                       hipStream_t st) {
+  const int64_t n_chunks = rows * cols / 8;
+  dequant_rowwise_kernel<S><<<grid_for(n_chunks, kThreads, 16), kThreads, 0, st>>>(q, s, n_chunks, out);
+  return hipGetLastError();
+}
 hipError_t launch_dequant_rowwise(const uint8_t* q, const float* s, int64_t rows, int64_t cols, uint16_t* out,
                                   hipStream_t st) {
-  const int64_t n_chunks = rows * cols / 8;
-  dequant_rowwise_kernel<<<grid_for(n_chunks, kThreads, 16), kThreads, 0, st>>>(q, s, n_chunks, out);
-  return hipGetLastError();
+  return dequant_rowwise_impl(q, s, rows, cols, out, st);
+}
+hipError_t launch_dequant_rowwise(const uint8_t* q, const e8m0_t* s, int64_t rows, int64_t cols, uint16_t* out,
+                                  hipStream_t st) {
+  return dequant_rowwise_impl(q, s, rows, cols, out, st);
 }
 
 hipError_t launch_transpose_bf16(const uint16_t* in, int64_t rows, int64_t cols, uint16_t* out, hipStream_t st) {

@@ -101,11 +101,11 @@ __device__ __forceinline__ void shift_transpose_store(uint32_t (&w0)[8], uint32_
 // k of block b of output row o sits at b*16 + (k ^ ((o >> 3) & 15)).  Rows of the input are
 // 8-byte units of the output; the swizzle keeps the sub-block writes and the row reads
 // conflict-free.
-template <int RB, bool kLoad16>
-__global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict__ q, const float* __restrict__ s,
+template <int RB, bool kLoad16, typename S>
+__global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict__ q, const S* __restrict__ s,
                                                        int64_t rows, int64_t cols, const int32_t* __restrict__ offsets,
                                                        int E, int n_rb_groups, int diagonal, uint8_t* __restrict__ qT,
-                                                       float* __restrict__ sT) {
+                                                       S* __restrict__ sT) {
   static_assert(!kLoad16 || RB % 2 == 0, "16-byte loads: half the workgroup per block");
   __shared__ u32x2 tile[128 * RB * 16];
   __shared__ int t_rows[RB][128];
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
     if (bi < RB) {
       int t_row = -256;
       if (bi < n_valid && (rb0 + bi) * kTile + r < m_rows)
-        t_row = (int)(__float_as_uint(s[((rb0 + bi) * kTile + r) * n_cb + cb]) >> 23) - 127;
+        t_row = scale_exp(s[((rb0 + bi) * kTile + r) * n_cb + cb]);
       t_rows[bi][r] = t_row;
       const uint32_t m = max64_u32((uint32_t)(t_row + 256));
       if ((tid & 63) == 0) wmax[bi][(tid >> 6) & 1] = m;
@@ -226,14 +226,15 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
   // column-wise scales: S_max of each block for the tile's 128 columns
   if (tid < 128) {
     for (int bi = 0; bi < n_valid; ++bi)
-      sT[(rb0 + bi) * cols + (int64_t)cb * kTile + tid] = exp2i((int)max(wmax[bi][0], wmax[bi][1]) - 256);
+      put_scale(&sT[(rb0 + bi) * cols + (int64_t)cb * kTile + tid], (int)max(wmax[bi][0], wmax[bi][1]) - 256);
   }
 }
 
 }  // namespace
 
-hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
-                      uint8_t* qT, float* sT, hipStream_t st) {
+template <typename S>
+static hipError_t sat_impl(const uint8_t* q, const S* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
+                           uint8_t* qT, S* sT, hipStream_t st) {
   const int64_t n_rb = rows / kTile;
   const int64_t n_cb = cols / kTile;
   // output row stride a multiple of 16 KB: one block per workgroup in the diagonal order;
@@ -241,14 +242,23 @@ hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t co
   const bool diagonal = rows % 16384 == 0;
   if (diagonal) {
     const int n_groups = (int)n_rb;
-    sat_kernel<1, false><<<(unsigned)(n_cb * n_groups), kThreads, 0, st>>>(q, s, rows, cols, offsets, E, n_groups, 1,
-                                                                           qT, sT);
+    sat_kernel<1, false, S><<<(unsigned)(n_cb * n_groups), kThreads, 0, st>>>(q, s, rows, cols, offsets, E, n_groups,
+                                                                              1, qT, sT);
   } else {
     const int n_groups = (int)((n_rb + 1) / 2);
-    sat_kernel<2, true><<<(unsigned)(n_cb * n_groups), kThreads, 0, st>>>(q, s, rows, cols, offsets, E, n_groups, 0,
-                                                                          qT, sT);
+    sat_kernel<2, true, S><<<(unsigned)(n_cb * n_groups), kThreads, 0, st>>>(q, s, rows, cols, offsets, E, n_groups, 0,
+                                                                             qT, sT);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
+                      uint8_t* qT, float* sT, hipStream_t st) {
+  return sat_impl(q, s, rows, cols, offsets, E, qT, sT, st);
+}
+hipError_t launch_sat(const uint8_t* q, const e8m0_t* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
+                      uint8_t* qT, e8m0_t* sT, hipStream_t st) {
+  return sat_impl(q, s, rows, cols, offsets, E, qT, sT, st);
 }
 
 }  // namespace ff8

@@ -37,12 +37,12 @@ __device__ __forceinline__ void dequant16(const u32x4& w, float s, float* v) {
 // lanes one 1x128 tile, one 16-byte store per lane; one item per thread, no grid-stride
 // loop.  (16 columns per lane measured faster than 8 here, and slower in the backward.)
 // kKeepA: also write A as 1x128 FP8 (aq [rows, 2I], as_ [rows, 2I/128]).
-template <bool kKeepA>
+template <bool kKeepA, typename S>
 __global__ __launch_bounds__(kThreads) void swiglu_quant_kernel(const uint16_t* __restrict__ a,
                                                                 const int32_t* __restrict__ offsets, int E,
                                                                 int64_t M_cap, int64_t I, uint8_t* __restrict__ hq,
-                                                                float* __restrict__ hs, uint8_t* __restrict__ aq,
-                                                                float* __restrict__ as_) {
+                                                                S* __restrict__ hs, uint8_t* __restrict__ aq,
+                                                                S* __restrict__ as_) {
   const int64_t rows = active_rows(offsets, E, M_cap);
   const int64_t cpr = I / 16, n_items = rows * cpr, sh = I / kTile;
   const int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kThreads) void swiglu_quant_kernel(const uint16_t* 
   int t;
   const u32x4 r = quant16_tile8(h, t);
   stnt16(hq + m * I + c * 16, r);
-  if ((threadIdx.x & 7) == 0) hs[m * sh + (c >> 3)] = exp2i(t);
+  if ((threadIdx.x & 7) == 0) put_scale(&hs[m * sh + (c >> 3)], t);
   if (kKeepA) {
     int tg, tu;
     const u32x4 rg = quant16_tile8(g, tg);
@@ -68,19 +68,20 @@ __global__ __launch_bounds__(kThreads) void swiglu_quant_kernel(const uint16_t* 
     stnt16(aq + m * 2 * I + c * 16, rg);
     stnt16(aq + m * 2 * I + I + c * 16, ru);
     if ((threadIdx.x & 7) == 0) {
-      as_[m * 2 * sh + (c >> 3)] = exp2i(tg);
-      as_[m * 2 * sh + sh + (c >> 3)] = exp2i(tu);
+      put_scale(&as_[m * 2 * sh + (c >> 3)], tg);
+      put_scale(&as_[m * 2 * sh + sh + (c >> 3)], tu);
     }
   }
 }
 
 // Backward: the same layout, three 16-byte loads per lane.
+template <typename S>
 __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_kernel(const uint16_t* __restrict__ a,
                                                                     const uint16_t* __restrict__ dh,
                                                                     const int32_t* __restrict__ offsets, int E,
                                                                     int64_t M_cap, int64_t I,
                                                                     uint8_t* __restrict__ daq,
-                                                                    float* __restrict__ das) {
+                                                                    S* __restrict__ das) {
   const int64_t rows = active_rows(offsets, E, M_cap);
   const int64_t cpr = I / 8, n_items = rows * cpr, sh = 2 * I / kTile;
   const int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -105,32 +106,33 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_kernel(const uint16
   stnt8(out, rg);
   stnt8(out + I, ru);
   if ((threadIdx.x & 15) == 0) {
-    das[m * sh + (c >> 4)] = exp2i(tg);
-    das[m * sh + I / kTile + (c >> 4)] = exp2i(tu);
+    put_scale(&das[m * sh + (c >> 4)], tg);
+    put_scale(&das[m * sh + I / kTile + (c >> 4)], tu);
   }
 }
 
 // Backward from the FP8 checkpoint of A: lane c covers 16 columns (16-byte loads of the
 // gate and up codes, two of dH), 8 lanes one 1x128 tile of each half of the output.
+template <typename S>
 __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_fp8a_kernel(const uint8_t* __restrict__ aq,
-                                                                         const float* __restrict__ as_,
+                                                                         const S* __restrict__ as_,
                                                                          const uint16_t* __restrict__ dh,
                                                                          const int32_t* __restrict__ offsets, int E,
                                                                          int64_t M_cap, int64_t I,
                                                                          uint8_t* __restrict__ daq,
-                                                                         float* __restrict__ das) {
+                                                                         S* __restrict__ das) {
   const int64_t rows = active_rows(offsets, E, M_cap);
   const int64_t cpr = I / 16, n_items = rows * cpr, sh = 2 * I / kTile;
   const int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (it >= n_items) return;  // whole 8-lane tiles (cpr is a multiple of 8)
   const int64_t m = it / cpr, c = it - m * cpr;
   const uint8_t* row = aq + m * 2 * I + c * 16;
-  const float* srow = as_ + m * sh;  // gate tiles, then up tiles
+  const S* srow = as_ + m * sh;  // gate tiles, then up tiles
   const u32x4 qg = ldnt16(row), qu = ldnt16(row + I);
   const u32x4 d0 = ldnt16(dh + m * I + c * 16), d1 = ldnt16(dh + m * I + c * 16 + 8);
   float g[16], u[16], d[16], dg[16], du[16];
-  dequant16(qg, srow[c >> 3], g);
-  dequant16(qu, srow[I / kTile + (c >> 3)], u);
+  dequant16(qg, scale_value(srow[c >> 3]), g);
+  dequant16(qu, scale_value(srow[I / kTile + (c >> 3)]), u);
   unpack_bf16x8(d0, d);
   unpack_bf16x8(d1, d + 8);
 #pragma unroll
@@ -147,8 +149,8 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_quant_fp8a_kernel(const u
   stnt16(out, rg);
   stnt16(out + I, ru);
   if ((threadIdx.x & 7) == 0) {
-    das[m * sh + (c >> 3)] = exp2i(tg);
-    das[m * sh + I / kTile + (c >> 3)] = exp2i(tu);
+    put_scale(&das[m * sh + (c >> 3)], tg);
+    put_scale(&das[m * sh + I / kTile + (c >> 3)], tu);
   }
 }
 
@@ -183,36 +185,70 @@ int grid_for(int64_t items) {
 
 }  // namespace
 
+namespace {
+
+unsigned blocks_of(int64_t items) { return (unsigned)((items + kThreads - 1) / kThreads); }
+
+template <typename S>
+hipError_t swiglu_quant_impl(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I, uint8_t* hq,
+                             S* hs, uint8_t* aq, S* as_, hipStream_t st) {
+  const unsigned grid = blocks_of(M_cap * (I / 16));
+  if (aq)
+    swiglu_quant_kernel<true, S><<<grid, kThreads, 0, st>>>(a, offsets, E, M_cap, I, hq, hs, aq, as_);
+  else
+    swiglu_quant_kernel<false, S><<<grid, kThreads, 0, st>>>(a, offsets, E, M_cap, I, hq, hs, nullptr, nullptr);
+  return hipGetLastError();
+}
+
+template <typename S>
+hipError_t swiglu_bwd_quant_impl(const uint16_t* a, const uint16_t* dh, const int32_t* offsets, int E, int64_t M_cap,
+                                 int64_t I, uint8_t* daq, S* das, hipStream_t st) {
+  swiglu_bwd_quant_kernel<S><<<blocks_of(M_cap * (I / 8)), kThreads, 0, st>>>(a, dh, offsets, E, M_cap, I, daq, das);
+  return hipGetLastError();
+}
+
+template <typename S>
+hipError_t swiglu_bwd_quant_fp8a_impl(const uint8_t* aq, const S* as_, const uint16_t* dh, const int32_t* offsets,
+                                      int E, int64_t M_cap, int64_t I, uint8_t* daq, S* das, hipStream_t st) {
+  swiglu_bwd_quant_fp8a_kernel<S><<<blocks_of(M_cap * (I / 16)), kThreads, 0, st>>>(aq, as_, dh, offsets, E, M_cap, I,
+                                                                                    daq, das);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_swiglu_quant(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
                                uint8_t* hq, float* hs, hipStream_t st) {
-  const int64_t items = M_cap * (I / 16);
-  swiglu_quant_kernel<false><<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(
-      a, offsets, E, M_cap, I, hq, hs, nullptr, nullptr);
-  return hipGetLastError();
+  return swiglu_quant_impl<float>(a, offsets, E, M_cap, I, hq, hs, nullptr, nullptr, st);
 }
-
+hipError_t launch_swiglu_quant(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                               uint8_t* hq, e8m0_t* hs, hipStream_t st) {
+  return swiglu_quant_impl<e8m0_t>(a, offsets, E, M_cap, I, hq, hs, nullptr, nullptr, st);
+}
 hipError_t launch_swiglu_quant_keep_fp8(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
                                         uint8_t* hq, float* hs, uint8_t* aq, float* as_, hipStream_t st) {
-  const int64_t items = M_cap * (I / 16);
-  swiglu_quant_kernel<true><<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(
-      a, offsets, E, M_cap, I, hq, hs, aq, as_);
-  return hipGetLastError();
+  return swiglu_quant_impl(a, offsets, E, M_cap, I, hq, hs, aq, as_, st);
 }
-
+hipError_t launch_swiglu_quant_keep_fp8(const uint16_t* a, const int32_t* offsets, int E, int64_t M_cap, int64_t I,
+                                        uint8_t* hq, e8m0_t* hs, uint8_t* aq, e8m0_t* as_, hipStream_t st) {
+  return swiglu_quant_impl(a, offsets, E, M_cap, I, hq, hs, aq, as_, st);
+}
 hipError_t launch_swiglu_bwd_quant(const uint16_t* a, const uint16_t* dh, const int32_t* offsets, int E,
                                    int64_t M_cap, int64_t I, uint8_t* daq, float* das, hipStream_t st) {
-  const int64_t items = M_cap * (I / 8);
-  swiglu_bwd_quant_kernel<<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(a, dh, offsets, E, M_cap,
-                                                                                             I, daq, das);
-  return hipGetLastError();
+  return swiglu_bwd_quant_impl(a, dh, offsets, E, M_cap, I, daq, das, st);
 }
-
+hipError_t launch_swiglu_bwd_quant(const uint16_t* a, const uint16_t* dh, const int32_t* offsets, int E,
+                                   int64_t M_cap, int64_t I, uint8_t* daq, e8m0_t* das, hipStream_t st) {
+  return swiglu_bwd_quant_impl(a, dh, offsets, E, M_cap, I, daq, das, st);
+}
 hipError_t launch_swiglu_bwd_quant_fp8a(const uint8_t* aq, const float* as_, const uint16_t* dh, const int32_t* offsets,
                                         int E, int64_t M_cap, int64_t I, uint8_t* daq, float* das, hipStream_t st) {
-  const int64_t items = M_cap * (I / 16);
-  swiglu_bwd_quant_fp8a_kernel<<<(unsigned)((items + kThreads - 1) / kThreads), kThreads, 0, st>>>(
-      aq, as_, dh, offsets, E, M_cap, I, daq, das);
-  return hipGetLastError();
+  return swiglu_bwd_quant_fp8a_impl(aq, as_, dh, offsets, E, M_cap, I, daq, das, st);
+}
+hipError_t launch_swiglu_bwd_quant_fp8a(const uint8_t* aq, const e8m0_t* as_, const uint16_t* dh,
+                                        const int32_t* offsets, int E, int64_t M_cap, int64_t I, uint8_t* daq,
+                                        e8m0_t* das, hipStream_t st) {
+  return swiglu_bwd_quant_fp8a_impl(aq, as_, dh, offsets, E, M_cap, I, daq, das, st);
 }
 
 hipError_t launch_swiglu_bf16(const uint16_t* a, const int32_t* offsets, int E, int64_t rows, int64_t I,

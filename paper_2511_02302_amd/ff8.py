@@ -53,6 +53,23 @@ _SIGNATURES = {
     "ff8_swiglu_bwd_quant_fp8a": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp,
                                            _c_vp]),
     "ff8_unpermute": (_c_int, [_c_vp, _c_vp, _c_vp, _c_i64, _c_int, _c_i64, _c_i64, _c_vp, _c_vp]),
+    "ff8_quant_rowwise_e8m0": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_quant_block128_e8m0": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_permute_quant_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp, _c_vp,
+                                        _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_int, _c_vp]),
+    "ff8_scaling_aware_transpose_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
+    "ff8_grouped_gemm_fprop_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64,
+                                             _c_vp, _c_vp]),
+    "ff8_grouped_gemm_dgrad_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64,
+                                             _c_vp, _c_vp]),
+    "ff8_grouped_gemm_wgrad_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64,
+                                             _c_vp, _c_int, _c_vp]),
+    "ff8_swiglu_quant_e8m0": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_swiglu_bwd_quant_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
+    "ff8_swiglu_quant_keep_fp8_e8m0": (_c_int, [_c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp, _c_vp,
+                                                _c_vp]),
+    "ff8_swiglu_bwd_quant_fp8a_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_vp, _c_vp,
+                                                _c_vp]),
     "ff8_cast_f32_to_e4m3": (_c_int, [_c_vp, _c_i64, _c_vp, _c_vp]),
     "ff8_cast_e4m3_to_f32": (_c_int, [_c_vp, _c_i64, _c_vp, _c_vp]),
     "ff8_baseline_dequant_rowwise": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_vp]),
@@ -130,6 +147,17 @@ def _numel(t, n, name):
 _bf16, _u8, _f32, _i32 = torch.bfloat16, torch.uint8, torch.float32, torch.int32
 
 
+def _scale_kind(*scales):
+    """Scale storage of a call: float32 tensors (powers of two) or uint8 tensors (UE8M0 bytes,
+    T + 127), the same for every scale tensor of the call.  Returns (dtype, C-symbol suffix)."""
+    kinds = {t.dtype for t in scales if t is not None}
+    if kinds == {_f32}:
+        return _f32, ""
+    if kinds == {_u8}:
+        return _u8, "_e8m0"
+    raise TypeError(f"scale tensors must all be float32 or all uint8 (UE8M0), got {sorted(map(str, kinds))}")
+
+
 def ff8_version():
     return load().ff8_version()
 
@@ -149,32 +177,39 @@ def ff8_permute_workspace_bytes(T, k, E):
 def ff8_quant_rowwise(x, q, s, stream=None):
     rows, cols = x.shape
     _shape(q, (rows, cols), "q"); _shape(s, (rows, cols // 128), "s")
-    _check(load().ff8_quant_rowwise(_ptr(x, _bf16, "x", 2), rows, cols, _ptr(q, _u8, "q"), _ptr(s, _f32, "s"),
-                                    _stream(stream)), "ff8_quant_rowwise")
+    sd, sfx = _scale_kind(s)
+    name = "ff8_quant_rowwise" + sfx
+    _check(getattr(load(), name)(_ptr(x, _bf16, "x", 2), rows, cols, _ptr(q, _u8, "q"), _ptr(s, sd, "s"),
+                                 _stream(stream)), name)
 
 
 def ff8_quant_block128(w, q, s, stream=None):
     rows, cols = w.reshape(-1, w.shape[-1]).shape
     _shape(q, w.shape, "q"); _numel(s, (rows // 128) * (cols // 128), "s")
-    _check(load().ff8_quant_block128(_ptr(w, _bf16, "w"), rows, cols, _ptr(q, _u8, "q"), _ptr(s, _f32, "s"),
-                                     _stream(stream)), "ff8_quant_block128")
+    sd, sfx = _scale_kind(s)
+    name = "ff8_quant_block128" + sfx
+    _check(getattr(load(), name)(_ptr(w, _bf16, "w"), rows, cols, _ptr(q, _u8, "q"), _ptr(s, sd, "s"),
+                                 _stream(stream)), name)
 
 
 def ff8_permute_quant(x, row_w, k, E, topk_idx, reuse_map, row_map, offsets, src_row, q, s, workspace=None,
                       stream=None, align=None):
     """align None calls ff8_permute_quant (groups padded to 128 rows); 16/32/64/128 calls
-    ff8_permute_quant_aligned."""
+    ff8_permute_quant_aligned; a uint8 (UE8M0) scale tensor calls ff8_permute_quant_e8m0."""
     T, H = x.shape
     M_cap = q.shape[0]
     _numel(row_w, T * k, "row_w"); _numel(topk_idx, T * k, "topk_idx"); _numel(row_map, T * k, "row_map")
     _numel(offsets, E + 1, "offsets"); _numel(src_row, M_cap, "src_row")
     _shape(q, (M_cap, H), "q"); _shape(s, (M_cap, H // 128), "s")
     ws = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    sd, sfx = _scale_kind(s)
     args = [_ptr(x, _bf16, "x", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E, _ptr(topk_idx, _i32, "topk_idx"),
             int(reuse_map), _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
-            _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2),
+            _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, sd, "s", 2),
             None if workspace is None else ctypes.c_void_p(workspace.data_ptr()), ws]
-    if align is None:
+    if sfx:
+        _check(load().ff8_permute_quant_e8m0(*args, int(align or 128), _stream(stream)), "ff8_permute_quant_e8m0")
+    elif align is None:
         _check(load().ff8_permute_quant(*args, _stream(stream)), "ff8_permute_quant")
     else:
         _check(load().ff8_permute_quant_aligned(*args, int(align), _stream(stream)), "ff8_permute_quant_aligned")
@@ -212,9 +247,11 @@ def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):
     _shape(s, (rows, cols // 128), "s"); _shape(qT, (cols, rows), "qT"); _shape(sT, (rows // 128, cols), "sT")
     if offsets is not None:
         _numel(offsets, E + 1, "offsets")
-    _check(load().ff8_scaling_aware_transpose(
-        _ptr(q, _u8, "q", 2), _ptr(s, _f32, "s", 2), rows, cols, _ptr(offsets, _i32, "offsets"), E,
-        _ptr(qT, _u8, "qT", 2), _ptr(sT, _f32, "sT", 2), _stream(stream)), "ff8_scaling_aware_transpose")
+    sd, sfx = _scale_kind(s, sT)
+    name = "ff8_scaling_aware_transpose" + sfx
+    _check(getattr(load(), name)(
+        _ptr(q, _u8, "q", 2), _ptr(s, sd, "s", 2), rows, cols, _ptr(offsets, _i32, "offsets"), E,
+        _ptr(qT, _u8, "qT", 2), _ptr(sT, sd, "sT", 2), _stream(stream)), name)
 
 
 def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):
@@ -222,10 +259,11 @@ def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):
     E, N, _ = w.shape
     _shape(a_s, (M_cap, K // 128), "a_s"); _shape(w, (E, N, K), "w"); _numel(w_s, E * (N // 128) * (K // 128), "w_s")
     _numel(offsets, E + 1, "offsets"); _shape(out, (M_cap, N), "out")
-    _check(load().ff8_grouped_gemm_fprop(
-        _ptr(a, _u8, "a", 2), _ptr(a_s, _f32, "a_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, _f32, "w_s"),
-        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)),
-        "ff8_grouped_gemm_fprop")
+    sd, sfx = _scale_kind(a_s, w_s)
+    name = "ff8_grouped_gemm_fprop" + sfx
+    _check(getattr(load(), name)(
+        _ptr(a, _u8, "a", 2), _ptr(a_s, sd, "a_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, sd, "w_s"),
+        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)), name)
 
 
 def ff8_grouped_gemm_dgrad(g, g_s, w, w_s, offsets, out, stream=None):
@@ -233,10 +271,11 @@ def ff8_grouped_gemm_dgrad(g, g_s, w, w_s, offsets, out, stream=None):
     E, _, K = w.shape
     _shape(g_s, (M_cap, N // 128), "g_s"); _shape(w, (E, N, K), "w"); _numel(w_s, E * (N // 128) * (K // 128), "w_s")
     _numel(offsets, E + 1, "offsets"); _shape(out, (M_cap, K), "out")
-    _check(load().ff8_grouped_gemm_dgrad(
-        _ptr(g, _u8, "g", 2), _ptr(g_s, _f32, "g_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, _f32, "w_s"),
-        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)),
-        "ff8_grouped_gemm_dgrad")
+    sd, sfx = _scale_kind(g_s, w_s)
+    name = "ff8_grouped_gemm_dgrad" + sfx
+    _check(getattr(load(), name)(
+        _ptr(g, _u8, "g", 2), _ptr(g_s, sd, "g_s"), _ptr(w, _u8, "w", 3), _ptr(w_s, sd, "w_s"),
+        _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(out, _bf16, "out", 2), _stream(stream)), name)
 
 
 def ff8_grouped_gemm_wgrad(gT, gT_s, xT, xT_s, offsets, dw, accumulate=False, stream=None):
@@ -245,10 +284,12 @@ def ff8_grouped_gemm_wgrad(gT, gT_s, xT, xT_s, offsets, dw, accumulate=False, st
     E = dw.shape[0]
     _shape(gT_s, (M_cap // 128, N), "gT_s"); _shape(xT, (K, M_cap), "xT"); _shape(xT_s, (M_cap // 128, K), "xT_s")
     _numel(offsets, E + 1, "offsets"); _shape(dw, (E, N, K), "dw")
-    _check(load().ff8_grouped_gemm_wgrad(
-        _ptr(gT, _u8, "gT", 2), _ptr(gT_s, _f32, "gT_s"), _ptr(xT, _u8, "xT", 2), _ptr(xT_s, _f32, "xT_s"),
+    sd, sfx = _scale_kind(gT_s, xT_s)
+    name = "ff8_grouped_gemm_wgrad" + sfx
+    _check(getattr(load(), name)(
+        _ptr(gT, _u8, "gT", 2), _ptr(gT_s, sd, "gT_s"), _ptr(xT, _u8, "xT", 2), _ptr(xT_s, sd, "xT_s"),
         _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(dw, _f32, "dw", 3), int(bool(accumulate)),
-        _stream(stream)), "ff8_grouped_gemm_wgrad")
+        _stream(stream)), name)
 
 
 def ff8_swiglu_quant(a, hq, hs, offsets=None, E=0, stream=None):
@@ -256,9 +297,10 @@ def ff8_swiglu_quant(a, hq, hs, offsets=None, E=0, stream=None):
     _shape(hq, (M_cap, I2 // 2), "hq"); _shape(hs, (M_cap, I2 // 256), "hs")
     if offsets is not None:
         _numel(offsets, E + 1, "offsets")
-    _check(load().ff8_swiglu_quant(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
-                                   _ptr(hq, _u8, "hq", 2), _ptr(hs, _f32, "hs", 2), _stream(stream)),
-           "ff8_swiglu_quant")
+    sd, sfx = _scale_kind(hs)
+    name = "ff8_swiglu_quant" + sfx
+    _check(getattr(load(), name)(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
+                                 _ptr(hq, _u8, "hq", 2), _ptr(hs, sd, "hs", 2), _stream(stream)), name)
 
 
 def ff8_swiglu_bwd_quant(a, dh, daq, das, offsets=None, E=0, stream=None):
@@ -266,9 +308,11 @@ def ff8_swiglu_bwd_quant(a, dh, daq, das, offsets=None, E=0, stream=None):
     _shape(dh, (M_cap, I2 // 2), "dh"); _shape(daq, (M_cap, I2), "daq"); _shape(das, (M_cap, I2 // 128), "das")
     if offsets is not None:
         _numel(offsets, E + 1, "offsets")
-    _check(load().ff8_swiglu_bwd_quant(_ptr(a, _bf16, "a", 2), _ptr(dh, _bf16, "dh", 2),
-                                       _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2, _ptr(daq, _u8, "daq", 2),
-                                       _ptr(das, _f32, "das", 2), _stream(stream)), "ff8_swiglu_bwd_quant")
+    sd, sfx = _scale_kind(das)
+    name = "ff8_swiglu_bwd_quant" + sfx
+    _check(getattr(load(), name)(_ptr(a, _bf16, "a", 2), _ptr(dh, _bf16, "dh", 2),
+                                 _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2, _ptr(daq, _u8, "daq", 2),
+                                 _ptr(das, sd, "das", 2), _stream(stream)), name)
 
 
 def ff8_swiglu_quant_keep_fp8(a, hq, hs, a_q, a_s, offsets=None, E=0, stream=None):
@@ -277,9 +321,11 @@ def ff8_swiglu_quant_keep_fp8(a, hq, hs, a_q, a_s, offsets=None, E=0, stream=Non
     _shape(a_q, (M_cap, I2), "a_q"); _shape(a_s, (M_cap, I2 // 128), "a_s")
     if offsets is not None:
         _numel(offsets, E + 1, "offsets")
-    _check(load().ff8_swiglu_quant_keep_fp8(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
-                                            _ptr(hq, _u8, "hq", 2), _ptr(hs, _f32, "hs", 2), _ptr(a_q, _u8, "a_q", 2),
-                                            _ptr(a_s, _f32, "a_s", 2), _stream(stream)), "ff8_swiglu_quant_keep_fp8")
+    sd, sfx = _scale_kind(hs, a_s)
+    name = "ff8_swiglu_quant_keep_fp8" + sfx
+    _check(getattr(load(), name)(_ptr(a, _bf16, "a", 2), _ptr(offsets, _i32, "offsets"), E, M_cap, I2 // 2,
+                                 _ptr(hq, _u8, "hq", 2), _ptr(hs, sd, "hs", 2), _ptr(a_q, _u8, "a_q", 2),
+                                 _ptr(a_s, sd, "a_s", 2), _stream(stream)), name)
 
 
 def ff8_swiglu_bwd_quant_fp8a(a_q, a_s, dh, daq, das, offsets=None, E=0, stream=None):
@@ -288,10 +334,12 @@ def ff8_swiglu_bwd_quant_fp8a(a_q, a_s, dh, daq, das, offsets=None, E=0, stream=
     _shape(daq, (M_cap, I2), "daq"); _shape(das, (M_cap, I2 // 128), "das")
     if offsets is not None:
         _numel(offsets, E + 1, "offsets")
-    _check(load().ff8_swiglu_bwd_quant_fp8a(_ptr(a_q, _u8, "a_q", 2), _ptr(a_s, _f32, "a_s", 2),
-                                            _ptr(dh, _bf16, "dh", 2), _ptr(offsets, _i32, "offsets"), E, M_cap,
-                                            I2 // 2, _ptr(daq, _u8, "daq", 2), _ptr(das, _f32, "das", 2),
-                                            _stream(stream)), "ff8_swiglu_bwd_quant_fp8a")
+    sd, sfx = _scale_kind(a_s, das)
+    name = "ff8_swiglu_bwd_quant_fp8a" + sfx
+    _check(getattr(load(), name)(_ptr(a_q, _u8, "a_q", 2), _ptr(a_s, sd, "a_s", 2),
+                                 _ptr(dh, _bf16, "dh", 2), _ptr(offsets, _i32, "offsets"), E, M_cap,
+                                 I2 // 2, _ptr(daq, _u8, "daq", 2), _ptr(das, sd, "das", 2),
+                                 _stream(stream)), name)
 
 
 def ff8_unpermute(y_perm, row_map, row_w, y, stream=None):

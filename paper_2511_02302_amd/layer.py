@@ -33,6 +33,11 @@ combine), in the same pass over dY; Y_perm is then saved for the backward.
 
 align=16 pads the expert groups to 16 rows, the paper's padding (section 3.3.1), instead
 of 128.
+
+scale_fmt="e8m0" stores every scale tensor as UE8M0 bytes (T + 127 for the scale 2^T; the
+format section 2.1 names) instead of float32: a quarter of the scale bytes, and bit-identical
+FP8 tensors and outputs.  It needs H and I to be multiples of 512 and is not combined with the
+router gradient.
 """
 
 from dataclasses import dataclass
@@ -62,6 +67,7 @@ class Dims:
 
 
 _u8, _f32, _bf16, _i32 = torch.uint8, torch.float32, torch.bfloat16, torch.int32
+SCALE_DTYPES = {"f32": torch.float32, "e8m0": torch.uint8}
 
 
 def _alloc(spec, device):
@@ -78,25 +84,26 @@ class Workspace:
     passes run one at a time on one stream (a layer's pass leaves nothing in it that a
     later pass reads)."""
 
-    def __init__(self, dims, device="cuda", fp8_checkpoint=False, router_grad=False):
+    def __init__(self, dims, device="cuda", fp8_checkpoint=False, router_grad=False, scale_fmt="f32"):
         self.d = d = dims
-        self.fp8_checkpoint, self.router_grad = fp8_checkpoint, router_grad
+        self.fp8_checkpoint, self.router_grad, self.scale_fmt = fp8_checkpoint, router_grad, scale_fmt
         self.device = torch.device(device)
         M, H, I, T, k, E = d.m_cap, d.H, d.I, d.T, d.k, d.E
+        sdt = SCALE_DTYPES[scale_fmt]
         spec = {"ws": ((max(1, ff8.ff8_permute_workspace_bytes(T, k, E)),), _u8)}
         if fp8_checkpoint:
             spec["a"] = ((M, 2 * I), _bf16)      # fc1 output, consumed by the activation only
         if not router_grad:
             spec["y_perm"] = ((M, H), _bf16)     # fc2 output, consumed by the combine only
         spec.update({
-            "dyq": ((M, H), _u8), "dys": ((M, H // 128), _f32),
+            "dyq": ((M, H), _u8), "dys": ((M, H // 128), sdt),
             "dh": ((M, I), _bf16),
-            "daq": ((M, 2 * I), _u8), "das": ((M, 2 * I // 128), _f32),
+            "daq": ((M, 2 * I), _u8), "das": ((M, 2 * I // 128), sdt),
             "dx_perm": ((M, H), _bf16),
         })
         for name, cols in (("x", H), ("h", I), ("dy", H), ("da", 2 * I)):
             spec[name + "Tq"] = ((cols, M), _u8)
-            spec[name + "Ts"] = ((M // 128, cols), _f32)  # block-major column scales
+            spec[name + "Ts"] = ((M // 128, cols), sdt)  # block-major column scales
         self.buf = _alloc(spec, self.device)
 
     def nbytes(self):
@@ -107,21 +114,27 @@ class ExpertLayerFP8:
     """Buffers and step sequence of one expert layer (E local experts, top-k routing)."""
 
     def __init__(self, T, H, E, k, I, device="cuda", fp8_checkpoint=False, router_grad=False, align=128,
-                 workspace=None):
+                 workspace=None, scale_fmt="f32"):
         self.d = d = Dims(T, H, E, k, I, align)
         self.fp8_checkpoint = fp8_checkpoint
         self.router_grad = router_grad
+        if scale_fmt not in SCALE_DTYPES:
+            raise ValueError(f"scale_fmt must be one of {sorted(SCALE_DTYPES)}")
+        if scale_fmt == "e8m0" and (H % 512 or I % 512 or router_grad):
+            raise ValueError("UE8M0 scales need H and I multiples of 512, without the router gradient")
+        self.scale_fmt = scale_fmt
+        sdt = SCALE_DTYPES[scale_fmt]
         self.device = dev = torch.device(device)
         self.M_cap = M = d.m_cap
         if workspace is None:
-            workspace = Workspace(d, dev, fp8_checkpoint, router_grad)
+            workspace = Workspace(d, dev, fp8_checkpoint, router_grad, scale_fmt)
         elif (workspace.d != d or workspace.fp8_checkpoint != fp8_checkpoint
-              or workspace.router_grad != router_grad):
+              or workspace.router_grad != router_grad or workspace.scale_fmt != scale_fmt):
             raise ValueError("the shared workspace was made for other dimensions or options")
         self.ws = workspace
         spec = {
-            "w1q": ((E, 2 * I, H), _u8), "w1s": ((E, 2 * I // 128, H // 128), _f32),
-            "w2q": ((E, H, I), _u8), "w2s": ((E, H // 128, I // 128), _f32),
+            "w1q": ((E, 2 * I, H), _u8), "w1s": ((E, 2 * I // 128, H // 128), sdt),
+            "w2q": ((E, H, I), _u8), "w2s": ((E, H // 128, I // 128), sdt),
             "y": ((T, H), _bf16), "dx": ((T, H), _bf16),
             "dw1": ((E, 2 * I, H), _f32), "dw2": ((E, H, I), _f32),
         }
@@ -131,11 +144,11 @@ class ExpertLayerFP8:
         self.saved = None
         saved = {
             "row_map": ((T, k), _i32), "offsets": ((E + 1,), _i32), "src_row": ((M,), _i32),
-            "xq": ((M, H), _u8), "xs": ((M, H // 128), _f32),
-            "hq": ((M, I), _u8), "hs": ((M, I // 128), _f32),
+            "xq": ((M, H), _u8), "xs": ((M, H // 128), sdt),
+            "hq": ((M, I), _u8), "hs": ((M, I // 128), sdt),
         }
         if fp8_checkpoint:
-            saved.update({"aq": ((M, 2 * I), _u8), "as": ((M, 2 * I // 128), _f32)})
+            saved.update({"aq": ((M, 2 * I), _u8), "as": ((M, 2 * I // 128), sdt)})
         else:
             saved["a"] = ((M, 2 * I), _bf16)
         if router_grad:

@@ -6,6 +6,8 @@ per-element rounding bound of e4m3, the idempotence argument of section 3.1
 e4m3 cast for the element encoding.
 """
 
+import math
+
 import numpy as np
 import torch
 
@@ -118,3 +120,28 @@ def test_block128_brute_force():
                 assert q[bi * 128 + i, bj * 128 + j] == c
     d = dequant_block128(q, s)
     assert np.max(np.abs(d - w) / np.repeat(np.repeat(s, 128, 0), 128, 1)) <= 16.0  # half ulp at 448 is 16
+
+
+def test_e8m0_scale_bytes():
+    """UE8M0 storage of the power-of-two scales: for every T in [-126, 127] the byte is T + 127,
+    which is the exponent field of the float32 scale (IEEE 754 binary32, bias 127), and the byte
+    decodes back to exactly 2^T; the scales a quantizer produces are always bytes 1..254 (never
+    0, and never 255, the format's NaN)."""
+    from oracle.quant import scale_to_e8m0, e8m0_to_scale, quant_rowwise
+
+    T = np.arange(-126, 128)
+    s = np.array([2.0 ** int(t) for t in T], dtype=np.float32)  # exact powers of two
+    b = scale_to_e8m0(s)
+    assert b.dtype == np.uint8 and np.array_equal(b.astype(np.int64), T + 127)
+    assert np.array_equal(b.astype(np.uint32), s.view(np.uint32) >> 23)      # the exponent field
+    assert np.array_equal(s.view(np.uint32) & 0x7FFFFF, np.zeros_like(T))    # no mantissa bits
+    assert np.array_equal(e8m0_to_scale(b), s)
+    for t, v in zip(T, e8m0_to_scale(b)):
+        assert float(v) == math.ldexp(1.0, int(t))
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((64, 512)) * np.exp2(rng.integers(-120, 120, size=(64, 1)))
+    x[0] = 0.0  # all-zero tiles: T = -126, byte 1
+    _, sx = quant_rowwise(x)
+    bx = scale_to_e8m0(sx)
+    assert bx.min() >= 1 and bx.max() <= 254 and np.all(bx[0] == 1)
+    assert np.array_equal(e8m0_to_scale(bx), sx)
