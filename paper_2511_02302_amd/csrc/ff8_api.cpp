@@ -180,9 +180,9 @@ int ff8_permute_quant_noalloc(const ff8_bf16* x, const float* row_w, int64_t T, 
   if (!reuse_map && need > (size_t)ff8::kRouteScratchInts * sizeof(int32_t))
     return fail(FF8_ERR_ARG,
                 "%s: the routing of T = %lld tokens over E = %d experts needs %zu bytes of workspace, more than the "
-                "%lld bytes the library holds (ceil(T / 256) * E must not exceed %lld); use ff8_permute_quant_aligned "
+                "%lld bytes the library holds (ceil(T / %d) * E must not exceed %lld); use ff8_permute_quant_aligned "
                 "with a caller-owned workspace",
-                __func__, (long long)T, E, need, (long long)(ff8::kRouteScratchInts * 4),
+                __func__, (long long)T, E, need, (long long)(ff8::kRouteScratchInts * 4), ff8::kRouteChunk,
                 (long long)ff8::kRouteScratchInts);
   int32_t* ws = nullptr;
   if (!reuse_map) {

@@ -32,6 +32,7 @@ hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t co
 hipError_t launch_sat(const uint8_t* q, const e8m0_t* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
                       uint8_t* qT, e8m0_t* sT, hipStream_t st);
 
+constexpr int kRouteChunk = 256;  // tokens per routing chunk: the workspace holds ceil(T / 256) x E counts
 size_t permute_workspace_bytes(int64_t T, int k, int E);
 // Capacity (int32 entries) of the routing workspace the library keeps in device memory for the
 // no-allocation entry point, and its device address on the current device (looked up once per

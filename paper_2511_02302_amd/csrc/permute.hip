@@ -11,11 +11,13 @@
 //                  offsets[E+1] and marks the padding rows' src_row = -1;
 //   route_assign : one wave per chunk walks its tokens 64 at a time; a 64-bit LDS
 //                  ballot mask per expert gives each pair its rank among earlier lanes.
+// (64-token chunks, four times the workgroups, measured the same: the three routing launches
+// take about 26 us at the DeepSeek-V3 share whatever the chunk.)
 // Then permute_quant reads each token row ONCE (one workgroup per token, 16 elements per
 // lane, 8 lanes per 1x128 tile, DPP amax), quantizes it and writes it to each of its k
 // rows; with routing weights each copy is scaled (float32 product) and quantized
-// separately.  pad_fill writes the padding rows.  unpermute gathers a token's k rows the
-// same way and sums them in slot order.
+// separately.  E more workgroups of the same launch write the padding rows, one expert
+// group each.  unpermute gathers a token's k rows the same way and sums them in slot order.
 
 #include <mutex>
 
@@ -26,16 +28,16 @@ namespace ff8 {
 
 namespace {
 
-constexpr int kChunk = 256;  // tokens per routing chunk
+constexpr int kChunk = kRouteChunk;  // tokens per routing chunk
 constexpr int kThreads = 256;
 constexpr int kRowThreadsMax = 512;  // one-token workgroups (permute, unpermute)
 
 int64_t n_chunks_of(int64_t T) { return (T + kChunk - 1) / kChunk; }
 
-__global__ __launch_bounds__(kThreads) void route_count_kernel(const int32_t* __restrict__ idx, int64_t T, int k,
-                                                               int E, int32_t* __restrict__ counts) {
+__global__ __launch_bounds__(kChunk) void route_count_kernel(const int32_t* __restrict__ idx, int64_t T, int k,
+                                                             int E, int32_t* __restrict__ counts) {
   __shared__ int cnt[1024];
-  for (int e = threadIdx.x; e < E; e += kThreads) cnt[e] = 0;
+  for (int e = threadIdx.x; e < E; e += kChunk) cnt[e] = 0;
   __syncthreads();
   const int64_t t = (int64_t)blockIdx.x * kChunk + threadIdx.x;
   if (t < T) {
@@ -45,7 +47,7 @@ __global__ __launch_bounds__(kThreads) void route_count_kernel(const int32_t* __
     }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < E; e += kThreads) counts[(int64_t)blockIdx.x * E + e] = cnt[e];
+  for (int e = threadIdx.x; e < E; e += kChunk) counts[(int64_t)blockIdx.x * E + e] = cnt[e];
 }
 
 // Thread (e, part) of P = 1024 / E parts owns a contiguous range of chunks of expert e:
@@ -135,8 +137,30 @@ __global__ __launch_bounds__(64) void route_assign_kernel(const int32_t* __restr
   }
 }
 
+// Padding rows of expert e's group (src_row == -1, below offsets[e + 1]): bytes 0x00, scales
+// 2^-126.  A group is padded by fewer than 128 rows, all among its last 128; the workgroup's
+// waves take those rows in turn (wave-uniform tests, one 16-byte store per lane and chunk).
+template <typename S>
+__device__ __forceinline__ void pad_group(int e, const int32_t* __restrict__ offsets,
+                                          const int32_t* __restrict__ src_row, int64_t H, uint8_t* __restrict__ q,
+                                          S* __restrict__ s) {
+  const int64_t g0 = offsets[e], g1 = offsets[e + 1];
+  const int64_t r0 = g1 - g0 > kTile ? g1 - kTile : g0;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int n_waves = blockDim.x >> 6;
+  const int64_t c16 = H / 16, sh = H / kTile;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int64_t r = r0 + wave; r < g1; r += n_waves) {
+    if (src_row[r] >= 0) continue;
+    uint8_t* row = q + r * H;
+    for (int64_t c = lane; c < c16; c += 64) stnt16(row + c * 16, z);
+    for (int64_t c = lane; c < sh; c += 64) put_scale(&s[r * sh + c], kTMin);
+  }
+}
+
 // One workgroup per token: lane c covers 16 elements (two 16-byte loads) of the row, 8
-// lanes one 128-element tile (8-lane DPP amax).  The token's k destination rows and
+// lanes one 128-element tile (8-lane DPP amax).  Workgroups T.. T + E - 1 fill the padding
+// rows of expert groups 0..E-1 instead.  The token's k destination rows and
 // weights are workgroup-uniform (scalar loads); every copy is one 16-byte store per lane,
 // so a wave writes 1 KB contiguous of one destination row.
 template <bool kWeighted, typename S>
@@ -144,8 +168,14 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uin
                                                                        const float* __restrict__ row_w, int64_t H,
                                                                        int k, const int32_t* __restrict__ row_map,
                                                                        int64_t M_cap, uint8_t* __restrict__ q,
-                                                                       S* __restrict__ s) {
+                                                                       S* __restrict__ s, int64_t T,
+                                                                       const int32_t* __restrict__ offsets,
+                                                                       const int32_t* __restrict__ src_row) {
   const int64_t t = blockIdx.x;
+  if (t >= T) {
+    pad_group<S>((int)(t - T), offsets, src_row, H, q, s);
+    return;
+  }
   const int64_t n16 = H / 16, sh = H / kTile;
   for (int64_t c = threadIdx.x; c < n16; c += blockDim.x) {  // uniform per 8-lane tile
     const bool leader = (c & 7) == 0;
@@ -191,9 +221,14 @@ constexpr int kMaxKDprobs = 64;
 __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_dprobs_kernel(
     const uint16_t* __restrict__ dy, const float* __restrict__ row_w, int64_t H, int k,
     const int32_t* __restrict__ row_map, int64_t M_cap, uint8_t* __restrict__ q, float* __restrict__ s,
-    const uint16_t* __restrict__ y_perm, float* __restrict__ dprobs) {
+    const uint16_t* __restrict__ y_perm, float* __restrict__ dprobs, int64_t T, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ src_row) {
   __shared__ float part[kMaxKDprobs * (kRowThreadsMax / 64)];
   const int64_t t = blockIdx.x;
+  if (t >= T) {  // padding rows of group t - T (the whole workgroup leaves before any barrier)
+    pad_group<float>((int)(t - T), offsets, src_row, H, q, s);
+    return;
+  }
   const int64_t n16 = H / 16, sh = H / kTile;
   const int c = threadIdx.x, wave = c >> 6, n_waves = blockDim.x >> 6;
   const bool act = c < n16;  // uniform per 8-lane tile
@@ -236,30 +271,6 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_dprobs_kernel(
     float sum = 0.0f;
     for (int w = 0; w < n_waves; ++w) sum += part[j * (kRowThreadsMax / 64) + w];
     dprobs[t * k + j] = (row >= 0 && row < M_cap) ? sum : 0.0f;
-  }
-}
-
-// Padding rows (src_row == -1 below offsets[E]): bytes 0x00, scales 2^-126.  Padding
-// only occurs in the last 128-row block of a group; other blocks exit after their reads.
-// kPadSplit workgroups share a block: wave w of part p takes rows p * 4 + w + 32 j, a
-// fixed partition, so every padding row is written exactly once.
-constexpr int kPadSplit = 8;
-template <typename S>
-__global__ __launch_bounds__(kThreads) void pad_fill_kernel(const int32_t* __restrict__ offsets, int E,
-                                                            const int32_t* __restrict__ src_row, int H,
-                                                            uint8_t* __restrict__ q, S* __restrict__ s) {
-  const int blk = blockIdx.x / kPadSplit, part = blockIdx.x - blk * kPadSplit;
-  const int64_t r0 = (int64_t)blk * kTile, r_end = offsets[E];
-  if (r0 >= r_end) return;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int c16 = H / 16, sh = H / kTile;
-  const u32x4 z = {0u, 0u, 0u, 0u};
-  for (int i = part * (kThreads / 64) + wave; i < kTile; i += kPadSplit * (kThreads / 64)) {
-    const int64_t r = r0 + i;
-    if (r >= r_end || src_row[r] >= 0) continue;  // wave-uniform (groups padded to 16 may end inside a block)
-    uint8_t* row = q + r * H;
-    for (int c = lane; c < c16; c += 64) stnt16(row + c * 16, z);
-    for (int c = lane; c < sh; c += 64) put_scale(&s[r * sh + c], kTMin);
   }
 }
 
@@ -339,7 +350,7 @@ hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int al
   (void)M_cap;
   const int64_t nc = n_chunks_of(T);
   int32_t* counts = static_cast<int32_t*>(workspace);
-  if (nc > 0) route_count_kernel<<<(unsigned)nc, kThreads, 0, st>>>(topk_idx, T, k, E, counts);
+  if (nc > 0) route_count_kernel<<<(unsigned)nc, kChunk, 0, st>>>(topk_idx, T, k, E, counts);
   route_scan_kernel<<<1, 1024, 0, st>>>(counts, nc, E, align, offsets, src_row);
   if (nc > 0) route_assign_kernel<<<(unsigned)nc, 64, 0, st>>>(topk_idx, T, k, E, counts, row_map, src_row);
   return hipGetLastError();
@@ -373,13 +384,13 @@ template <typename S>
 static hipError_t permute_quant_impl(const uint16_t* x, const float* row_w, int64_t T, int64_t H, int k, int E,
                                      const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                      int64_t M_cap, uint8_t* q, S* s, hipStream_t st) {
-  if (T > 0) {
-    if (row_w)
-      permute_quant_kernel<true, S><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
-    else
-      permute_quant_kernel<false, S><<<(unsigned)T, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s);
-  }
-  pad_fill_kernel<S><<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
+  const unsigned grid = (unsigned)(T + E);  // tokens, then one padding workgroup per expert group
+  if (row_w)
+    permute_quant_kernel<true, S><<<grid, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s, T, offsets,
+                                                                   src_row);
+  else
+    permute_quant_kernel<false, S><<<grid, row_threads(H), 0, st>>>(x, row_w, H, k, row_map, M_cap, q, s, T, offsets,
+                                                                    src_row);
   return hipGetLastError();
 }
 
@@ -398,10 +409,8 @@ hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, i
                                        const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                        int64_t M_cap, uint8_t* q, float* s, const uint16_t* y_perm, float* dprobs,
                                        hipStream_t st) {
-  if (T > 0)
-    permute_quant_dprobs_kernel<<<(unsigned)T, row_threads(H), 0, st>>>(dy, row_w, H, k, row_map, M_cap, q, s, y_perm,
-                                                                       dprobs);
-  pad_fill_kernel<float><<<(unsigned)(M_cap / kTile * kPadSplit), kThreads, 0, st>>>(offsets, E, src_row, (int)H, q, s);
+  permute_quant_dprobs_kernel<<<(unsigned)(T + E), row_threads(H), 0, st>>>(dy, row_w, H, k, row_map, M_cap, q, s,
+                                                                             y_perm, dprobs, T, offsets, src_row);
   return hipGetLastError();
 }
 
