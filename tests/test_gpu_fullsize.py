@@ -198,6 +198,56 @@ def test_fc2_fc1_wgrad_sampled(run):
     _wgrad_samples(run, "daT", "xT", "dw1")
 
 
+def _whole_tiles(run):
+    """Two 256 x 256 output tiles per GEMM: the first row tile of the busiest expert with the
+    first column tile, and the last (ragged) row tile of another busy expert with the last
+    column tile.  Every lane, accumulator and epilogue position of the tile is compared."""
+    off, rng = run["off"], run["rng"]
+    rows = off[1:] - off[:-1]
+    busy = np.nonzero(rows > 0)[0]
+    e0 = int(np.argmax(rows))
+    e1 = int(rng.choice(busy[busy != e0])) if busy.size > 1 else e0
+    lo1, hi1 = int(off[e1]), int(off[e1 + 1])
+    last = lo1 + (hi1 - lo1 - 1) // 256 * 256
+    return [(e0, np.arange(int(off[e0]), min(int(off[e0]) + 256, int(off[e0 + 1]))), True),
+            (e1, np.arange(last, hi1), False)]
+
+
+def _cols(n, first):
+    return np.arange(0, 256) if first else np.arange(n - 256, n)
+
+
+def test_gemm_whole_tiles(run):
+    b, off = run["b"], run["off"]
+    for e, m, first in _whole_tiles(run):
+        for qa, sa, wn, out in (("xq", "xs", "w1", "a"), ("hq", "hs", "w2", "y_perm")):  # fprop
+            n = _cols(b[out].shape[1], first)
+            a = quant.dequant_rowwise(_rows(b[qa], m), _rows(b[sa], m))
+            w = _dequant_weight(host(b[wn + "q"][e].index_select(0, _cuda_idx(n))),
+                                host(b[wn + "s"][e].index_select(0, _cuda_idx(n // 128))))
+            got = host(b[out].index_select(0, _cuda_idx(m)).index_select(1, _cuda_idx(n)).float())
+            _check_gemm_samples(got.ravel(), (a @ w.T).ravel(), (np.abs(a) @ np.abs(w).T).ravel(), True, a.shape[1])
+        for qg, sg, wn, out in (("dyq", "dys", "w2", "dh"), ("daq", "das", "w1", "dx_perm")):  # dgrad
+            c = _cols(b[out].shape[1], first)
+            g = quant.dequant_rowwise(_rows(b[qg], m), _rows(b[sg], m))
+            wq = host(b[wn + "q"][e].index_select(1, _cuda_idx(c))).T           # [256 c, N]
+            ws = host(b[wn + "s"][e].index_select(1, _cuda_idx(c // 128))).T    # [256 c, N / 128]
+            w = _dequant_weight(wq, ws)
+            got = host(b[out].index_select(0, _cuda_idx(m)).index_select(1, _cuda_idx(c)).float())
+            _check_gemm_samples(got.ravel(), (g @ w.T).ravel(), (np.abs(g) @ np.abs(w).T).ravel(), True, g.shape[1])
+        lo, hi = int(off[e]), int(off[e + 1])
+        blk = _cuda_idx(np.arange(lo, hi) // 128)
+        for gT, xT, out in (("dyT", "hT", "dw2"), ("daT", "xT", "dw1")):  # wgrad
+            N, K = b[out].shape[1:]
+            n, c = _cols(N, first), _cols(K, first)
+            g = codec.e4m3_decode(host(b[gT + "q"][_cuda_idx(n), lo:hi])) * \
+                host(b[gT + "s"].index_select(0, blk)[:, _cuda_idx(n)]).T.astype(np.float64)
+            x = codec.e4m3_decode(host(b[xT + "q"][_cuda_idx(c), lo:hi])) * \
+                host(b[xT + "s"].index_select(0, blk)[:, _cuda_idx(c)]).T.astype(np.float64)
+            got = host(b[out][e].index_select(0, _cuda_idx(n)).index_select(1, _cuda_idx(c)))
+            _check_gemm_samples(got.ravel(), (g @ x.T).ravel(), (np.abs(g) @ np.abs(x).T).ravel(), False, hi - lo)
+
+
 def test_swiglu_fwd_bwd_sampled_rows(run):
     b = run["b"]
     m, _ = _sample_rows(run, 48)
