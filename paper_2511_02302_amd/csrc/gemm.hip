@@ -124,11 +124,14 @@ __device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
 // rows past a tensor's end read zeros, so tiles at the edges need no clamping.  Issued
 // through inline asm so that the compiler does not serialize the pipeline with
 // conservative waits; the kernel waits for its own DMA (vmcnt) before the barrier that
-// publishes a stage.  The compiler's hazard checks do not look inside asm, so each asm
-// starts with the 5 wait states that a buffer instruction needs after a VALU write of an
-// SGPR it reads (the resource or M0 may come straight from v_readfirstlane, or from
-// v_readlane when the compiler reloads a spilled SGPR); with fewer, the load can use the
-// register's old value.
+// publishes a stage.  The compiler's hazard checks do not look inside asm.  A buffer
+// instruction needs 5 wait states after a VALU write of an SGPR it reads (the resource or M0
+// may come straight from v_readfirstlane, or from v_readlane when the compiler reloads a
+// spilled SGPR), and an LDS DMA 1 after an SALU write of M0; with fewer, the load can use the
+// register's old value.  The DMAs issued right after a tile's setup (kLoop false) carry all 5.
+// Inside the K loop the resources are loop-invariant and M0 is set by s_mov, so the DMAs there
+// carry 1 (4 issue cycles fewer per DMA, 1-2% on every GEMM); the hazard scan of the compiled
+// kernels checks that no VALU write of an SGPR they read comes closer.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 // Raw (stride 0) buffer resource: loads at offsets >= `bytes` return zeros.
 __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0xFFFFFFFFu) {
@@ -140,15 +143,25 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes = 0x
   r[3] = 0x00020000;   // raw 32-bit data format
   return r;
 }
+template <bool kLoop = false>
 __device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
-               : "memory");
+  if constexpr (kLoop)
+    asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+                 : "memory");
+  else
+    asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+                 : "memory");
 }
 // 4-byte form (scales).  The scale DMAs, like the operand DMAs, keep their whole offset in
 // the range-checked voffset, so a lane past a scale tensor's end reads zeros.
+template <bool kLoop = false>
 __device__ __forceinline__ void dma4(const i32x4& rsrc, uint32_t voff, uint32_t lds_off) {
-  asm volatile("s_nop 4\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
-               : "memory");
+  if constexpr (kLoop)
+    asm volatile("s_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+                 : "memory");
+  else
+    asm volatile("s_nop 4\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "{m0}"(lds_off), "v"(voff), "s"(rsrc)
+                 : "memory");
 }
 
 __device__ __forceinline__ i32x8 with_half(i32x8 f, const u32x4& x, int half) {
@@ -223,20 +236,20 @@ struct Tile {
     const bool drop = (kp == 0 && c16 < k_lo) || ((int)kp == nk - 1 && c16 >= k_hi);
     return drop ? end : off;
   }
-  template <int B, int I, bool kMask = false>
+  template <int B, int I, bool kMask = false, bool kLoop = false>
   __device__ __forceinline__ void dma_tile(int ks) {
     const uint32_t stage = stage_lds<B>();
     const uint32_t kp = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(ks));  // uniform
     if constexpr (I < 8) {
       if constexpr (MODE == kDgrad) {
         const uint32_t step = kp * (uint32_t)p_kstep + (uint32_t)(I >> 1) * (uint32_t)p_istep;
-        dma16(p_rsrc, p_voff[I & 1] + step, stage + (uint32_t)wave * 8192u + I * 1024);
+        dma16<kLoop>(p_rsrc, p_voff[I & 1] + step, stage + (uint32_t)wave * 8192u + I * 1024);
       } else {
         const uint32_t step = kp * (uint32_t)p_kstep + (uint32_t)(I & 3) * (uint32_t)p_istep;
         const uint32_t grp = (uint32_t)wave + (I < 4 ? 8 * I : 4 + 8 * (I - 4));
         uint32_t off = p_voff[I >> 2] + step;
         if constexpr (kMask) off = masked_off(off, kp, (uint32_t)p_rsrc[2]);
-        dma16(p_rsrc, off, stage + grp * 1024u);
+        dma16<kLoop>(p_rsrc, off, stage + grp * 1024u);
       }
     } else {
       constexpr int J = I - 8;
@@ -244,7 +257,7 @@ struct Tile {
       const uint32_t grp = (uint32_t)wave + (J < 4 ? 8 * J : 4 + 8 * (J - 4));
       uint32_t off = q_voff[J >> 2] + step;
       if constexpr (kMask) off = masked_off(off, kp, (uint32_t)q_rsrc[2]);
-      dma16(q_rsrc, off, stage + kTileBytes + grp * 1024u);
+      dma16<kLoop>(q_rsrc, off, stage + kTileBytes + grp * 1024u);
     }
   }
   // Scale DMA of batch b (K blocks kb0..kb0+3 in loop order) into batch buffer b % 2:
@@ -258,33 +271,35 @@ struct Tile {
   //     lane l the tile rows 4l..4l+3, one contiguous 1 KB (256-byte) run -> LDS [K block][256 rows].
   // Batches are rotated with the K order (k_rot is a multiple of the batch); blocks past
   // the last K block read neighbouring scales or zeros and are never multiplied.
+  template <bool kLoop = false>
   __device__ __forceinline__ void dma_scale_p(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1));
     if constexpr (kBlockP) {
       const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
-      dma4(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * kSB, lbase);
+      dma4<kLoop>(sp_rsrc, sp_off + kb0 * (uint32_t)sp_kb * kSB, lbase);
     } else {  // wgrad: wave w takes the block of stage 4 b + w (the rotation may wrap inside a batch)
       const uint32_t kbw = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch + wave));
       if constexpr (kE8)
-        dma4(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb, lbase + (uint32_t)wave * 256u);
+        dma4<kLoop>(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb, lbase + (uint32_t)wave * 256u);
       else
-        dma16(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
+        dma16<kLoop>(sp_rsrc, sp_off + kbw * (uint32_t)sp_kb * 4u, lbase + (uint32_t)wave * 1024u);
     }
   }
+  template <bool kLoop = false>
   __device__ __forceinline__ void dma_scale_q(int b) {
     const uint32_t lbase = scale_lds((int)(b & 1)) + kTP * kScaleBatch * 4;
     if constexpr (MODE == kWgrad) {
       const uint32_t kbw = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch + wave));
       if constexpr (kE8)
-        dma4(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb, lbase + (uint32_t)wave * 256u);
+        dma4<kLoop>(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb, lbase + (uint32_t)wave * 256u);
       else
-        dma16(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
+        dma16<kLoop>(sq_rsrc, sq_off + kbw * (uint32_t)sq_kb * 4u, lbase + (uint32_t)wave * 1024u);
     } else {
       const uint32_t kb0 = (uint32_t)__builtin_amdgcn_readfirstlane(kphys(b * kScaleBatch));
       if constexpr (kE8)
-        dma4(sq_rsrc, sq_off + kb0, lbase + (uint32_t)wave * 256u);
+        dma4<kLoop>(sq_rsrc, sq_off + kb0, lbase + (uint32_t)wave * 256u);
       else
-        dma16(sq_rsrc, sq_off + kb0 * 4u, lbase + (uint32_t)wave * 1024u);
+        dma16<kLoop>(sq_rsrc, sq_off + kb0 * 4u, lbase + (uint32_t)wave * 1024u);
     }
   }
 
@@ -411,7 +426,7 @@ struct Tile {
   template <int B, int D0, int D1>
   __device__ __forceinline__ void dma_range(int ks_dma) {
     if constexpr (D0 < D1) {
-      dma_tile<B, D0>(ks_dma);
+      dma_tile<B, D0, false, true>(ks_dma);
       dma_range<B, D0 + 1, D1>(ks_dma);
     }
   }
@@ -421,8 +436,8 @@ struct Tile {
   template <int B, int S4, int J>
   __device__ __forceinline__ void dma_slot(int ks_dma, int ks_next) {
     dma_range<B, dma_before(J), dma_before(J + 1)>(ks_dma);
-    if constexpr (S4 == 0 && J == 16 - kEarly + 1) dma_scale_p((ks_next >> 2) + 1);
-    if constexpr (S4 == 0 && J == 16 - kEarly + 3) dma_scale_q((ks_next >> 2) + 1);
+    if constexpr (S4 == 0 && J == 16 - kEarly + 1) dma_scale_p<true>((ks_next >> 2) + 1);
+    if constexpr (S4 == 0 && J == 16 - kEarly + 3) dma_scale_q<true>((ks_next >> 2) + 1);
   }
   // Fragment reads of MFMA slot I: the half-step's kFragReads reads spread evenly over
   // its first kReadSlots slots.
@@ -769,8 +784,8 @@ __device__ __forceinline__ void dma_first_stage(Tile<MODE, SC>& T) {
   T.template dma_tile<0, 9, MODE == kWgrad>(0); T.template dma_tile<0, 10, MODE == kWgrad>(0); T.template dma_tile<0, 11, MODE == kWgrad>(0);
   T.template dma_tile<0, 12, MODE == kWgrad>(0); T.template dma_tile<0, 13, MODE == kWgrad>(0); T.template dma_tile<0, 14, MODE == kWgrad>(0);
   T.template dma_tile<0, 15, MODE == kWgrad>(0);
-  T.dma_scale_p(0);
-  T.dma_scale_q(0);
+  T.template dma_scale_p<false>(0);
+  T.template dma_scale_q<false>(0);
 }
 // Second-stage DMA (stage 1, or a reload of stage 0 when nk == 1) into buffer 1: exactly
 // kStage1Dma instructions per wave, the newest in flight when stage 0 is awaited.
