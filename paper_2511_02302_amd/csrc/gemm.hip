@@ -207,6 +207,11 @@ struct Tile {
   // fprop / dgrad: a wave's 128 P rows are one 128x128 weight block, so its P scale is one
   // value per K block (stored compactly as [tile half][4 K blocks]); wgrad: one per row.
   static constexpr bool kBlockP = (MODE != kWgrad);
+  // wgrad reads and packs the next batch's per-row scales of P in the second stage of a batch
+  // and those of Q in the fourth (its scale DMA lands by the middle of the second), instead of
+  // both in the fourth: fewer VALU packs crowd one stage's MFMA slots (+0.6%).  fprop and dgrad
+  // keep them in the fourth stage, where the packed words are not live across stages.
+  static constexpr bool kSpreadScales = (MODE == kWgrad);
   int wave, lane, wp, wq;
   int nk;
   int k_rot;  // K stages this tile's loop is rotated by (fprop: a multiple of the scale batch)
@@ -474,21 +479,33 @@ struct Tile {
   // Second half-step: MFMAs on set B.  The rest of stage ks+2's DMA (with the next scale
   // batch among it when ks % 4 == 0, landing by the middle of the next stage); the reads of
   // stage ks+1's first half (other buffer) into set A over the first kReadSlots MFMAs; in
-  // the last stage of a batch the next batch's scales are read and packed.
+  // the last stage of a batch the next batch's scales are read and packed (wgrad: those of P
+  // in the second stage, kSpreadScales).
   template <int B, int S4, int I>
   __device__ __forceinline__ void half1_from(int ks_dma, int ks_next) {
     if constexpr (I < 16) {
       mfma_op<false, S4, I>();
       dma_slot<B, S4, 16 - kEarly + I>(ks_dma, ks_next);
       reads_of_slot<1 - B, 0, true, I>();
-      if constexpr (S4 == 3 && I == 8) read_scale_rows<false, 0, 2>(ks_next >> 2, rsp);
-      if constexpr (S4 == 3 && I == 9) read_scale_rows<true, 0, 2>(ks_next >> 2, rsq);
-      if constexpr (S4 == 3 && I == 10) pack_scales<false, 0, 2>(rsp, np);
-      if constexpr (S4 == 3 && I == 11) read_scale_rows<false, 2, 4>(ks_next >> 2, rsp);
-      if constexpr (S4 == 3 && I == 11) pack_scales<true, 0, 2>(rsq, nq);
-      if constexpr (S4 == 3 && I == 12) read_scale_rows<true, 2, 4>(ks_next >> 2, rsq);
-      if constexpr (S4 == 3 && I == 13) pack_scales<false, 2, 4>(rsp, np);
-      if constexpr (S4 == 3 && I == 14) pack_scales<true, 2, 4>(rsq, nq);
+      if constexpr (kSpreadScales) {
+        if constexpr (S4 == 1 && I == 8) read_scale_rows<false, 0, 2>((ks_next >> 2) + 1, rsp);
+        if constexpr (S4 == 1 && I == 10) pack_scales<false, 0, 2>(rsp, np);
+        if constexpr (S4 == 1 && I == 12) read_scale_rows<false, 2, 4>((ks_next >> 2) + 1, rsp);
+        if constexpr (S4 == 1 && I == 14) pack_scales<false, 2, 4>(rsp, np);
+        if constexpr (S4 == 3 && I == 8) read_scale_rows<true, 0, 2>(ks_next >> 2, rsq);
+        if constexpr (S4 == 3 && I == 10) pack_scales<true, 0, 2>(rsq, nq);
+        if constexpr (S4 == 3 && I == 12) read_scale_rows<true, 2, 4>(ks_next >> 2, rsq);
+        if constexpr (S4 == 3 && I == 14) pack_scales<true, 2, 4>(rsq, nq);
+      } else {
+        if constexpr (S4 == 3 && I == 8) read_scale_rows<false, 0, 2>(ks_next >> 2, rsp);
+        if constexpr (S4 == 3 && I == 9) read_scale_rows<true, 0, 2>(ks_next >> 2, rsq);
+        if constexpr (S4 == 3 && I == 10) pack_scales<false, 0, 2>(rsp, np);
+        if constexpr (S4 == 3 && I == 11) read_scale_rows<false, 2, 4>(ks_next >> 2, rsp);
+        if constexpr (S4 == 3 && I == 11) pack_scales<true, 0, 2>(rsq, nq);
+        if constexpr (S4 == 3 && I == 12) read_scale_rows<true, 2, 4>(ks_next >> 2, rsq);
+        if constexpr (S4 == 3 && I == 13) pack_scales<false, 2, 4>(rsp, np);
+        if constexpr (S4 == 3 && I == 14) pack_scales<true, 2, 4>(rsq, nq);
+      }
       __builtin_amdgcn_sched_barrier(0);
       half1_from<B, S4, I + 1>(ks_dma, ks_next);
     }
