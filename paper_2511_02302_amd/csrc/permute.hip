@@ -9,10 +9,11 @@
 //   route_scan   : one workgroup (E x parts threads) turns the counts into per-chunk
 //                  bases, pads every expert to a multiple of 128 rows, writes
 //                  offsets[E+1] and marks the padding rows' src_row = -1;
-//   route_assign : one wave per chunk walks its tokens 64 at a time; a 64-bit LDS
-//                  ballot mask per expert gives each pair its rank among earlier lanes.
-// (64-token chunks, four times the workgroups, measured the same: the three routing launches
-// take about 26 us at the DeepSeek-V3 share whatever the chunk.)
+//   route_assign : one workgroup per chunk, one wave per 64 tokens; a 64-bit LDS mask per
+//                  wave and expert gives each pair its rank among earlier lanes and waves.
+// (64-token chunks, four times the workgroups, measured the same; four waves per chunk in
+// route_assign instead of one wave walking it 64 tokens at a time saved 6 us of the routing
+// launches' ~26 us at the DeepSeek-V3 share.)
 // Then permute_quant reads each token row ONCE (one workgroup per token, 16 elements per
 // lane, 8 lanes per 1x128 tile, DPP amax), quantizes it and writes it to each of its k
 // rows; with routing weights each copy is scaled (float32 product) and quantized
@@ -102,38 +103,42 @@ __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ 
   if (threadIdx.x == 0) offsets[E] = offs[E];
 }
 
-__global__ __launch_bounds__(64) void route_assign_kernel(const int32_t* __restrict__ idx, int64_t T, int k, int E,
-                                                          const int32_t* __restrict__ bases,
-                                                          int32_t* __restrict__ row_map, int32_t* __restrict__ src_row) {
+// One workgroup (4 waves) per chunk: wave w takes tokens 64 w .. 64 w + 63 of the chunk and
+// sets, per expert, a 64-bit LDS mask of its lanes routed there; a pair's rank is the
+// chunk's base for its expert, plus the popcounts of that expert's masks in earlier waves,
+// plus its position among earlier lanes of its own mask.  All four waves work at once (one
+// round of routing loads per chunk instead of four).
+__global__ __launch_bounds__(kChunk) void route_assign_kernel(const int32_t* __restrict__ idx, int64_t T, int k, int E,
+                                                             const int32_t* __restrict__ bases,
+                                                             int32_t* __restrict__ row_map, int32_t* __restrict__ src_row) {
+  static_assert(kChunk == 256, "four waves of 64 tokens per chunk");
   __shared__ int run[1024];
-  __shared__ unsigned long long mask[1024];
-  const int lane = threadIdx.x;
+  __shared__ unsigned long long mask[4][1024];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t chunk = blockIdx.x;
-  for (int e = lane; e < E; e += 64) run[e] = bases[chunk * E + e];
+  for (int e = tid; e < E; e += kChunk) {
+    run[e] = bases[chunk * E + e];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mask[w][e] = 0ull;
+  }
+  __syncthreads();
+  const int64_t t = chunk * kChunk + tid;
+  const bool valid = t < T;
+  for (int j = 0; j < k && valid; ++j) {
+    const int e = idx[t * k + j];
+    if (e >= 0 && e < E) atomicOr(&mask[wave][e], 1ull << lane);
+  }
+  __syncthreads();
   const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int b = 0; b < kChunk / 64; ++b) {
-    const int64_t t = chunk * kChunk + b * 64 + lane;
-    if (chunk * kChunk + b * 64 >= T) break;  // uniform
-    for (int e = lane; e < E; e += 64) mask[e] = 0ull;
-    __syncthreads();
-    const bool valid = t < T;
-    for (int j = 0; j < k; ++j) {
-      const int e = valid ? idx[t * k + j] : -1;
-      if (e >= 0 && e < E) atomicOr(&mask[e], 1ull << lane);
+  for (int j = 0; j < k && valid; ++j) {
+    const int e = idx[t * k + j];
+    int row = -1;
+    if (e >= 0 && e < E) {
+      row = run[e] + __popcll(mask[wave][e] & below);
+      for (int w = 0; w < wave; ++w) row += __popcll(mask[w][e]);
+      src_row[row] = (int32_t)(t * k + j);
     }
-    __syncthreads();
-    for (int j = 0; j < k && valid; ++j) {
-      const int e = idx[t * k + j];
-      int row = -1;
-      if (e >= 0 && e < E) {
-        row = run[e] + __popcll(mask[e] & below);
-        src_row[row] = (int32_t)(t * k + j);
-      }
-      row_map[t * k + j] = row;
-    }
-    __syncthreads();
-    for (int e = lane; e < E; e += 64) run[e] += __popcll(mask[e]);
-    __syncthreads();
+    row_map[t * k + j] = row;
   }
 }
 
@@ -352,7 +357,7 @@ hipError_t launch_route(const int32_t* topk_idx, int64_t T, int k, int E, int al
   int32_t* counts = static_cast<int32_t*>(workspace);
   if (nc > 0) route_count_kernel<<<(unsigned)nc, kChunk, 0, st>>>(topk_idx, T, k, E, counts);
   route_scan_kernel<<<1, 1024, 0, st>>>(counts, nc, E, align, offsets, src_row);
-  if (nc > 0) route_assign_kernel<<<(unsigned)nc, 64, 0, st>>>(topk_idx, T, k, E, counts, row_map, src_row);
+  if (nc > 0) route_assign_kernel<<<(unsigned)nc, kChunk, 0, st>>>(topk_idx, T, k, E, counts, row_map, src_row);
   return hipGetLastError();
 }
 
