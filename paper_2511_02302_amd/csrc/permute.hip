@@ -51,15 +51,43 @@ __global__ __launch_bounds__(kChunk) void route_count_kernel(const int32_t* __re
   for (int e = threadIdx.x; e < E; e += kChunk) counts[(int64_t)blockIdx.x * E + e] = cnt[e];
 }
 
-// Thread (e, part) of P = 1024 / E parts owns a contiguous range of chunks of expert e:
-// it sums them, the parts' sums are scanned per expert in LDS, and each thread then
-// rewrites its range as exclusive bases.  All chunk loads of a pass are independent.
+// Inclusive sum over the 1024 threads of the workgroup, in thread order: a 64-lane shuffle
+// scan per wave, then the 16 wave totals scanned by one wave (wsum: 16 ints of LDS).
+__device__ __forceinline__ int block_inclusive_sum(int v, int* wsum) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d);
+    if (lane >= d) v += u;
+  }
+  if (lane == 63) wsum[w] = v;
+  __syncthreads();
+  if (w == 0) {
+    int x = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+    for (int d = 1; d < 16; d <<= 1) {
+      const int u = __shfl_up(x, d);
+      if (lane >= d) x += u;
+    }
+    if (lane < 16) wsum[lane] = x;
+  }
+  __syncthreads();
+  const int r = w > 0 ? v + wsum[w - 1] : v;
+  __syncthreads();  // wsum is reused by the next call
+  return r;
+}
+
+// Thread (e, part) of P = 1024 / E parts owns a contiguous range of chunks of expert e: it
+// sums them; one block-wide scan of the part sums (expert-major) gives each part's base
+// within its expert and each expert's total; a second scan of the padded totals gives the
+// group offsets; each thread then rewrites its range as exclusive bases.  All chunk loads
+// of a pass are independent.
 __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ counts, int64_t n_chunks, int E,
                                                           int align, int32_t* __restrict__ offsets,
                                                           int32_t* __restrict__ src_row) {
-  __shared__ int part_sum[1024];  // [e][part], then exclusive prefix within e
-  __shared__ int totals[1024];
+  __shared__ int incl[1024];  // inclusive scan of the part sums, expert-major
   __shared__ int offs[1025];
+  __shared__ int wsum[16];
   const int P = 1024 / E;  // parts per expert (E <= 1024)
   const int e = threadIdx.x / P, part = threadIdx.x - e * P;
   const int64_t per = (n_chunks + P - 1) / P;
@@ -68,29 +96,21 @@ __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ 
   int sum = 0;
   if (e < E)
     for (int64_t c = c0; c < c1; ++c) sum += counts[c * E + e];
-  part_sum[threadIdx.x] = sum;
+  incl[threadIdx.x] = block_inclusive_sum(sum, wsum);
   __syncthreads();
-  if (threadIdx.x < E) {  // per expert: exclusive scan over its parts, total, padded size
-    int acc = 0;
-    for (int i = 0; i < P; ++i) {
-      const int v = part_sum[threadIdx.x * P + i];
-      part_sum[threadIdx.x * P + i] = acc;
-      acc += v;
-    }
-    totals[threadIdx.x] = acc;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int i = 0; i < E; ++i) {
-      offs[i] = acc;
-      acc += (totals[i] + align - 1) / align * align;
-    }
-    offs[E] = acc;
-  }
+  // expert x's rows: incl[x P + P - 1] - incl[x P - 1]; padded to the alignment, scanned
+  const int x = threadIdx.x;
+  int total = 0;
+  if (x < E) total = incl[x * P + P - 1] - (x > 0 ? incl[x * P - 1] : 0);
+  const int padded = (total + align - 1) / align * align;
+  const int end = block_inclusive_sum(padded, wsum);
+  if (x < E) offs[x + 1] = end;
+  if (x == 0) offs[0] = 0;
   __syncthreads();
   if (e < E) {
-    int run = offs[e] + part_sum[threadIdx.x];
+    const int seg0 = e > 0 ? incl[e * P - 1] : 0;
+    const int tot = incl[e * P + P - 1] - seg0;
+    int run = offs[e] + (incl[threadIdx.x] - sum - seg0);  // the part's exclusive base in the group
     for (int64_t c = c0; c < c1; ++c) {
       const int v = counts[c * E + e];
       counts[c * E + e] = run;
@@ -98,7 +118,7 @@ __global__ __launch_bounds__(1024) void route_scan_kernel(int32_t* __restrict__ 
     }
     if (part == 0) offsets[e] = offs[e];
     // padding rows of the group: src_row = -1, spread over the expert's parts
-    for (int r = offs[e] + totals[e] + part; r < offs[e + 1]; r += P) src_row[r] = -1;
+    for (int r = offs[e] + tot + part; r < offs[e + 1]; r += P) src_row[r] = -1;
   }
   if (threadIdx.x == 0) offsets[E] = offs[E];
 }
