@@ -361,8 +361,10 @@ def cast_accuracy(torch):
     d_row = dec(q) * rep(s)                                   # D(Q_row X), [R, C]
     d_rowT = d_row.t().contiguous()
     del d_row
-    qT, sT = torch.empty((C, R), dtype=torch.uint8, device="cuda"), torch.empty((R // 128, C), device="cuda")
-    ff8.ff8_scaling_aware_transpose(q, s, qT, sT)
+    qK, sT = torch.empty((R // 128, C, 128), dtype=torch.uint8, device="cuda"), torch.empty((R // 128, C), device="cuda")
+    ff8.ff8_scaling_aware_transpose(q, s, qK, sT)
+    qT = qK.permute(1, 0, 2).reshape(C, R)                   # the K-blocked transpose as [C, R]
+    del qK
     xT = x.float().t().contiguous()
 
     def rel(a, b):
@@ -473,7 +475,7 @@ def cast_ops(torch, reps=20):
     xs = [x0] + [x0.clone() for _ in range(n_sets - 1)]
     qs = [torch.empty((R, C), dtype=torch.uint8, device="cuda") for _ in range(n_sets)]
     ss = [torch.empty((R, C // 128), dtype=torch.float32, device="cuda") for _ in range(n_sets)]
-    qTs = [torch.empty((C, R), dtype=torch.uint8, device="cuda") for _ in range(n_sets)]
+    qTs = [torch.empty((R // 128, C, 128), dtype=torch.uint8, device="cuda") for _ in range(n_sets)]
     sTs = [torch.empty((R // 128, C), dtype=torch.float32, device="cuda") for _ in range(n_sets)]
     for i in range(n_sets):
         ff8.ff8_quant_rowwise(xs[i], qs[i], ss[i])

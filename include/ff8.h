@@ -18,9 +18,12 @@
  *    Inputs to the quantizers must be finite.  The GEMMs read only the exponent
  *    field of each scale, so scales passed to them must be such powers of two.
  *  - Row-wise (1x128) scaled tensor: q [rows, cols] row-major, s [rows, cols/128].
- *    Column-wise scaled tensors are stored transposed, qT [cols, rows], with
- *    block-major scales sT [rows/128, cols]: row b holds the scale of every column
- *    over rows 128b..128b+127.  Block (128x128) scaled weights: q [E, N, K],
+ *    Column-wise scaled tensors are stored transposed and K-blocked,
+ *    qT [rows/128, cols, 128]: element (c, r) of the transpose (input row r,
+ *    column c) is byte (r/128) * cols * 128 + c * 128 + r % 128, so each block of
+ *    128 input rows is one contiguous [cols][128] slab.  Their scales are
+ *    block-major, sT [rows/128, cols]: row b holds the scale of every column over
+ *    rows 128b..128b+127.  Block (128x128) scaled weights: q [E, N, K],
  *    s [E, N/128, K/128].
  *  - Grouped (expert-contiguous) tensors have M_cap rows; expert e owns rows
  *    [offsets[e], offsets[e+1]), every group is padded to a multiple of the
@@ -202,12 +205,13 @@ int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, 
  *   dec(b) * 2^-k is rounded to nearest even on the subnormal grid.  No
  *   dequantize / requantize round trip happens, so there is no double
  *   quantization error.
- *   qT [cols, rows] e4m3 (physically transposed), sT [rows/128, cols] float32
- *   (block-major: sT[b, c] is the S_max of the 128x128 block holding row 128b and
- *   column c, the same for all 128 columns of a tile).
+ *   qT [rows/128, cols, 128] e4m3, the K-blocked transpose (element (c, r) at
+ *   [r/128, c, r%128]), sT [rows/128, cols] float32 (block-major: sT[b, c] is the
+ *   S_max of the 128x128 block holding row 128b and column c, the same for all
+ *   128 columns of a tile).  rows must be a multiple of 128 and cols of 128.
  *   offsets: [E+1] device int32 (only offsets[E] is read: rows at and beyond it
- *   are skipped and the matching qT columns / sT entries untouched) or NULL
- *   (all rows).  E is ignored when offsets is NULL.
+ *   are skipped and their qT bytes / sT entries untouched) or NULL (all rows).
+ *   E is ignored when offsets is NULL.
  */
 int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows, int64_t cols,
                                 const int32_t* offsets, int E, ff8_e4m3* qT, float* sT, void* stream);
@@ -239,8 +243,9 @@ int ff8_grouped_gemm_dgrad(const ff8_e4m3* g, const float* g_s, const ff8_e4m3* 
  * ff8_grouped_gemm_wgrad -- FP8 grouped GEMM, weight gradient ("Wgrad" of paper
  * section 3.1, fed by column-wise operands from the scaling-aware transpose).
  *   dw[e, n, k] (+)= sum_{m in expert e's rows} D(gT)[n, m] * D(xT)[k, m].
- *   gT [N, M_cap] e4m3 + gT_s [M_cap/128, N]; xT [K, M_cap] e4m3 + xT_s [M_cap/128, K]
- *   (block-major scales, as written by ff8_scaling_aware_transpose);
+ *   gT [M_cap/128, N, 128] e4m3 + gT_s [M_cap/128, N]; xT [M_cap/128, K, 128] e4m3
+ *   + xT_s [M_cap/128, K] (K-blocked transposes with block-major scales, as written
+ *   by ff8_scaling_aware_transpose);
  *   dw [E, N, K] float32.  accumulate = 0 overwrites (experts without rows get
  *   zeros); accumulate = 1 adds to dw (experts without rows are left untouched).
  */

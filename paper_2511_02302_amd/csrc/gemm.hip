@@ -7,6 +7,8 @@
 //   fprop: p = n (W_e rows),        q = token row m, k over K  -> out[m, n] bf16
 //   dgrad: p = k (W_e columns),     q = token row m, k = n     -> out[m, k] bf16
 //   wgrad: p = k (xT rows),         q = n (gT rows), k = token -> dw[e, n, k] fp32
+// The wgrad operands come K-blocked from the transpose: row r's bytes of token block b at
+// (b * rows + r) * 128.
 //
 // Matrix core: v_mfma_scale_f32_32x32x64_f8f6f4 (e4m3 x e4m3, fp32 accumulate).  The
 // library's scales are powers of two, i.e. exactly E8M0 values (the fp32 exponent
@@ -121,7 +123,9 @@ __device__ __forceinline__ int wswz(int j) { return ((2 * j) ^ (j >> 2)) & 15; }
 // LDS DMA (buffer_load ... lds): each lane loads 16 (or 4) bytes at resource base +
 // soff + voff into LDS at M0 + 16 * lane (or 4 * lane).  The resources cover exactly
 // their tensor, and every operand offset is in voffset, which the hardware range-checks:
-// rows past a tensor's end read zeros, so tiles at the edges need no clamping.  Issued
+// rows past a tensor's end read zeros, so tiles at the edges need no clamping (K-blocked
+// wgrad operands: rows past the end read the next block's rows, or zeros after the last
+// block; those rows' accumulators are never stored).  Issued
 // through inline asm so that the compiler does not serialize the pipeline with
 // conservative waits; the kernel waits for its own DMA (vmcnt) before the barrier that
 // publishes a stage.  The compiler's hazard checks do not look inside asm.  A buffer
@@ -610,14 +614,16 @@ __device__ __forceinline__ void setup_tile(Tile<MODE, SC>& T, const GemmArgs& g,
   const uint32_t q_rows = (MODE == kWgrad) ? (uint32_t)g.Nq : M_cap;
   // K-major row of pattern h (h = 0, 1) for this lane: group w + 4h, row 8 group + l / 8,
   // 16-byte chunk (l % 8) ^ kswz(row) (kswz depends on the group's parity and l / 16 only).
+  // wgrad operands are K-blocked ([M_cap/128][rows][128]): row r's 128 bytes of K block b sit
+  // at (b * rows + r) * 128, so one stage of a panel is 32 KB of consecutive bytes.
   T.q_rsrc = make_rsrc(g.Q, q_rows * q_ld);
-  T.q_kstep = kBK;
-  T.q_istep = (int)(64 * q_ld);
+  T.q_kstep = (MODE == kWgrad) ? (int)(q_rows * kBK) : kBK;
+  T.q_istep = (MODE == kWgrad) ? 64 * kBK : (int)(64 * q_ld);
 #pragma unroll
   for (uint32_t hh = 0; hh < 2; ++hh) {
     const uint32_t r = 8 * (wave + 4 * hh) + (lane >> 3);
     const uint32_t c = (lane & 7) ^ (uint32_t)kswz((int)r);
-    T.q_voff[hh] = (q0 + r) * q_ld + k0 + c * 16;
+    T.q_voff[hh] = (MODE == kWgrad) ? ((k0 / kBK) * q_rows + q0 + r) * kBK + c * 16 : (q0 + r) * q_ld + k0 + c * 16;
   }
   if (MODE == kDgrad) {  // W_e [N = Kdim][K = Np], rows n = 32w + 4i + l / 16
     T.p_rsrc = make_rsrc(g.P, (uint32_t)g.E * Kdim * Np);
@@ -634,13 +640,14 @@ __device__ __forceinline__ void setup_tile(Tile<MODE, SC>& T, const GemmArgs& g,
     const uint32_t p_rows = (MODE == kWgrad) ? Np : (uint32_t)g.E * Np;  // fprop: all experts' rows
     const uint32_t p_row0 = (MODE == kFprop) ? e * Np + p0 : p0;
     T.p_rsrc = make_rsrc(g.P, p_rows * p_ld);
-    T.p_kstep = kBK;
-    T.p_istep = (int)(64 * p_ld);
+    T.p_kstep = (MODE == kWgrad) ? (int)(p_rows * kBK) : kBK;
+    T.p_istep = (MODE == kWgrad) ? 64 * kBK : (int)(64 * p_ld);
 #pragma unroll
     for (uint32_t hh = 0; hh < 2; ++hh) {
       const uint32_t r = 8 * (wave + 4 * hh) + (lane >> 3);
       const uint32_t c = (lane & 7) ^ (uint32_t)kswz((int)r);
-      T.p_voff[hh] = (p_row0 + r) * p_ld + k0 + c * 16;
+      T.p_voff[hh] = (MODE == kWgrad) ? ((k0 / kBK) * p_rows + p_row0 + r) * kBK + c * 16
+                                      : (p_row0 + r) * p_ld + k0 + c * 16;
     }
   }
   // scale DMA sources (resources range-checked to the end of each scale tensor; offsets

@@ -243,15 +243,17 @@ def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y
 
 
 def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):
+    """qT is K-blocked: [rows // 128, cols, 128], element (c, r) of the transpose at [r // 128, c, r % 128]."""
     rows, cols = q.shape
-    _shape(s, (rows, cols // 128), "s"); _shape(qT, (cols, rows), "qT"); _shape(sT, (rows // 128, cols), "sT")
+    _shape(s, (rows, cols // 128), "s"); _shape(qT, (rows // 128, cols, 128), "qT")
+    _shape(sT, (rows // 128, cols), "sT")
     if offsets is not None:
         _numel(offsets, E + 1, "offsets")
     sd, sfx = _scale_kind(s, sT)
     name = "ff8_scaling_aware_transpose" + sfx
     _check(getattr(load(), name)(
         _ptr(q, _u8, "q", 2), _ptr(s, sd, "s", 2), rows, cols, _ptr(offsets, _i32, "offsets"), E,
-        _ptr(qT, _u8, "qT", 2), _ptr(sT, sd, "sT", 2), _stream(stream)), name)
+        _ptr(qT, _u8, "qT", 3), _ptr(sT, sd, "sT", 2), _stream(stream)), name)
 
 
 def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):
@@ -279,15 +281,19 @@ def ff8_grouped_gemm_dgrad(g, g_s, w, w_s, offsets, out, stream=None):
 
 
 def ff8_grouped_gemm_wgrad(gT, gT_s, xT, xT_s, offsets, dw, accumulate=False, stream=None):
-    N, M_cap = gT.shape
-    K = xT.shape[0]
+    """gT [M_cap // 128, N, 128] and xT [M_cap // 128, K, 128]: K-blocked transposes (as
+    ff8_scaling_aware_transpose writes them)."""
+    n_kb, N, _ = gT.shape
+    M_cap = 128 * n_kb
+    K = xT.shape[1]
     E = dw.shape[0]
-    _shape(gT_s, (M_cap // 128, N), "gT_s"); _shape(xT, (K, M_cap), "xT"); _shape(xT_s, (M_cap // 128, K), "xT_s")
+    _shape(gT, (n_kb, N, 128), "gT"); _shape(gT_s, (n_kb, N), "gT_s"); _shape(xT, (n_kb, K, 128), "xT")
+    _shape(xT_s, (n_kb, K), "xT_s")
     _numel(offsets, E + 1, "offsets"); _shape(dw, (E, N, K), "dw")
     sd, sfx = _scale_kind(gT_s, xT_s)
     name = "ff8_grouped_gemm_wgrad" + sfx
     _check(getattr(load(), name)(
-        _ptr(gT, _u8, "gT", 2), _ptr(gT_s, sd, "gT_s"), _ptr(xT, _u8, "xT", 2), _ptr(xT_s, sd, "xT_s"),
+        _ptr(gT, _u8, "gT", 3), _ptr(gT_s, sd, "gT_s"), _ptr(xT, _u8, "xT", 3), _ptr(xT_s, sd, "xT_s"),
         _ptr(offsets, _i32, "offsets"), E, M_cap, N, K, _ptr(dw, _f32, "dw", 3), int(bool(accumulate)),
         _stream(stream)), name)
 

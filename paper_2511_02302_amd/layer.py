@@ -59,9 +59,7 @@ class Dims:
     @property
     def m_cap(self):
         """Rows of the grouped buffers: the smallest admissible count, rounded up to a multiple
-        of 2048.  M_cap is also the row stride of the transposed operands, and strides that
-        are only a multiple of 512 bytes (131584 at the DeepSeek-V3 share with 16-row
-        padding) measured 17% slower in the transpose than multiples of 2048."""
+        of 2048."""
         need = ff8.ff8_rows_bound_aligned(self.T, self.k, self.E, self.align)
         return -(-need // 2048) * 2048
 
@@ -102,7 +100,7 @@ class Workspace:
             "dx_perm": ((M, H), _bf16),
         })
         for name, cols in (("x", H), ("h", I), ("dy", H), ("da", 2 * I)):
-            spec[name + "Tq"] = ((cols, M), _u8)
+            spec[name + "Tq"] = ((M // 128, cols, 128), _u8)  # K-blocked transpose
             spec[name + "Ts"] = ((M // 128, cols), sdt)  # block-major column scales
         self.buf = _alloc(spec, self.device)
 

@@ -115,13 +115,16 @@ def test_binding_checks_every_shape():
     bad_calls = [
         lambda: ff8.ff8_quant_rowwise(e(M, K, dtype=bf16), e(M, K), e(M, 1, dtype=f32)),
         lambda: ff8.ff8_quant_block128(e(N, K, dtype=bf16), e(N, K), e(2, 2, dtype=f32)),
-        lambda: ff8.ff8_scaling_aware_transpose(e(M, K), e(M, 2, dtype=f32), e(K, M - 128), e(4, K, dtype=f32)),
+        lambda: ff8.ff8_scaling_aware_transpose(e(M, K), e(M, 2, dtype=f32), e(M // 128 - 1, K, 128), e(4, K, dtype=f32)),
+        lambda: ff8.ff8_scaling_aware_transpose(e(M, K), e(M, 2, dtype=f32), e(K, M), e(4, K, dtype=f32)),  # not K-blocked
         lambda: ff8.ff8_grouped_gemm_fprop(e(M, K), e(M, 2, dtype=f32), e(E, N, K), e(E, 3, 2, dtype=f32),
                                            e(E + 1, dtype=i32), e(M - 128, N, dtype=bf16)),
         lambda: ff8.ff8_grouped_gemm_dgrad(e(M, N), e(M, 3, dtype=f32), e(E, N, K), e(E, 3, 2, dtype=f32),
                                            e(E, dtype=i32), e(M, K, dtype=bf16)),
-        lambda: ff8.ff8_grouped_gemm_wgrad(e(N, M), e(M // 128, N, dtype=f32), e(K, M), e(M // 128, K, dtype=f32),
-                                           e(E + 1, dtype=i32), e(E, K, N, dtype=f32)),
+        lambda: ff8.ff8_grouped_gemm_wgrad(e(M // 128, N, 128), e(M // 128, N, dtype=f32), e(M // 128, K, 128),
+                                           e(M // 128, K, dtype=f32), e(E + 1, dtype=i32), e(E, K, N, dtype=f32)),
+        lambda: ff8.ff8_grouped_gemm_wgrad(e(M // 128, N, 128), e(M // 128, N, dtype=f32), e(M // 128 - 1, K, 128),
+                                           e(M // 128, K, dtype=f32), e(E + 1, dtype=i32), e(E, N, K, dtype=f32)),
         lambda: ff8.ff8_swiglu_quant(e(M, 2 * K, dtype=bf16), e(M, K), e(M, 1, dtype=f32)),
         lambda: ff8.ff8_swiglu_bwd_quant(e(M, 2 * K, dtype=bf16), e(M, K, dtype=bf16), e(M, K), e(M, 4, dtype=f32)),
         lambda: ff8.ff8_unpermute(e(M, K, dtype=bf16), e(128, 2, dtype=i32), e(128, 1, dtype=f32),
@@ -135,8 +138,8 @@ def test_binding_checks_every_shape():
             call()
     # consistent shapes get past the shape checks (and stop at the device check here)
     with pytest.raises(ValueError, match="device tensor"):
-        ff8.ff8_grouped_gemm_wgrad(e(N, M), e(M // 128, N, dtype=f32), e(K, M), e(M // 128, K, dtype=f32),
-                                   e(E + 1, dtype=i32), e(E, N, K, dtype=f32))
+        ff8.ff8_grouped_gemm_wgrad(e(M // 128, N, 128), e(M // 128, N, dtype=f32), e(M // 128, K, 128),
+                                   e(M // 128, K, dtype=f32), e(E + 1, dtype=i32), e(E, N, K, dtype=f32))
 
 
 def test_header_compiles_as_c_and_links(tmp_path):

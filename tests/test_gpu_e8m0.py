@@ -56,8 +56,8 @@ def test_quantizers_and_transpose_e8m0():
     qd = dev(torch.from_numpy(codes))
     for rows_valid in (R, 1024 - 112):  # all rows; a last block cut after 16 of its rows
         off = torch.tensor([0, rows_valid], dtype=torch.int32, device="cuda")
-        qT, sT = poisoned((C, R), torch.uint8), poisoned((R // 128, C), torch.float32)
-        qT8, sT8 = poisoned((C, R), torch.uint8), poisoned((R // 128, C), torch.uint8)
+        qT, sT = poisoned((R // 128, C, 128), torch.uint8), poisoned((R // 128, C), torch.float32)
+        qT8, sT8 = poisoned((R // 128, C, 128), torch.uint8), poisoned((R // 128, C), torch.uint8)
         ff8.ff8_scaling_aware_transpose(qd, sf, qT, sT, off, 1)
         ff8.ff8_scaling_aware_transpose(qd, sb, qT8, sT8, off, 1)
         torch.cuda.synchronize()
@@ -92,8 +92,8 @@ def test_gemms_e8m0_match_f32():
         torch.cuda.synchronize()
         m_pad = int(off[-1])
         assert torch.equal(o[:m_pad].view(torch.int16), o8[:m_pad].view(torch.int16)), fn.__name__
-    gT, gTs = code((N, M_cap)), pow2((M_cap // 128, N), -10, 6)
-    xT, xTs = code((K, M_cap)), pow2((M_cap // 128, K), -10, 6)
+    gT, gTs = code((M_cap // 128, N, 128)), pow2((M_cap // 128, N), -10, 6)  # K-blocked transposes
+    xT, xTs = code((M_cap // 128, K, 128)), pow2((M_cap // 128, K), -10, 6)
     dw, dw8 = poisoned((E, N, K), torch.float32), poisoned((E, N, K), torch.float32)
     ff8.ff8_grouped_gemm_wgrad(gT, gTs, xT, xTs, offd, dw)
     ff8.ff8_grouped_gemm_wgrad(gT, to8(gTs), xT, to8(xTs), offd, dw8)
@@ -129,7 +129,9 @@ def test_layer_step_e8m0_equals_f32(case):
     for n in rows:
         assert torch.equal(b[n][:m_pad].view(torch.uint8), b8[n][:m_pad].view(torch.uint8)), n
     for n in ("xT", "hT", "dyT", "daT"):
-        assert torch.equal(b[n + "q"][:, :m_pad], b8[n + "q"][:, :m_pad]), n
+        kq, kq8 = b[n + "q"], b8[n + "q"]  # K-blocked: rows past m_pad in the last slab are untouched
+        assert torch.equal(kq.permute(1, 0, 2).reshape(kq.shape[1], -1)[:, :m_pad],
+                           kq8.permute(1, 0, 2).reshape(kq8.shape[1], -1)[:, :m_pad]), n
         assert np.array_equal(host(b8[n + "s"][:nb]), _bytes(b[n + "s"][:nb])), n
     for n in ("w1s", "w2s"):
         assert np.array_equal(host(b8[n]), _bytes(b[n])), n

@@ -51,6 +51,14 @@ def run(request):
     torch.cuda.empty_cache()
 
 
+def _kblock_rows(t, idx, lo, hi):
+    """Rows idx (transposed-operand rows: columns of the original) over tokens [lo, hi) of a
+    K-blocked transpose t [M_cap/128, rows, 128], on the host as [len(idx), hi - lo]."""
+    kb0, kb1 = lo // 128, -(-hi // 128)
+    slabs = t[kb0:kb1].index_select(1, _cuda_idx(idx))            # [blocks, len(idx), 128]
+    return host(slabs.permute(1, 0, 2).reshape(len(idx), -1))[:, lo - 128 * kb0:hi - 128 * kb0]
+
+
 def _sample_rows(r, n):
     """n distinct routed rows (padding excluded), sorted, and the expert of each."""
     real = np.nonzero(r["src_row"] >= 0)[0]
@@ -181,9 +189,9 @@ def _wgrad_samples(run, gT, xT, out):
         c = rng.integers(K, size=N_GEMM // 4)
         got = host(b[out][int(e)][_cuda_idx(n), _cuda_idx(c)])
         blk = _cuda_idx(np.arange(lo, hi) // 128)  # each token's 128-row block (groups may share one)
-        g = codec.e4m3_decode(host(b[gT + "q"][_cuda_idx(n), lo:hi])) * \
+        g = codec.e4m3_decode(_kblock_rows(b[gT + "q"], n, lo, hi)) * \
             host(b[gT + "s"].index_select(0, blk)[:, _cuda_idx(n)]).T.astype(np.float64)
-        x = codec.e4m3_decode(host(b[xT + "q"][_cuda_idx(c), lo:hi])) * \
+        x = codec.e4m3_decode(_kblock_rows(b[xT + "q"], c, lo, hi)) * \
             host(b[xT + "s"].index_select(0, blk)[:, _cuda_idx(c)]).T.astype(np.float64)
         _check_gemm_samples(got, np.sum(g * x, axis=1), np.sum(np.abs(g * x), axis=1), False, hi - lo)
     empty = np.nonzero(off[1:] == off[:-1])[0]
@@ -240,9 +248,9 @@ def test_gemm_whole_tiles(run):
         for gT, xT, out in (("dyT", "hT", "dw2"), ("daT", "xT", "dw1")):  # wgrad
             N, K = b[out].shape[1:]
             n, c = _cols(N, first), _cols(K, first)
-            g = codec.e4m3_decode(host(b[gT + "q"][_cuda_idx(n), lo:hi])) * \
+            g = codec.e4m3_decode(_kblock_rows(b[gT + "q"], n, lo, hi)) * \
                 host(b[gT + "s"].index_select(0, blk)[:, _cuda_idx(n)]).T.astype(np.float64)
-            x = codec.e4m3_decode(host(b[xT + "q"][_cuda_idx(c), lo:hi])) * \
+            x = codec.e4m3_decode(_kblock_rows(b[xT + "q"], c, lo, hi)) * \
                 host(b[xT + "s"].index_select(0, blk)[:, _cuda_idx(c)]).T.astype(np.float64)
             got = host(b[out][e].index_select(0, _cuda_idx(n)).index_select(1, _cuda_idx(c)))
             _check_gemm_samples(got.ravel(), (g @ x.T).ravel(), (np.abs(g) @ np.abs(x).T).ravel(), False, hi - lo)
@@ -340,5 +348,5 @@ def test_sat_sampled_blocks(run):
             r1 = min((rb + 1) * 128, m_pad)
             rs = slice(rb * 128, r1)
             wqT, wsT = sat.scaling_aware_transpose(host(q[rs]), host(s[rs]), r1 - rb * 128)
-            assert np.array_equal(host(qT[:, rs]), wqT), (name, rb)
+            assert np.array_equal(host(qT[rb])[:, :r1 - rb * 128], wqT), (name, rb)  # block rb's slab
             assert np.array_equal(host(sT[rb:rb + 1]).T, wsT), (name, rb)

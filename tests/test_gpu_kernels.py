@@ -12,6 +12,7 @@ import torch
 
 import workloads
 from oracle import codec, quant, sat, moe
+from layouts import from_kblock, to_kblock
 from paper_2511_02302_amd import ff8
 
 pytestmark = pytest.mark.gpu
@@ -144,10 +145,10 @@ def _row_scaled_fp8(rows, cols, seed, kmax=12):
 
 
 @pytest.mark.parametrize("rows,cols,n_rows", [(128, 128, 128), (640, 384, 640), (1024, 256, 512), (896, 128, 384),
-                                         (16384, 256, 12800)])  # the last: diagonal order
+                                         (16384, 256, 12800), (384, 256, 272)])  # odd block count; 16-row end
 def test_sat_bit_exact(rows, cols, n_rows):
     q, s = _row_scaled_fp8(rows, cols, seed=rows + cols)
-    qT = poisoned((cols, rows), torch.uint8)
+    qT = poisoned((rows // 128, cols, 128), torch.uint8)  # K-blocked transpose
     sT = poisoned((rows // 128, cols), torch.float32)
     offsets = None
     if n_rows != rows:
@@ -156,9 +157,12 @@ def test_sat_bit_exact(rows, cols, n_rows):
                                     2 if offsets is not None else 0)
     torch.cuda.synchronize()
     wqT, wsT = sat.scaling_aware_transpose(q, s, n_rows)
-    assert np.array_equal(host(qT[:, :n_rows]), wqT)
-    assert np.array_equal(host(sT[: n_rows // 128]).T, wsT)  # block-major on the device
-    assert untouched(qT[:, n_rows:]) and untouched(sT[n_rows // 128:])
+    nb = -(-n_rows // 128)
+    assert np.array_equal(from_kblock(host(qT))[:, :n_rows], wqT)
+    assert np.array_equal(host(sT[:nb]).T, wsT)  # block-major on the device
+    assert untouched(qT[nb:]) and untouched(sT[nb:])
+    if n_rows % 128:  # the rows of the last slab past the active rows stay untouched
+        assert untouched(qT[nb - 1, :, n_rows % 128:].contiguous())
 
 
 def test_sat_extreme_row_range():
@@ -173,12 +177,12 @@ def test_sat_extreme_row_range():
         x[128 + r] *= -(2.0 ** o)
     x = x.to(torch.bfloat16)
     q, s = quant.quant_rowwise(f64(x))
-    qT = poisoned((256, 256), torch.uint8)
+    qT = poisoned((2, 256, 128), torch.uint8)
     sT = poisoned((2, 256), torch.float32)
     ff8.ff8_scaling_aware_transpose(dev(torch.from_numpy(q)), dev(torch.from_numpy(s)), qT, sT)
     torch.cuda.synchronize()
     wqT, wsT = sat.scaling_aware_transpose(q, s)
-    assert np.array_equal(host(qT), wqT)
+    assert np.array_equal(from_kblock(host(qT)), wqT)
     assert np.array_equal(host(sT).T, wsT)
 
 
@@ -188,7 +192,7 @@ def test_sat_full_size_sampled_blocks():
     q = torch.empty((rows, cols), dtype=torch.uint8, device="cuda")
     s = torch.empty((rows, cols // 128), dtype=torch.float32, device="cuda")
     ff8.ff8_quant_rowwise(x, q, s)
-    qT = torch.empty((cols, rows), dtype=torch.uint8, device="cuda")
+    qT = torch.empty((rows // 128, cols, 128), dtype=torch.uint8, device="cuda")
     sT = torch.empty((rows // 128, cols), dtype=torch.float32, device="cuda")
     ff8.ff8_scaling_aware_transpose(q, s, qT, sT)
     torch.cuda.synchronize()
@@ -198,7 +202,7 @@ def test_sat_full_size_sampled_blocks():
         qb = host(q[rb * 128:(rb + 1) * 128, cb * 128:(cb + 1) * 128])
         sb = host(s[rb * 128:(rb + 1) * 128, cb:cb + 1])
         wqT, wsT = sat.scaling_aware_transpose(qb, sb)
-        assert np.array_equal(host(qT[cb * 128:(cb + 1) * 128, rb * 128:(rb + 1) * 128]), wqT)
+        assert np.array_equal(host(qT[rb, cb * 128:(cb + 1) * 128]), wqT)  # the block's slab rows
         assert np.array_equal(host(sT[rb:rb + 1, cb * 128:(cb + 1) * 128]).T, wsT)
 
 

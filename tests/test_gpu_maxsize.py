@@ -16,7 +16,7 @@ from oracle import codec, quant, sat
 from paper_2511_02302_amd import ff8
 
 from test_gpu_kernels import host
-from test_gpu_fullsize import _check_gemm_samples, _dequant_weight
+from test_gpu_fullsize import _check_gemm_samples, _dequant_weight, _kblock_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -98,11 +98,12 @@ def test_dgrad_largest_gradient_operand(gen):
 
 
 def test_wgrad_largest_column_wise_operand(gen):
-    """dW[e, n, c] = sum over expert e's tokens of GT[n, m] XT[c, m]: XT is 7168 x 599040,
-    and the last expert contracts over 594944 tokens (4648 K blocks)."""
-    xT = _rand_e4m3((K_BIG, M_MAX), gen)
+    """dW[e, n, c] = sum over expert e's tokens of GT[n, m] XT[c, m]: XT is 7168 x 599040
+    (K-blocked, [4680, 7168, 128]), and the last expert contracts over 594944 tokens (4648 K
+    blocks)."""
+    xT = _rand_e4m3((M_MAX // 128, K_BIG, 128), gen)
     xT_s = _rand_pow2((M_MAX // 128, K_BIG), -6, 3, gen)
-    gT = _rand_e4m3((N_SMALL, M_MAX), gen)
+    gT = _rand_e4m3((M_MAX // 128, N_SMALL, 128), gen)
     gT_s = _rand_pow2((M_MAX // 128, N_SMALL), -10, -6, gen)
     dw = torch.full((E, N_SMALL, K_BIG), 7.0, dtype=torch.float32, device="cuda")
     print(f"\nwgrad M_cap {M_MAX} N {N_SMALL} K {K_BIG} offsets {OFFSETS}", flush=True)
@@ -116,9 +117,9 @@ def test_wgrad_largest_column_wise_operand(gen):
         ns = np.concatenate([[0, N_SMALL - 1], rng.integers(N_SMALL, size=10)])
         cs = np.concatenate([[0, K_BIG - 1], rng.integers(K_BIG, size=10)])
         for n, c in zip(ns, cs):
-            gv = codec.e4m3_decode(host(gT[int(n), lo:hi])) * \
+            gv = codec.e4m3_decode(_kblock_rows(gT, [int(n)], lo, hi)[0]) * \
                 np.repeat(host(gT_s.index_select(0, scale_rows)[:, int(n)]).astype(np.float64), 128)
-            xv = codec.e4m3_decode(host(xT[int(c), lo:hi])) * \
+            xv = codec.e4m3_decode(_kblock_rows(xT, [int(c)], lo, hi)[0]) * \
                 np.repeat(host(xT_s.index_select(0, scale_rows)[:, int(c)]).astype(np.float64), 128)
             t = gv * xv
             got.append(float(dw[e, int(n), int(c)]))
@@ -134,7 +135,7 @@ def test_sat_largest_operand(gen):
     included."""
     q = _rand_e4m3((M_MAX, K_BIG), gen)
     s = _rand_pow2((M_MAX, K_BIG // 128), -6, 3, gen)
-    qT = torch.empty((K_BIG, M_MAX), dtype=torch.uint8, device="cuda")
+    qT = torch.empty((M_MAX // 128, K_BIG, 128), dtype=torch.uint8, device="cuda")
     sT = torch.empty((M_MAX // 128, K_BIG), dtype=torch.float32, device="cuda")
     print(f"\nSAT rows {M_MAX} cols {K_BIG}", flush=True)
     ff8.ff8_scaling_aware_transpose(q, s, qT, sT)
@@ -146,5 +147,5 @@ def test_sat_largest_operand(gen):
         qb = host(q[rb * 128:(rb + 1) * 128, cb * 128:(cb + 1) * 128])
         sb = host(s[rb * 128:(rb + 1) * 128, cb:cb + 1])
         wqT, wsT = sat.scaling_aware_transpose(qb, sb)
-        assert np.array_equal(host(qT[cb * 128:(cb + 1) * 128, rb * 128:(rb + 1) * 128]), wqT), (rb, cb)
+        assert np.array_equal(host(qT[rb, cb * 128:(cb + 1) * 128]), wqT), (rb, cb)
         assert np.array_equal(host(sT[rb:rb + 1, cb * 128:(cb + 1) * 128]).T, wsT), (rb, cb)

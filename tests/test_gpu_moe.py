@@ -12,6 +12,7 @@ from paper_2511_02302_amd import ff8
 from paper_2511_02302_amd.layer import ExpertLayerFP8
 
 from test_gpu_kernels import dev, host, f64, rel_frob, poisoned, untouched
+from layouts import from_kblock, to_kblock
 
 pytestmark = pytest.mark.gpu
 
@@ -213,16 +214,16 @@ def test_grouped_gemms(case):
     want = moe.grouped_gemm_dgrad(g2q_np, g2s_np, host(w2q), host(w2s), off)
     assert rel_frob(f64(dh[:m_pad]), want) < GEMM_TOL
     # wgrad: dW1[e] = G_e^T X_e from column-wise operands (scaling-aware transposes)
-    gT = torch.empty((2 * I, M_cap), dtype=torch.uint8, device="cuda")
+    gT = torch.empty((M_cap // 128, 2 * I, 128), dtype=torch.uint8, device="cuda")  # K-blocked
     gTs = torch.empty((M_cap // 128, 2 * I), dtype=torch.float32, device="cuda")  # block-major
-    xT = torch.empty((H, M_cap), dtype=torch.uint8, device="cuda")
+    xT = torch.empty((M_cap // 128, H, 128), dtype=torch.uint8, device="cuda")
     xTs = torch.empty((M_cap // 128, H), dtype=torch.float32, device="cuda")
     ff8.ff8_scaling_aware_transpose(gq, gs, gT, gTs, offsets, E)
     ff8.ff8_scaling_aware_transpose(xq, xs, xT, xTs, offsets, E)
     dw = torch.full((E, 2 * I, H), 7.0, dtype=torch.float32, device="cuda")
     ff8.ff8_grouped_gemm_wgrad(gT, gTs, xT, xTs, offsets, dw, accumulate=False)
     torch.cuda.synchronize()
-    want = moe.grouped_gemm_wgrad(host(gT), host(gTs).T, host(xT), host(xTs).T, off)
+    want = moe.grouped_gemm_wgrad(from_kblock(host(gT)), host(gTs).T, from_kblock(host(xT)), host(xTs).T, off)
     assert rel_frob(host(dw), want) < GEMM_TOL
     for e in range(E):
         if off[e + 1] == off[e]:
@@ -498,11 +499,13 @@ def test_layer_stagewise(case, mode):
     assert rel_frob(f64(b["dx"]), dx) < 1e-3
     for name in ("x", "h", "dy", "da"):
         qT, sT = sat.scaling_aware_transpose(host(b[name + "q"][:m_pad]), host(b[name + "s"][:m_pad]))
-        assert np.array_equal(host(b[name + "Tq"][:, :m_pad]), qT), name
+        assert np.array_equal(from_kblock(host(b[name + "Tq"]))[:, :m_pad], qT), name
         assert np.array_equal(host(b[name + "Ts"][: -(-m_pad // 128)]).T, sT), name
-    dW2 = moe.grouped_gemm_wgrad(host(b["dyTq"]), host(b["dyTs"]).T, host(b["hTq"]), host(b["hTs"]).T, off)
+    dW2 = moe.grouped_gemm_wgrad(from_kblock(host(b["dyTq"])), host(b["dyTs"]).T, from_kblock(host(b["hTq"])),
+                                 host(b["hTs"]).T, off)
     assert rel_frob(host(b["dw2"]), dW2) < GEMM_TOL
-    dW1 = moe.grouped_gemm_wgrad(host(b["daTq"]), host(b["daTs"]).T, host(b["xTq"]), host(b["xTs"]).T, off)
+    dW1 = moe.grouped_gemm_wgrad(from_kblock(host(b["daTq"])), host(b["daTs"]).T, from_kblock(host(b["xTq"])),
+                                 host(b["xTs"]).T, off)
     assert rel_frob(host(b["dw1"]), dW1) < GEMM_TOL
 
 
@@ -607,8 +610,9 @@ def test_wgrad_tile_schedules(rows):
     gTs = np.exp2(rng.integers(-8, 0, size=(M_cap // 128, N))).astype(np.float32)
     xTs = np.exp2(rng.integers(-4, 4, size=(M_cap // 128, K))).astype(np.float32)
     dw = torch.full((E, N, K), 7.0, dtype=torch.float32, device="cuda")
-    ff8.ff8_grouped_gemm_wgrad(dev(torch.from_numpy(gT)), dev(torch.from_numpy(gTs)), dev(torch.from_numpy(xT)),
-                               dev(torch.from_numpy(xTs)), dev(torch.from_numpy(off.astype(np.int32))), dw)
+    ff8.ff8_grouped_gemm_wgrad(dev(torch.from_numpy(to_kblock(gT))), dev(torch.from_numpy(gTs)),
+                               dev(torch.from_numpy(to_kblock(xT))), dev(torch.from_numpy(xTs)),
+                               dev(torch.from_numpy(off.astype(np.int32))), dw)
     torch.cuda.synchronize()
     want = moe.grouped_gemm_wgrad(gT, gTs.T, xT, xTs.T, off)
     got = host(dw)
@@ -618,7 +622,7 @@ def test_wgrad_tile_schedules(rows):
         else:
             assert rel_frob(got[e], want[e]) < GEMM_TOL, e
     # accumulating into the same gradient doubles it (experts without rows keep their zeros)
-    args = [dev(torch.from_numpy(a)) for a in (gT, gTs, xT, xTs, off.astype(np.int32))]
+    args = [dev(torch.from_numpy(a)) for a in (to_kblock(gT), gTs, to_kblock(xT), xTs, off.astype(np.int32))]
     ff8.ff8_grouped_gemm_wgrad(*args, dw, accumulate=True)
     torch.cuda.synchronize()
     got = host(dw)
