@@ -3,7 +3,7 @@
 One step = one pass of the whole hot path: 128x128 weight quantization (F0), the
 forward (F1 permute+quant, F2 fc1 fprop, F3 SwiGLU+quant, F4 fc2 fprop, F5 unpermute)
 and the backward (B1 dY permute+quant, B2 fc2 dgrad, B3 SwiGLU backward+quant, B4 fc1
-dgrad, B5 unpermute, B6 four scaling-aware transposes, B7/B8 wgrad), on the
+dgrad, B5 unpermute, B6 four scaling-aware transposes in one launch, B7/B8 wgrad), on the
 DeepSeek-V3 expert layer of one expert-parallel rank: 16384 tokens, hidden 7168,
 32 local experts, top-8 softmax routing, SwiGLU intermediate 2048.  Inputs are
 synthetic (seeded), resident in HBM before timing starts.
@@ -132,8 +132,8 @@ def run_step(L, d, ev=None, ckpt=None, dprobs=None):
         b3,
         lambda: ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"]),
         lambda: ff8.ff8_unpermute(b["dx_perm"], b["row_map"], None, b["dx"]),
-        lambda: [ff8.ff8_scaling_aware_transpose(b[n + "q"], b[n + "s"], b[n + "Tq"], b[n + "Ts"], off, dm.E)
-                 for n in ("x", "h", "dy", "da")],
+        lambda: ff8.ff8_scaling_aware_transpose_batch(*[[b[n + sfx] for n in ("x", "h", "dy", "da")]
+                                                        for sfx in ("q", "s", "Tq", "Ts")], off, dm.E),
         lambda: ff8.ff8_grouped_gemm_wgrad(b["dyTq"], b["dyTs"], b["hTq"], b["hTs"], off, b["dw2"]),
         lambda: ff8.ff8_grouped_gemm_wgrad(b["daTq"], b["daTs"], b["xTq"], b["xTs"], off, b["dw1"]),
     ]

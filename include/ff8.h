@@ -217,6 +217,25 @@ int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows,
                                 const int32_t* offsets, int E, ff8_e4m3* qT, float* sT, void* stream);
 
 /*
+ * ff8_scaling_aware_transpose_batch -- the same transpose (paper section 3.1,
+ * Algorithm 1) of n tensors in one launch: the backward pass turns its four
+ * row-wise operands (X, H, dY, dA of section 3.2's column-wise Wgrad) into their
+ * column-wise forms at once.
+ *   n in [1, 4]; q, s, cols, qT, sT are host arrays of n entries.  Tensor i is
+ *   q[i] [rows, cols[i]] with s[i] [rows, cols[i]/128] and is written to qT[i]
+ *   [rows/128, cols[i], 128], sT[i] [rows/128, cols[i]] exactly as
+ *   ff8_scaling_aware_transpose writes it; rows (a multiple of 128) and offsets
+ *   (NULL or [E+1], only offsets[E] read) are shared by all n.  The result is
+ *   bit-identical to n separate calls.  The host arrays are read during the call
+ *   only.  n outside [1, 4] returns FF8_ERR_ARG; a NULL array or entry
+ *   FF8_ERR_NULL; a rows or cols[i] that is not a positive multiple of 128
+ *   FF8_ERR_SHAPE.
+ */
+int ff8_scaling_aware_transpose_batch(int n, const ff8_e4m3* const* q, const float* const* s, const int64_t* cols,
+                                      int64_t rows, const int32_t* offsets, int E, ff8_e4m3* const* qT,
+                                      float* const* sT, void* stream);
+
+/*
  * ff8_grouped_gemm_fprop -- FP8 grouped GEMM, forward (paper section 3.2: the
  * grouped linear consumes row-wise FP8 activations; "Fprop").
  *   out[m, n] = sum_k D(a)[m, k] * D(w_e)[n, k] for m in expert e's rows,
@@ -326,6 +345,9 @@ int ff8_permute_quant_e8m0(const ff8_bf16* x, const float* row_w, int64_t T, int
                            void* stream);
 int ff8_scaling_aware_transpose_e8m0(const ff8_e4m3* q, const ff8_e8m0* s, int64_t rows, int64_t cols,
                                      const int32_t* offsets, int E, ff8_e4m3* qT, ff8_e8m0* sT, void* stream);
+int ff8_scaling_aware_transpose_batch_e8m0(int n, const ff8_e4m3* const* q, const ff8_e8m0* const* s,
+                                           const int64_t* cols, int64_t rows, const int32_t* offsets, int E,
+                                           ff8_e4m3* const* qT, ff8_e8m0* const* sT, void* stream);
 int ff8_grouped_gemm_fprop_e8m0(const ff8_e4m3* a, const ff8_e8m0* a_s, const ff8_e4m3* w, const ff8_e8m0* w_s,
                                 const int32_t* offsets, int E, int64_t M_cap, int64_t N, int64_t K, ff8_bf16* out,
                                 void* stream);

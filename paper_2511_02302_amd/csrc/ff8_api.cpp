@@ -64,6 +64,20 @@ int device_cu_count() {
 
 }  // namespace ff8
 
+template <typename S>
+static int sat_batch(const char* fn, int n, const ff8_e4m3* const* q, const S* const* s, const int64_t* cols,
+                     int64_t rows, const int32_t* offsets, int E, ff8_e4m3* const* qT, S* const* sT, void* stream) {
+  if (n < 1 || n > ff8::kSatMaxJobs) return fail(FF8_ERR_ARG, "%s: n must be in [1, %d]", fn, ff8::kSatMaxJobs);
+  if (!q || !s || !cols || !qT || !sT) return fail(FF8_ERR_NULL, "%s: a required array is NULL", fn);
+  for (int i = 0; i < n; ++i) {
+    if (!q[i] || !s[i] || !qT[i] || !sT[i]) return fail(FF8_ERR_NULL, "%s: a pointer of tensor %d is NULL", fn, i);
+    if (!mult128(cols[i])) return fail(FF8_ERR_SHAPE, "%s: cols[%d] must be a positive multiple of 128", fn, i);
+  }
+  if (!mult128(rows)) return fail(FF8_ERR_SHAPE, "%s: rows must be a positive multiple of 128", fn);
+  if (offsets && E < 1) return fail(FF8_ERR_ARG, "%s: E must be >= 1 with offsets", fn);
+  return hip_status(ff8::launch_sat_batch(n, q, s, cols, rows, offsets, E, qT, sT, as_stream(stream)), fn);
+}
+
 extern "C" {
 
 int ff8_version(void) { return 100; }
@@ -215,6 +229,18 @@ int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows,
   REQUIRE_SHAPE(mult128(rows) && mult128(cols));
   if (offsets) REQUIRE_ARG(E >= 1);
   return hip_status(ff8::launch_sat(q, s, rows, cols, offsets, E, qT, sT, as_stream(stream)), __func__);
+}
+
+int ff8_scaling_aware_transpose_batch(int n, const ff8_e4m3* const* q, const float* const* s, const int64_t* cols,
+                                      int64_t rows, const int32_t* offsets, int E, ff8_e4m3* const* qT,
+                                      float* const* sT, void* stream) {
+  return sat_batch(__func__, n, q, s, cols, rows, offsets, E, qT, sT, stream);
+}
+
+int ff8_scaling_aware_transpose_batch_e8m0(int n, const ff8_e4m3* const* q, const ff8_e8m0* const* s,
+                                           const int64_t* cols, int64_t rows, const int32_t* offsets, int E,
+                                           ff8_e4m3* const* qT, ff8_e8m0* const* sT, void* stream) {
+  return sat_batch(__func__, n, q, s, cols, rows, offsets, E, qT, sT, stream);
 }
 
 static int gemm_common(const char* fn, const void* a, const void* as, const void* b, const void* bs,

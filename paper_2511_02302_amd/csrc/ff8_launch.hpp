@@ -31,6 +31,12 @@ hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t co
                       uint8_t* qT, float* sT, hipStream_t st);
 hipError_t launch_sat(const uint8_t* q, const e8m0_t* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
                       uint8_t* qT, e8m0_t* sT, hipStream_t st);
+// Up to kSatMaxJobs tensors with the same rows (and active rows) in one launch.
+constexpr int kSatMaxJobs = 4;
+hipError_t launch_sat_batch(int n, const uint8_t* const* q, const float* const* s, const int64_t* cols, int64_t rows,
+                            const int32_t* offsets, int E, uint8_t* const* qT, float* const* sT, hipStream_t st);
+hipError_t launch_sat_batch(int n, const uint8_t* const* q, const e8m0_t* const* s, const int64_t* cols, int64_t rows,
+                            const int32_t* offsets, int E, uint8_t* const* qT, e8m0_t* const* sT, hipStream_t st);
 
 constexpr int kRouteChunk = 256;  // tokens per routing chunk: the workspace holds ceil(T / 256) x E counts
 size_t permute_workspace_bytes(int64_t T, int k, int E);

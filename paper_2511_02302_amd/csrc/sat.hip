@@ -28,6 +28,10 @@
 // K-blocked output is 3-7% faster at the layer's 135168 rows and 37% faster on 32768 x 7168.
 // Groups padded to 16 rows can end inside a block: the last block's S_max covers only the
 // rows below m_rows (offsets[E]), and only those rows of its slab are written.
+// One launch can transpose up to four tensors with the same rows (the backward pass's four
+// weight-gradient operands): tensor t owns the logical workgroups [first[t], first[t + 1]), so
+// the tail of one tensor's grid overlaps the head of the next instead of draining the chip
+// between launches.
 
 #include "ff8_device.hpp"
 #include "ff8_launch.hpp"
@@ -102,18 +106,40 @@ __device__ __forceinline__ void shift_transpose_store(uint32_t (&w0)[8], uint32_
 // b*16 + (k ^ ((o >> 3) & 15)).  Rows of the input are 8-byte units of the output; the swizzle
 // keeps the sub-block writes and the row reads conflict-free.
 constexpr int RB = 2;  // 128x128 blocks per workgroup
+
+// The tensors of one launch; all have `rows` rows and the same active rows.
 template <typename S>
-__global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict__ q, const S* __restrict__ s,
-                                                       int64_t rows, int64_t cols, const int32_t* __restrict__ offsets,
-                                                       int E, uint8_t* __restrict__ qT, S* __restrict__ sT) {
+struct SatJobs {
+  const uint8_t* q[kSatMaxJobs];
+  const S* s[kSatMaxJobs];
+  uint8_t* qT[kSatMaxJobs];
+  S* sT[kSatMaxJobs];
+  int64_t cols[kSatMaxJobs];
+  int first[kSatMaxJobs + 1];  // first logical workgroup of each tensor; first[n] = the grid
+  int n;
+};
+
+template <typename S>
+__global__ __launch_bounds__(kThreads) void sat_kernel(const SatJobs<S> jobs, int64_t rows,
+                                                       const int32_t* __restrict__ offsets, int E) {
   __shared__ u32x2 tile[128 * RB * 16];
   __shared__ int t_rows[RB][128];
   __shared__ uint32_t wmax[RB][2];
 
-  const int n_cb = (int)(cols / kTile), n_cp = (n_cb + 1) / 2;
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t rb = logical / n_cp;                   // the 128-row block
-  const int cb0 = 2 * (logical - (int)rb * n_cp);      // its first column tile
+  int t = 0;  // the tensor of this workgroup (uniform)
+#pragma unroll
+  for (int i = 1; i < kSatMaxJobs; ++i)
+    if (i < jobs.n && logical >= jobs.first[i]) t = i;
+  const uint8_t* __restrict__ q = jobs.q[t];
+  const S* __restrict__ s = jobs.s[t];
+  uint8_t* __restrict__ qT = jobs.qT[t];
+  S* __restrict__ sT = jobs.sT[t];
+  const int64_t cols = jobs.cols[t];
+  const int local = logical - jobs.first[t];
+  const int n_cb = (int)(cols / kTile), n_cp = (n_cb + 1) / 2;
+  const int64_t rb = local / n_cp;                     // the 128-row block
+  const int cb0 = 2 * (local - (int)rb * n_cp);        // its first column tile
   const int64_t m_rows = active_rows(offsets, E, rows);
   if (rb * kTile >= m_rows) return;                    // uniform: a block past the active rows
   const int n_valid = cb0 + 1 < n_cb ? 2 : 1;          // column tiles of this pair (uniform)
@@ -187,21 +213,42 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const uint8_t* __restrict
 }  // namespace
 
 template <typename S>
-static hipError_t sat_impl(const uint8_t* q, const S* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
-                           uint8_t* qT, S* sT, hipStream_t st) {
+static hipError_t sat_impl(int n, const uint8_t* const* q, const S* const* s, const int64_t* cols, int64_t rows,
+                           const int32_t* offsets, int E, uint8_t* const* qT, S* const* sT, hipStream_t st) {
+  SatJobs<S> jobs{};
   const int64_t n_rb = rows / kTile;
-  const int64_t n_cb = cols / kTile;
-  sat_kernel<S><<<(unsigned)(n_rb * ((n_cb + 1) / 2)), kThreads, 0, st>>>(q, s, rows, cols, offsets, E, qT, sT);
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    jobs.q[i] = q[i];
+    jobs.s[i] = s[i];
+    jobs.qT[i] = qT[i];
+    jobs.sT[i] = sT[i];
+    jobs.cols[i] = cols[i];
+    jobs.first[i] = (int)total;
+    total += n_rb * ((cols[i] / kTile + 1) / 2);
+    if (total >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  }
+  jobs.first[n] = (int)total;
+  jobs.n = n;
+  sat_kernel<S><<<(unsigned)total, kThreads, 0, st>>>(jobs, rows, offsets, E);
   return hipGetLastError();
 }
 
 hipError_t launch_sat(const uint8_t* q, const float* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
                       uint8_t* qT, float* sT, hipStream_t st) {
-  return sat_impl(q, s, rows, cols, offsets, E, qT, sT, st);
+  return sat_impl(1, &q, &s, &cols, rows, offsets, E, &qT, &sT, st);
 }
 hipError_t launch_sat(const uint8_t* q, const e8m0_t* s, int64_t rows, int64_t cols, const int32_t* offsets, int E,
                       uint8_t* qT, e8m0_t* sT, hipStream_t st) {
-  return sat_impl(q, s, rows, cols, offsets, E, qT, sT, st);
+  return sat_impl(1, &q, &s, &cols, rows, offsets, E, &qT, &sT, st);
+}
+hipError_t launch_sat_batch(int n, const uint8_t* const* q, const float* const* s, const int64_t* cols, int64_t rows,
+                            const int32_t* offsets, int E, uint8_t* const* qT, float* const* sT, hipStream_t st) {
+  return sat_impl(n, q, s, cols, rows, offsets, E, qT, sT, st);
+}
+hipError_t launch_sat_batch(int n, const uint8_t* const* q, const e8m0_t* const* s, const int64_t* cols, int64_t rows,
+                            const int32_t* offsets, int E, uint8_t* const* qT, e8m0_t* const* sT, hipStream_t st) {
+  return sat_impl(n, q, s, cols, rows, offsets, E, qT, sT, st);
 }
 
 }  // namespace ff8

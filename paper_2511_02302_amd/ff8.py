@@ -38,6 +38,8 @@ _SIGNATURES = {
     "ff8_permute_quant_noalloc": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp,
                                            _c_vp, _c_vp, _c_i64, _c_vp, _c_vp, _c_int, _c_vp]),
     "ff8_scaling_aware_transpose": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
+    "ff8_scaling_aware_transpose_batch": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_vp, _c_int, _c_vp, _c_vp,
+                                                   _c_vp]),
     "ff8_grouped_gemm_fprop": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
                                         _c_vp]),
     "ff8_grouped_gemm_dgrad": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64, _c_vp,
@@ -58,6 +60,8 @@ _SIGNATURES = {
     "ff8_permute_quant_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp, _c_vp,
                                         _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_int, _c_vp]),
     "ff8_scaling_aware_transpose_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
+    "ff8_scaling_aware_transpose_batch_e8m0": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_vp, _c_int, _c_vp,
+                                                        _c_vp, _c_vp]),
     "ff8_grouped_gemm_fprop_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64,
                                              _c_vp, _c_vp]),
     "ff8_grouped_gemm_dgrad_e8m0": (_c_int, [_c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_i64, _c_i64, _c_i64,
@@ -254,6 +258,35 @@ def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):
     _check(getattr(load(), name)(
         _ptr(q, _u8, "q", 2), _ptr(s, sd, "s", 2), rows, cols, _ptr(offsets, _i32, "offsets"), E,
         _ptr(qT, _u8, "qT", 3), _ptr(sT, sd, "sT", 2), _stream(stream)), name)
+
+
+def ff8_scaling_aware_transpose_batch(qs, ss, qTs, sTs, offsets=None, E=0, stream=None):
+    """Transposes of up to four tensors with the same rows in one launch; each tensor's
+    arguments are those of ff8_scaling_aware_transpose."""
+    n = len(qs)
+    if not (len(ss) == len(qTs) == len(sTs) == n):
+        raise ValueError("qs, ss, qTs and sTs must have the same length")
+    if n == 0:
+        raise ValueError("at least one tensor is required")
+    rows = qs[0].shape[0]
+    for i in range(n):
+        r, cols = qs[i].shape
+        if r != rows:
+            raise ValueError(f"qs[{i}] must have shape ({rows}, cols): every tensor has the same rows")
+        _shape(ss[i], (rows, cols // 128), f"ss[{i}]"); _shape(qTs[i], (rows // 128, cols, 128), f"qTs[{i}]")
+        _shape(sTs[i], (rows // 128, cols), f"sTs[{i}]")
+    sd, sfx = _scale_kind(*ss, *sTs)
+    if offsets is not None:
+        _numel(offsets, E + 1, "offsets")
+    arr = lambda vals: (ctypes.c_void_p * n)(*[v.value for v in vals])
+    q_a = arr([_ptr(q, _u8, f"qs[{i}]", 2) for i, q in enumerate(qs)])
+    s_a = arr([_ptr(x, sd, f"ss[{i}]", 2) for i, x in enumerate(ss)])
+    qT_a = arr([_ptr(x, _u8, f"qTs[{i}]", 3) for i, x in enumerate(qTs)])
+    sT_a = arr([_ptr(x, sd, f"sTs[{i}]", 2) for i, x in enumerate(sTs)])
+    cols_a = (ctypes.c_int64 * n)(*[q.shape[1] for q in qs])
+    name = "ff8_scaling_aware_transpose_batch" + sfx
+    _check(getattr(load(), name)(n, q_a, s_a, cols_a, rows, _ptr(offsets, _i32, "offsets"), E, qT_a, sT_a,
+                                 _stream(stream)), name)
 
 
 def ff8_grouped_gemm_fprop(a, a_s, w, w_s, offsets, out, stream=None):

@@ -223,8 +223,9 @@ class ExpertLayerFP8:
             ff8.ff8_swiglu_bwd_quant(b["a"], b["dh"], b["daq"], b["das"], off, d.E)
         ff8.ff8_grouped_gemm_dgrad(b["daq"], b["das"], b["w1q"], b["w1s"], off, b["dx_perm"])
         ff8.ff8_unpermute(b["dx_perm"], b["row_map"], None, b["dx"])
-        for name in ("x", "h", "dy", "da"):
-            ff8.ff8_scaling_aware_transpose(b[name + "q"], b[name + "s"], b[name + "Tq"], b[name + "Ts"], off, d.E)
+        names = ("x", "h", "dy", "da")  # one launch for the four column-wise Wgrad operands
+        ff8.ff8_scaling_aware_transpose_batch([b[n + "q"] for n in names], [b[n + "s"] for n in names],
+                                              [b[n + "Tq"] for n in names], [b[n + "Ts"] for n in names], off, d.E)
         ff8.ff8_grouped_gemm_wgrad(b["dyTq"], b["dyTs"], b["hTq"], b["hTs"], off, b["dw2"])
         ff8.ff8_grouped_gemm_wgrad(b["daTq"], b["daTs"], b["xTq"], b["xTs"], off, b["dw1"])
         if release:

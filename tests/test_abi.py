@@ -95,6 +95,22 @@ def test_validation_errors_without_gpu(lib):
     assert b"1048576 bytes" in lib.ff8_last_error()
     assert lib.ff8_permute_quant_noalloc(fake, None, 16, 128, 2, 4, fake, 0, fake, fake, fake, 640, fake, fake,
                                          24, None) == 3  # align
+    # the batched transpose: n in [1, 4], every array and entry present, every extent a multiple of 128
+    arr = lambda *v: (ctypes.c_void_p * len(v))(*v)
+    cols = lambda *c: (ctypes.c_int64 * len(c))(*c)
+    f5 = [0x1000] * 5
+    sat_b = lib.ff8_scaling_aware_transpose_batch
+    assert sat_b(0, arr(0x1000), arr(0x1000), cols(128), 128, None, 0, arr(0x1000), arr(0x1000), None) == 3
+    assert sat_b(5, arr(*f5), arr(*f5), cols(*[128] * 5), 128, None, 0, arr(*f5), arr(*f5), None) == 3
+    assert sat_b(1, None, arr(0x1000), cols(128), 128, None, 0, arr(0x1000), arr(0x1000), None) == 1
+    assert sat_b(2, arr(0x1000, None), arr(0x1000, 0x1000), cols(128, 128), 128, None, 0, arr(0x1000, 0x1000),
+                 arr(0x1000, 0x1000), None) == 1
+    assert b"tensor 1" in lib.ff8_last_error()
+    assert sat_b(2, arr(0x1000, 0x1000), arr(0x1000, 0x1000), cols(128, 200), 128, None, 0, arr(0x1000, 0x1000),
+                 arr(0x1000, 0x1000), None) == 2
+    assert lib.ff8_scaling_aware_transpose_batch_e8m0(1, arr(0x1000), arr(0x1000), cols(128), 100, None, 0,
+                                                      arr(0x1000), arr(0x1000), None) == 2
+    assert sat_b(1, arr(0x1000), arr(0x1000), cols(128), 128, fake, 0, arr(0x1000), arr(0x1000), None) == 3
     assert lib.ff8_swiglu_quant(fake, None, 0, 128, 100, fake, fake, None) == 2
     assert lib.ff8_baseline_copy(fake, fake, 17, None) == 2
     # operands of 4 GiB and more: the kernels address each operand with 32-bit byte offsets
@@ -117,6 +133,12 @@ def test_binding_checks_every_shape():
         lambda: ff8.ff8_quant_block128(e(N, K, dtype=bf16), e(N, K), e(2, 2, dtype=f32)),
         lambda: ff8.ff8_scaling_aware_transpose(e(M, K), e(M, 2, dtype=f32), e(M // 128 - 1, K, 128), e(4, K, dtype=f32)),
         lambda: ff8.ff8_scaling_aware_transpose(e(M, K), e(M, 2, dtype=f32), e(K, M), e(4, K, dtype=f32)),  # not K-blocked
+        lambda: ff8.ff8_scaling_aware_transpose_batch([e(M, K), e(M, N)], [e(M, 2, dtype=f32), e(M, 3, dtype=f32)],
+                                                      [e(M // 128, K, 128), e(M // 128, N, 128)],
+                                                      [e(M // 128, K, dtype=f32), e(M // 128, K, dtype=f32)]),
+        lambda: ff8.ff8_scaling_aware_transpose_batch([e(M, K), e(M - 128, N)], [e(M, 2, dtype=f32), e(M, 3, dtype=f32)],
+                                                      [e(M // 128, K, 128), e(M // 128, N, 128)],
+                                                      [e(M // 128, K, dtype=f32), e(M // 128, N, dtype=f32)]),
         lambda: ff8.ff8_grouped_gemm_fprop(e(M, K), e(M, 2, dtype=f32), e(E, N, K), e(E, 3, 2, dtype=f32),
                                            e(E + 1, dtype=i32), e(M - 128, N, dtype=bf16)),
         lambda: ff8.ff8_grouped_gemm_dgrad(e(M, N), e(M, 3, dtype=f32), e(E, N, K), e(E, 3, 2, dtype=f32),

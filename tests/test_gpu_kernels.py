@@ -165,6 +165,34 @@ def test_sat_bit_exact(rows, cols, n_rows):
         assert untouched(qT[nb - 1, :, n_rows % 128:].contiguous())
 
 
+@pytest.mark.parametrize("fmt", ["f32", "e8m0"])
+@pytest.mark.parametrize("n_rows", [1024, 912])  # all rows; a last block cut after 16 of its rows
+def test_sat_batch_bit_exact(fmt, n_rows):
+    """One launch over four tensors of one row count (7, 1, 5 and 2 column tiles: odd and even
+    tile counts, a single tile) writes, for each, the oracle's transpose and block scales, and
+    nothing past the active rows."""
+    rows, cols_list = 1024, [896, 128, 640, 256]
+    qs, ss, want, qTs, sTs = [], [], [], [], []
+    for i, cols in enumerate(cols_list):
+        q, s = _row_scaled_fp8(rows, cols, seed=40 + i, kmax=20 + 10 * i)
+        want.append(sat.scaling_aware_transpose(q, s, n_rows))
+        qs.append(dev(torch.from_numpy(q)))
+        ss.append(dev(torch.from_numpy(s if fmt == "f32" else quant.scale_to_e8m0(s))))
+        qTs.append(poisoned((rows // 128, cols, 128), torch.uint8))
+        sTs.append(poisoned((rows // 128, cols), torch.float32 if fmt == "f32" else torch.uint8))
+    offsets = dev(torch.tensor([0, 400, n_rows], dtype=torch.int32))
+    ff8.ff8_scaling_aware_transpose_batch(qs, ss, qTs, sTs, offsets, 2)
+    torch.cuda.synchronize()
+    nb = -(-n_rows // 128)
+    for i, (wqT, wsT) in enumerate(want):
+        assert np.array_equal(from_kblock(host(qTs[i]))[:, :n_rows], wqT), i
+        ws = wsT.T if fmt == "f32" else quant.scale_to_e8m0(wsT.T)
+        assert np.array_equal(host(sTs[i][:nb]), ws), i
+        assert untouched(qTs[i][nb:]) and untouched(sTs[i][nb:]), i
+        if n_rows % 128:
+            assert untouched(qTs[i][nb - 1, :, n_rows % 128:].contiguous()), i
+
+
 def test_sat_extreme_row_range():
     """Rows of one block whose scales differ by up to 2^139: shifts of 18, 19 and >= 128
     (underflow to the nearest subnormal, to signed zero, and far beyond the float range of
