@@ -165,32 +165,34 @@ def test_sat_bit_exact(rows, cols, n_rows):
         assert untouched(qT[nb - 1, :, n_rows % 128:].contiguous())
 
 
-@pytest.mark.parametrize("fmt", ["f32", "e8m0"])
-@pytest.mark.parametrize("n_rows", [1024, 912])  # all rows; a last block cut after 16 of its rows
-def test_sat_batch_bit_exact(fmt, n_rows):
-    """One launch over four tensors of one row count (7, 1, 5 and 2 column tiles: odd and even
-    tile counts, a single tile) writes, for each, the oracle's transpose and block scales, and
-    nothing past the active rows."""
-    rows, cols_list = 1024, [896, 128, 640, 256]
+@pytest.mark.parametrize("fmt,n_rows,n", [("f32", 1024, 4), ("f32", 912, 4), ("e8m0", 1024, 4), ("e8m0", 912, 4),
+                                          ("f32", 912, 1), ("f32", 912, 3), ("f32", None, 2)])
+def test_sat_batch_bit_exact(fmt, n_rows, n):
+    """One launch over up to four tensors of one row count (7, 1, 5 and 2 column tiles: odd and
+    even tile counts, a single tile) writes, for each, the oracle's transpose and block scales,
+    and nothing past the active rows (912: a last block cut after 16 of its rows; None: no
+    offsets, every row)."""
+    rows, cols_list = 1024, [896, 128, 640, 256][:n]
     qs, ss, want, qTs, sTs = [], [], [], [], []
+    n_active = rows if n_rows is None else n_rows
     for i, cols in enumerate(cols_list):
         q, s = _row_scaled_fp8(rows, cols, seed=40 + i, kmax=20 + 10 * i)
-        want.append(sat.scaling_aware_transpose(q, s, n_rows))
+        want.append(sat.scaling_aware_transpose(q, s, n_active))
         qs.append(dev(torch.from_numpy(q)))
         ss.append(dev(torch.from_numpy(s if fmt == "f32" else quant.scale_to_e8m0(s))))
         qTs.append(poisoned((rows // 128, cols, 128), torch.uint8))
         sTs.append(poisoned((rows // 128, cols), torch.float32 if fmt == "f32" else torch.uint8))
-    offsets = dev(torch.tensor([0, 400, n_rows], dtype=torch.int32))
-    ff8.ff8_scaling_aware_transpose_batch(qs, ss, qTs, sTs, offsets, 2)
+    offsets = None if n_rows is None else dev(torch.tensor([0, 400, n_rows], dtype=torch.int32))
+    ff8.ff8_scaling_aware_transpose_batch(qs, ss, qTs, sTs, offsets, 0 if offsets is None else 2)
     torch.cuda.synchronize()
-    nb = -(-n_rows // 128)
+    nb = -(-n_active // 128)
     for i, (wqT, wsT) in enumerate(want):
-        assert np.array_equal(from_kblock(host(qTs[i]))[:, :n_rows], wqT), i
+        assert np.array_equal(from_kblock(host(qTs[i]))[:, :n_active], wqT), i
         ws = wsT.T if fmt == "f32" else quant.scale_to_e8m0(wsT.T)
         assert np.array_equal(host(sTs[i][:nb]), ws), i
         assert untouched(qTs[i][nb:]) and untouched(sTs[i][nb:]), i
-        if n_rows % 128:
-            assert untouched(qTs[i][nb - 1, :, n_rows % 128:].contiguous()), i
+        if n_active % 128:
+            assert untouched(qTs[i][nb - 1, :, n_active % 128:].contiguous()), i
 
 
 def test_sat_extreme_row_range():
