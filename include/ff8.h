@@ -343,6 +343,10 @@ int ff8_permute_quant_e8m0(const ff8_bf16* x, const float* row_w, int64_t T, int
                            const int32_t* topk_idx, int reuse_map, int32_t* row_map, int32_t* offsets, int32_t* src_row,
                            int64_t M_cap, ff8_e4m3* q, ff8_e8m0* s, void* workspace, size_t ws_bytes, int align,
                            void* stream);
+int ff8_permute_quant_dprobs_e8m0(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                  const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                  int64_t M_cap, ff8_e4m3* q, ff8_e8m0* s, const ff8_bf16* y_perm, float* dprobs,
+                                  void* stream);
 int ff8_scaling_aware_transpose_e8m0(const ff8_e4m3* q, const ff8_e8m0* s, int64_t rows, int64_t cols,
                                      const int32_t* offsets, int E, ff8_e4m3* qT, ff8_e8m0* sT, void* stream);
 int ff8_scaling_aware_transpose_batch_e8m0(int n, const ff8_e4m3* const* q, const ff8_e8m0* const* s,

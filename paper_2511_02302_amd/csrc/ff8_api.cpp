@@ -78,6 +78,28 @@ static int sat_batch(const char* fn, int n, const ff8_e4m3* const* q, const S* c
   return hip_status(ff8::launch_sat_batch(n, q, s, cols, rows, offsets, E, qT, sT, as_stream(stream)), fn);
 }
 
+template <typename S>
+static int permute_quant_dprobs_common(const char* fn, const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H,
+                                       int k, int E, const int32_t* row_map, const int32_t* offsets,
+                                       const int32_t* src_row, int64_t M_cap, ff8_e4m3* q, S* s,
+                                       const ff8_bf16* y_perm, float* dprobs, void* stream) {
+  if (!(k >= 1 && E >= 1 && k <= E && E <= 1024 && k <= ff8::max_k_dprobs()))
+    return fail(FF8_ERR_ARG, "%s: need 1 <= k <= E <= 1024 and k <= %d", fn, ff8::max_k_dprobs());
+  if (!(T >= 0 && mult128(H) && H <= ff8::max_h_dprobs() && M_cap % 128 == 0))
+    return fail(FF8_ERR_SHAPE, "%s: H must be a multiple of 128 up to %lld and M_cap a multiple of 128", fn,
+                (long long)ff8::max_h_dprobs());
+  if (M_cap < ff8_rows_bound_aligned(T, k, E, 16))  // the map may come from any alignment
+    return fail(FF8_ERR_SHAPE, "%s: M_cap is below the row bound", fn);
+  if (!(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31))
+    return fail(FF8_ERR_SHAPE, "%s: T*k and M_cap must be below 2^31", fn);
+  if (T > 0 && (!dy || !row_w || !y_perm || !dprobs || !row_map))  // an empty batch may pass NULL for these
+    return fail(FF8_ERR_NULL, "%s: dy, row_w, y_perm, dprobs or row_map is NULL", fn);
+  if (!offsets || !src_row || !q || !s) return fail(FF8_ERR_NULL, "%s: offsets, src_row, q or s is NULL", fn);
+  return hip_status(ff8::launch_permute_quant_dprobs(dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s,
+                                                     y_perm, dprobs, as_stream(stream)),
+                    fn);
+}
+
 extern "C" {
 
 int ff8_version(void) { return 100; }
@@ -210,17 +232,16 @@ int ff8_permute_quant_noalloc(const ff8_bf16* x, const float* row_w, int64_t T, 
 int ff8_permute_quant_dprobs(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
                              const int32_t* row_map, const int32_t* offsets, const int32_t* src_row, int64_t M_cap,
                              ff8_e4m3* q, float* s, const ff8_bf16* y_perm, float* dprobs, void* stream) {
-  REQUIRE_ARG(k >= 1 && E >= 1 && k <= E && E <= 1024 && k <= ff8::max_k_dprobs());
-  REQUIRE_SHAPE(T >= 0 && mult128(H) && H <= ff8::max_h_dprobs() && M_cap % 128 == 0);
-  REQUIRE_SHAPE(M_cap >= ff8_rows_bound_aligned(T, k, E, 16));  // the map may come from any alignment
-  REQUIRE_SHAPE(T * (int64_t)k < (int64_t)1 << 31 && M_cap < (int64_t)1 << 31);
-  if (T > 0) {  // an empty batch may pass NULL for its empty token-indexed arrays
-    REQUIRE_PTR(dy); REQUIRE_PTR(row_w); REQUIRE_PTR(y_perm); REQUIRE_PTR(dprobs); REQUIRE_PTR(row_map);
-  }
-  REQUIRE_PTR(offsets); REQUIRE_PTR(src_row); REQUIRE_PTR(q); REQUIRE_PTR(s);
-  return hip_status(ff8::launch_permute_quant_dprobs(dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s,
-                                                     y_perm, dprobs, as_stream(stream)),
-                    __func__);
+  return permute_quant_dprobs_common(__func__, dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, y_perm,
+                                     dprobs, stream);
+}
+
+int ff8_permute_quant_dprobs_e8m0(const ff8_bf16* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                  const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                  int64_t M_cap, ff8_e4m3* q, ff8_e8m0* s, const ff8_bf16* y_perm, float* dprobs,
+                                  void* stream) {
+  return permute_quant_dprobs_common(__func__, dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, y_perm,
+                                     dprobs, stream);
 }
 
 int ff8_scaling_aware_transpose(const ff8_e4m3* q, const float* s, int64_t rows, int64_t cols,

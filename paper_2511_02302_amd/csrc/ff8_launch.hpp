@@ -57,6 +57,10 @@ hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, i
                                        const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                        int64_t M_cap, uint8_t* q, float* s, const uint16_t* y_perm, float* dprobs,
                                        hipStream_t st);
+hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                       const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                       int64_t M_cap, uint8_t* q, e8m0_t* s, const uint16_t* y_perm, float* dprobs,
+                                       hipStream_t st);
 int max_k_dprobs();
 int64_t max_h_dprobs();
 hipError_t launch_unpermute(const uint16_t* y_perm, const int32_t* row_map, const float* row_w, int64_t T, int k,

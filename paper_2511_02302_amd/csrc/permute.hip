@@ -243,15 +243,16 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_kernel(const uin
 // (Loading 2, 4 or 8 slots' Y_perm rows ahead of their dot products measured no faster: the
 // registers it takes cost occupancy.)
 constexpr int kMaxKDprobs = 64;
+template <typename S>
 __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_dprobs_kernel(
     const uint16_t* __restrict__ dy, const float* __restrict__ row_w, int64_t H, int k,
-    const int32_t* __restrict__ row_map, int64_t M_cap, uint8_t* __restrict__ q, float* __restrict__ s,
+    const int32_t* __restrict__ row_map, int64_t M_cap, uint8_t* __restrict__ q, S* __restrict__ s,
     const uint16_t* __restrict__ y_perm, float* __restrict__ dprobs, int64_t T, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ src_row) {
   __shared__ float part[kMaxKDprobs * (kRowThreadsMax / 64)];
   const int64_t t = blockIdx.x;
   if (t >= T) {  // padding rows of group t - T (the whole workgroup leaves before any barrier)
-    pad_group<float>((int)(t - T), offsets, src_row, H, q, s);
+    pad_group<S>((int)(t - T), offsets, src_row, H, q, s);
     return;
   }
   const int64_t n16 = H / 16, sh = H / kTile;
@@ -284,7 +285,7 @@ __global__ __launch_bounds__(kRowThreadsMax) void permute_quant_dprobs_kernel(
       int tq;
       const u32x4 r = quant16_tile8(vw, tq);
       stnt16(q + (int64_t)row * H + c * 16, r);
-      if (leader) s[(int64_t)row * sh + (c >> 3)] = exp2i(tq);
+      if (leader) put_scale(&s[(int64_t)row * sh + (c >> 3)], tq);
     }
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) acc += __shfl_xor(acc, d);
@@ -430,13 +431,26 @@ hipError_t launch_permute_quant(const uint16_t* x, const float* row_w, int64_t T
   return permute_quant_impl(x, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, st);
 }
 
+template <typename S>
+static hipError_t permute_quant_dprobs_impl(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k,
+                                            int E, const int32_t* row_map, const int32_t* offsets,
+                                            const int32_t* src_row, int64_t M_cap, uint8_t* q, S* s,
+                                            const uint16_t* y_perm, float* dprobs, hipStream_t st) {
+  permute_quant_dprobs_kernel<S><<<(unsigned)(T + E), row_threads(H), 0, st>>>(dy, row_w, H, k, row_map, M_cap, q, s,
+                                                                                y_perm, dprobs, T, offsets, src_row);
+  return hipGetLastError();
+}
 hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
                                        const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
                                        int64_t M_cap, uint8_t* q, float* s, const uint16_t* y_perm, float* dprobs,
                                        hipStream_t st) {
-  permute_quant_dprobs_kernel<<<(unsigned)(T + E), row_threads(H), 0, st>>>(dy, row_w, H, k, row_map, M_cap, q, s,
-                                                                             y_perm, dprobs, T, offsets, src_row);
-  return hipGetLastError();
+  return permute_quant_dprobs_impl(dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, y_perm, dprobs, st);
+}
+hipError_t launch_permute_quant_dprobs(const uint16_t* dy, const float* row_w, int64_t T, int64_t H, int k, int E,
+                                       const int32_t* row_map, const int32_t* offsets, const int32_t* src_row,
+                                       int64_t M_cap, uint8_t* q, e8m0_t* s, const uint16_t* y_perm, float* dprobs,
+                                       hipStream_t st) {
+  return permute_quant_dprobs_impl(dy, row_w, T, H, k, E, row_map, offsets, src_row, M_cap, q, s, y_perm, dprobs, st);
 }
 
 int max_k_dprobs() { return kMaxKDprobs; }

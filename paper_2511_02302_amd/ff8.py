@@ -59,6 +59,8 @@ _SIGNATURES = {
     "ff8_quant_block128_e8m0": (_c_int, [_c_vp, _c_i64, _c_i64, _c_vp, _c_vp, _c_vp]),
     "ff8_permute_quant_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_int, _c_vp, _c_vp,
                                         _c_vp, _c_i64, _c_vp, _c_vp, _c_vp, _c_size, _c_int, _c_vp]),
+    "ff8_permute_quant_dprobs_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_vp, _c_vp,
+                                               _c_i64, _c_vp, _c_vp, _c_vp, _c_vp, _c_vp]),
     "ff8_scaling_aware_transpose_e8m0": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_vp, _c_int, _c_vp, _c_vp, _c_vp]),
     "ff8_scaling_aware_transpose_batch_e8m0": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_vp, _c_int, _c_vp,
                                                         _c_vp, _c_vp]),
@@ -239,11 +241,13 @@ def ff8_permute_quant_dprobs(dy, row_w, k, E, row_map, offsets, src_row, q, s, y
     _numel(row_w, T * k, "row_w"); _numel(row_map, T * k, "row_map"); _numel(dprobs, T * k, "dprobs")
     _numel(offsets, E + 1, "offsets"); _numel(src_row, M_cap, "src_row")
     _shape(q, (M_cap, H), "q"); _shape(s, (M_cap, H // 128), "s"); _shape(y_perm, (M_cap, H), "y_perm")
-    _check(load().ff8_permute_quant_dprobs(_ptr(dy, _bf16, "dy", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E,
-                                           _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
-                                           _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2),
-                                           _ptr(s, _f32, "s", 2), _ptr(y_perm, _bf16, "y_perm", 2),
-                                           _ptr(dprobs, _f32, "dprobs"), _stream(stream)), "ff8_permute_quant_dprobs")
+    sd, sfx = _scale_kind(s)
+    name = "ff8_permute_quant_dprobs" + sfx
+    _check(getattr(load(), name)(_ptr(dy, _bf16, "dy", 2), _ptr(row_w, _f32, "row_w"), T, H, k, E,
+                                 _ptr(row_map, _i32, "row_map"), _ptr(offsets, _i32, "offsets"),
+                                 _ptr(src_row, _i32, "src_row"), M_cap, _ptr(q, _u8, "q", 2), _ptr(s, sd, "s", 2),
+                                 _ptr(y_perm, _bf16, "y_perm", 2), _ptr(dprobs, _f32, "dprobs"), _stream(stream)),
+           name)
 
 
 def ff8_scaling_aware_transpose(q, s, qT, sT, offsets=None, E=0, stream=None):

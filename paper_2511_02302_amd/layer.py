@@ -36,8 +36,7 @@ of 128.
 
 scale_fmt="e8m0" stores every scale tensor as UE8M0 bytes (T + 127 for the scale 2^T; the
 format section 2.1 names) instead of float32: a quarter of the scale bytes, and bit-identical
-FP8 tensors and outputs.  It needs H and I to be multiples of 512 and is not combined with the
-router gradient.
+FP8 tensors and outputs.  It needs H and I to be multiples of 512.
 """
 
 from dataclasses import dataclass
@@ -118,8 +117,8 @@ class ExpertLayerFP8:
         self.router_grad = router_grad
         if scale_fmt not in SCALE_DTYPES:
             raise ValueError(f"scale_fmt must be one of {sorted(SCALE_DTYPES)}")
-        if scale_fmt == "e8m0" and (H % 512 or I % 512 or router_grad):
-            raise ValueError("UE8M0 scales need H and I multiples of 512, without the router gradient")
+        if scale_fmt == "e8m0" and (H % 512 or I % 512):
+            raise ValueError("UE8M0 scales need H and I multiples of 512")
         self.scale_fmt = scale_fmt
         sdt = SCALE_DTYPES[scale_fmt]
         self.device = dev = torch.device(device)

@@ -102,27 +102,28 @@ def test_gemms_e8m0_match_f32():
     assert not bool(dw8[1].any())  # the expert without rows gets zeros
 
 
-@pytest.mark.parametrize("case", ["uniform", "skewed_align16_fp8_checkpoint"])
+@pytest.mark.parametrize("case", ["uniform", "skewed_align16_fp8_checkpoint", "uniform_router_grad"])
 def test_layer_step_e8m0_equals_f32(case):
     """The whole step (F0..B8) with every scale tensor in UE8M0 against the same step with
-    float32 scales: every FP8 tensor, routing map and output bit-identical, every scale byte the
-    oracle's conversion of the float32 scale."""
-    if case == "uniform":
+    float32 scales: every FP8 tensor, routing map and output (and the router gradient)
+    bit-identical, every scale byte the oracle's conversion of the float32 scale."""
+    rg = case == "uniform_router_grad"
+    if case.startswith("uniform"):
         shape, align, ckpt = workloads.LayerShape("e8m0 T700 H1024 E8 k4 I512", 700, 1024, 8, 4, 512, "iid"), 128, False
     else:
         shape, align, ckpt = workloads.LayerShape("e8m0 skew T600 H512 E6 k2 I1024", 600, 512, 6, 2, 1024,
                                                   "zipf"), 16, True
     d = workloads.layer_inputs(shape, seed=7, device="cuda")
     args = (shape.T, shape.H, shape.E, shape.k, shape.I)
-    L = ExpertLayerFP8(*args, align=align, fp8_checkpoint=ckpt)
-    L8 = ExpertLayerFP8(*args, align=align, fp8_checkpoint=ckpt, scale_fmt="e8m0")
+    L = ExpertLayerFP8(*args, align=align, fp8_checkpoint=ckpt, router_grad=rg)
+    L8 = ExpertLayerFP8(*args, align=align, fp8_checkpoint=ckpt, router_grad=rg, scale_fmt="e8m0")
     for layer in (L, L8):
         layer.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
     b, b8 = L.buf, L8.buf
     m_pad = int(b["offsets"][-1].item())
     nb = -(-m_pad // 128)
-    same = ["row_map", "offsets", "w1q", "w2q", "y", "dx", "dw1", "dw2"]
+    same = ["row_map", "offsets", "w1q", "w2q", "y", "dx", "dw1", "dw2"] + (["dprobs"] if rg else [])
     rows = ["xq", "hq", "dyq", "daq", "a" if not ckpt else "aq", "dh", "dx_perm"]
     for n in same:
         assert torch.equal(b[n].view(torch.uint8), b8[n].view(torch.uint8)), n
