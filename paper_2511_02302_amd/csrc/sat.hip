@@ -15,7 +15,9 @@
 //   1. up front, the row scales of both blocks give every row's exponent (to LDS) and each
 //      block's S_max (wave DPP max + LDS);
 //   2. both blocks' data are loaded before the first barrier: lane (bl, sr, sc) holds 8 rows x
-//      16 bytes of block bl (16-byte non-temporal loads, 8 lanes per 128-byte row segment);
+//      16 bytes of block bl (16-byte non-temporal loads); the 16 lanes of both blocks' 128-byte
+//      pieces of a row are consecutive, so a load instruction reads 4 rows x 256 bytes (1-2%
+//      faster than 8 rows x 128 bytes of one block);
 //   3. rows with k_i = log2(S_max) - log2(s_i) > 0 are re-expressed at S_max: decode (exact),
 //      multiply by 2^-k (exact), hardware RNE encode -- equal to lowering the exponent field
 //      by k_i while it stays >= 1, and the nearest-even subnormal below;
@@ -159,17 +161,18 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const SatJobs<S> jobs, in
   }
 
   // 2.-4. both blocks loaded before the barrier, then shifted, transposed and staged
-  // lane (bl, sr, sc): rows 8 sr.. of block bl, 16 bytes from 16 sc
-  const int sr = (tid >> 3) & 15, sc = tid & 7;
+  // lane (db, sr, sc) = (bit 3, bits 4-7, bits 0-2 of tid): rows 8 sr.. of block db, 16 bytes
+  // from 16 sc
+  const int db = (tid >> 3) & 1, sr = tid >> 4, sc = tid & 7;
   u32x4 v[8];
-  if (bl < n_valid) {
-    const uint8_t* src = q + (r0 + sr * 8) * cols + (int64_t)(cb0 + bl) * kTile + sc * 16;
+  if (db < n_valid) {
+    const uint8_t* src = q + (r0 + sr * 8) * cols + (int64_t)(cb0 + db) * kTile + sc * 16;
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = ldnt16(src + (int64_t)i * cols);
   }
   __syncthreads();
-  if (bl < n_valid) {
-    const int t_max = (int)max(wmax[bl][0], wmax[bl][1]) - 256;
+  if (db < n_valid) {
+    const int t_max = (int)max(wmax[db][0], wmax[db][1]) - 256;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {  // the two 8-byte column halves
       uint32_t w0[8], w1[8];
@@ -178,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void sat_kernel(const SatJobs<S> jobs, in
         w0[i] = v[i][2 * h];
         w1[i] = v[i][2 * h + 1];
       }
-      shift_transpose_store<RB>(w0, w1, &t_rows[bl][sr * 8], t_max, tile, sc * 16 + 8 * h, bl, sr);
+      shift_transpose_store<RB>(w0, w1, &t_rows[db][sr * 8], t_max, tile, sc * 16 + 8 * h, db, sr);
     }
   }
   __syncthreads();
