@@ -81,6 +81,17 @@ def stage_costs(shape, M):
     return c
 
 
+def forward_only(costs, st_ms, shape):
+    """The forward alone (F1..F5: permute+quant, fc1, SwiGLU+quant, fc2, unpermute), from the per-stage
+    event times of the same timed steps; the weight quantization F0 is reported beside it."""
+    fwd = ["F1_permute_quant", "F2_fc1_fprop", "F3_swiglu_quant", "F4_fc2_fprop", "F5_unpermute"]
+    ms = sum(st_ms[n] for n in fwd)
+    flops = sum(costs[n][1] for n in fwd if costs[n][0] == "mfma")
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"workload": f"{shape.name} expert-layer forward F1..F5", "ms": round(ms, 4), "TFLOP/s": round(tf, 1),
+            "frac_mfma": round(tf / FP8_PEAK_TFLOPS, 4), "ms_with_weight_quant": round(ms + st_ms["F0_weight_quant"], 4)}
+
+
 class StageTimer:
     """HIP events recorded on the launch stream between stages."""
 
@@ -707,6 +718,7 @@ def main():
                       "ms": round(gemm_ms, 3)},
         "roofline": roof,
         "stages": stages,
+        "forward_only": forward_only(costs, st_ms, shape),
     }
     if not args.no_fp8_checkpoint:
         rec["fp8_checkpoint"] = fp8_checkpoint(torch, L, d, shape, M, args.steps, args.warmup, ms_step)
