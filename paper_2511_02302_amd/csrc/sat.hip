@@ -14,8 +14,8 @@
 // and write consecutive stretches of one slab.
 //   1. up front, the row scales of both blocks give every row's exponent (to LDS) and each
 //      block's S_max (wave DPP max + LDS);
-//   2. both blocks' data are loaded before the first barrier: lane (bl, sr, sc) holds 8 rows x
-//      16 bytes of block bl (16-byte non-temporal loads); the 16 lanes of both blocks' 128-byte
+//   2. both blocks' data are loaded before the first barrier: lane (db, sr, sc) holds 8 rows x
+//      16 bytes of block db (16-byte non-temporal loads); the 16 lanes of both blocks' 128-byte
 //      pieces of a row are consecutive, so a load instruction reads 4 rows x 256 bytes (1-2%
 //      faster than 8 rows x 128 bytes of one block);
 //   3. rows with k_i = log2(S_max) - log2(s_i) > 0 are re-expressed at S_max: decode (exact),
