@@ -45,7 +45,7 @@ def run(request):
     L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
     torch.cuda.synchronize()
     _, off, row_map, src_row = moe.route(host(d["topk_idx"]), shape.E, align)
-    yield {"shape": shape, "d": d, "b": L.buf, "off": off.astype(np.int64), "row_map": row_map,
+    yield {"shape": shape, "d": d, "b": L.buf, "L": L, "off": off.astype(np.int64), "row_map": row_map,
            "src_row": src_row, "rng": np.random.default_rng(zlib.crc32(request.param.encode()))}
     del L, d
     torch.cuda.empty_cache()
@@ -350,3 +350,20 @@ def test_sat_sampled_blocks(run):
             wqT, wsT = sat.scaling_aware_transpose(host(q[rs]), host(s[rs]), r1 - rb * 128)
             assert np.array_equal(host(qT[rb])[:, :r1 - rb * 128], wqT), (name, rb)  # block rb's slab
             assert np.array_equal(host(sT[rb:rb + 1]).T, wsT), (name, rb)
+
+
+def test_step_is_reproducible(run):
+    """A second step on the same inputs writes bit-identical routing maps, FP8 tensors and
+    outputs: every reduction (GEMM K order, tile amax, unpermute slot sum, routing ranks) has a
+    fixed order.  Runs last in the module, since it re-runs the step in the buffers the other
+    tests read (which it leaves identical when it passes)."""
+    b, d, L = run["b"], run["d"], run["L"]
+    names = ["row_map", "offsets", "xq", "xs", "a", "hq", "hs", "y_perm", "y", "dyq", "dh", "daq", "das", "dx",
+             "dw1", "dw2"]
+    first = {n: b[n].clone() for n in names}
+    L.step(d["x"], d["topk_idx"], d["probs"], d["dy"], d["w1"], d["w2"])
+    torch.cuda.synchronize()
+    after = L.buf
+    for n in names:
+        assert torch.equal(first[n].view(torch.uint8), after[n].view(torch.uint8)), n
+
